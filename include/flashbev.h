@@ -1,0 +1,156 @@
+/*
+ * flashbev.h -- C ABI of the fused Sampling-VT forward for AMD MI355X (gfx950).
+ *
+ * The operation (FlashBEV paper, Sec. 3.1, Eq. 1): for every batch element
+ * b, BEV cell (x, y) and channel c,
+ *
+ *   out[b,c,x,y] = sum_z ( sum_n M_n(x,y,z) f_n(x,y,z,c) ) / max(1, sum_n M_n(x,y,z))
+ *
+ * where M_n = 1 when the voxel centre projected through camera n's matrix
+ * has positive depth and lands inside camera n's image, and f_n is the
+ * bilinear sample of camera n's feature map at that pixel.  The operator is
+ * evaluated in one fused pass that never materializes the camera- and
+ * height-expanded B x N x C x X x Y x Z tensor (Sec. 3.3, Alg. 2); its only
+ * device memory is the caller's inputs and output.
+ *
+ * Conventions fixed by this library where the paper leaves them open:
+ *   - voxel centres: x = x_min + (i + 1/2) dx, y = y_min + (j + 1/2) dy,
+ *     heights taken from z_bins (bin centres chosen by the caller);
+ *   - projection: (u', v', d) = lidar2img[b,n][0:3] . (x, y, z, 1), pixel
+ *     (u, v) = (u'/d, v'/d); coordinates are float32 with every product
+ *     and sum rounded on its own and IEEE division;
+ *   - valid iff d > depth_eps and 0 <= u < img_w and 0 <= v < img_h;
+ *   - feature coordinates x_f = u * (W / img_w) - 1/2 (align_corners=False),
+ *     likewise y_f; taps outside the map contribute zero but the sample still
+ *     counts in the per-height denominator;
+ *   - accumulation in float32 for every input type; the output is float32.
+ *
+ * Thread safety: the library keeps no state; calls are asynchronous on the
+ * given stream and may be issued from several threads.  It never allocates
+ * device or host memory, never prints and never aborts.
+ */
+#ifndef FLASHBEV_H
+#define FLASHBEV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FLASHBEV_ABI_VERSION 1
+/* Largest number of height bins per call (heights travel as kernel
+ * arguments, so they cost no device memory). */
+#define FLASHBEV_ZMAX 256
+/* Largest number of cameras per batch element. */
+#define FLASHBEV_NMAX 64
+/* Largest feature row (C times the element size) in bytes. */
+#define FLASHBEV_ROW_BYTES_MAX 4096
+
+/* Status codes.  Every argument check runs before any HIP call. */
+typedef enum {
+    FLASHBEV_OK = 0,
+    FLASHBEV_ERR_NULLPTR = -1,     /* a required pointer is NULL                 */
+    FLASHBEV_ERR_SHAPE = -2,       /* a dimension is negative or zero where >= 1 is needed */
+    FLASHBEV_ERR_DTYPE = -3,       /* unknown feature dtype                      */
+    FLASHBEV_ERR_ALIGN = -4,       /* a device pointer is not element-aligned    */
+    FLASHBEV_ERR_UNSUPPORTED = -5, /* beyond a documented limit (Z, N, row, 2 GiB) */
+    FLASHBEV_ERR_ALIAS = -6,       /* out overlaps an input                      */
+    FLASHBEV_ERR_VALUE = -7,       /* non-finite grid spec or bad reduce mode    */
+    FLASHBEV_ERR_HIP = -8          /* the kernel launch failed                   */
+} flashbev_status;
+
+/* Feature element type; accumulation is float32 for all of them. */
+typedef enum {
+    FLASHBEV_F32 = 0,
+    FLASHBEV_F16 = 1,
+    FLASHBEV_BF16 = 2
+} flashbev_dtype;
+
+/* Reduction over cameras at each height (Eq. 1 uses the valid mean). */
+typedef enum {
+    FLASHBEV_REDUCE_VALID_MEAN = 0, /* num_z / max(1, den_z), Eq. 1 (default) */
+    FLASHBEV_REDUCE_SUM = 1         /* num_z: plain masked sum over cameras   */
+} flashbev_reduce;
+
+/* Camera feature maps F_n (Sec. 3.1): device memory, channel-last and
+ * contiguous, [B, N, H, W, C] in `dtype`, aligned to the element size.
+ * img_h x img_w is the image that lidar2img projects into; the feature map
+ * covers it with scale W / img_w horizontally and H / img_h vertically.
+ * The whole tensor must be smaller than 2 GiB and C * sizeof(dtype) at most
+ * FLASHBEV_ROW_BYTES_MAX.  Values must be finite. */
+typedef struct {
+    const void *data;
+    int32_t dtype;                  /* flashbev_dtype */
+    int32_t B, N, H, W, C;
+    int32_t img_h, img_w;
+} flashbev_features;
+
+/* BEV grid in the ego/lidar frame: X cells along x starting at x_min with
+ * pitch dx, Y cells along y starting at y_min with pitch dy; cell (i, j)
+ * has centre (x_min + (i + 1/2) dx, y_min + (j + 1/2) dy).  A sample is
+ * valid only if its depth exceeds depth_eps (use 1e-5). */
+typedef struct {
+    float x_min, dx;
+    int32_t X;
+    float y_min, dy;
+    int32_t Y;
+    float depth_eps;
+    int32_t reduce;                 /* flashbev_reduce */
+} flashbev_bev_grid_spec;
+
+/* Height bins: a HOST array of Z heights in metres (0 <= Z <= FLASHBEV_ZMAX),
+ * read during the call only. */
+typedef struct {
+    const float *z;
+    int32_t Z;
+} flashbev_z_bins;
+
+/*
+ * Fused Sampling-VT forward (Eq. 1; Sec. 3.3, Alg. 2).
+ *
+ *   features   feature maps and image size (see flashbev_features).
+ *   lidar2img  device, [B, N, 4, 4] float32 row-major, 4-byte aligned; the
+ *              paper's (B, N, 3, 4) projection matrices are rows 0..2 and
+ *              row 3 is ignored.
+ *   spec       BEV grid, depth threshold and reduction mode.
+ *   z_bins     heights (host memory).
+ *   out        device, [B, C, X, Y] float32, caller-allocated, 4-byte
+ *              aligned, must not overlap features or lidar2img.  Every
+ *              element is written exactly once (cells no camera sees get
+ *              +0.0), so it needs no zeroing beforehand.
+ *   stream     hipStream_t to launch on; NULL means the default stream.
+ *
+ * Returns FLASHBEV_OK once the work is enqueued (it completes
+ * asynchronously), or a negative flashbev_status.  Argument errors are
+ * reported before any HIP call; a failed launch returns FLASHBEV_ERR_HIP.
+ * An empty output (B, C, X or Y zero) enqueues nothing and returns OK.
+ */
+int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img,
+                       const flashbev_bev_grid_spec *spec, const flashbev_z_bins *z_bins,
+                       float *out, void *stream);
+
+/* Static, human-readable text for a status code (never NULL). */
+const char *flashbev_status_string(int status);
+
+/* FLASHBEV_ABI_VERSION of the built library. */
+int flashbev_abi_version(void);
+
+/*
+ * Launch geometry the library would use for these arguments, for tools that
+ * report per-launch figures.  On success writes the workgroup count, the
+ * threads per workgroup, the dynamic LDS bytes per workgroup, the BEV cells
+ * per wavefront and the lanes per cell.  Performs the same argument checks
+ * as flashbev_sample_vt (pointers to device data are not dereferenced and
+ * may be NULL here) and makes no HIP call.
+ */
+int flashbev_launch_info(const flashbev_features *features, const flashbev_bev_grid_spec *spec,
+                         const flashbev_z_bins *z_bins, int64_t *workgroups,
+                         int32_t *threads_per_workgroup, int32_t *lds_bytes,
+                         int32_t *cells_per_wave, int32_t *lanes_per_cell);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHBEV_H */

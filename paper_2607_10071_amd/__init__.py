@@ -1,0 +1,220 @@
+"""Fused Sampling-VT forward (FlashBEV) for AMD MI355X.
+
+A thin Python binding over the C ABI of ``include/flashbev.h``
+(``libflashbev.so``).  It only marshals arguments: every step of the
+operator runs in the library's HIP kernel.  PyTorch supplies device memory
+and the current stream.  If the built library is missing the calls raise;
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional, Sequence, Tuple
+
+__all__ = [
+    "BevGrid", "sample_vt", "launch_info", "status_string", "abi_version", "library_path",
+    "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libflashbev.so")
+_LIB = None
+
+DTYPE_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+REDUCE_CODES = {"mean": 0, "sum": 1}
+STATUS = {
+    "OK": 0, "ERR_NULLPTR": -1, "ERR_SHAPE": -2, "ERR_DTYPE": -3, "ERR_ALIGN": -4,
+    "ERR_UNSUPPORTED": -5, "ERR_ALIAS": -6, "ERR_VALUE": -7, "ERR_HIP": -8,
+}
+ZMAX = 256
+NMAX = 64
+ROW_BYTES_MAX = 4096
+
+
+class FlashBevError(RuntimeError):
+    def __init__(self, status: int, what: str = "flashbev_sample_vt"):
+        self.status = status
+        super().__init__(f"{what} failed: {status} ({status_string(status)})")
+
+
+class Features(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32),
+                ("B", ctypes.c_int32), ("N", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("W", ctypes.c_int32), ("C", ctypes.c_int32),
+                ("img_h", ctypes.c_int32), ("img_w", ctypes.c_int32)]
+
+
+class GridSpec(ctypes.Structure):
+    _fields_ = [("x_min", ctypes.c_float), ("dx", ctypes.c_float), ("X", ctypes.c_int32),
+                ("y_min", ctypes.c_float), ("dy", ctypes.c_float), ("Y", ctypes.c_int32),
+                ("depth_eps", ctypes.c_float), ("reduce", ctypes.c_int32)]
+
+
+class ZBins(ctypes.Structure):
+    _fields_ = [("z", ctypes.POINTER(ctypes.c_float)), ("Z", ctypes.c_int32)]
+
+
+@dataclasses.dataclass(frozen=True)
+class BevGrid:
+    """BEV grid: X cells from x_min with pitch dx, Y cells from y_min with pitch dy."""
+
+    x_min: float
+    dx: float
+    X: int
+    y_min: float
+    dy: float
+    Y: int
+    depth_eps: float = 1e-5
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_LIB_PATH):
+            raise FileNotFoundError(
+                f"{_LIB_PATH} is not built; run `python -m paper_2607_10071_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.POINTER
+        L.flashbev_sample_vt.argtypes = [P(Features), ctypes.c_void_p, P(GridSpec), P(ZBins),
+                                         ctypes.c_void_p, ctypes.c_void_p]
+        L.flashbev_sample_vt.restype = ctypes.c_int
+        L.flashbev_status_string.argtypes = [ctypes.c_int]
+        L.flashbev_status_string.restype = ctypes.c_char_p
+        L.flashbev_abi_version.argtypes = []
+        L.flashbev_abi_version.restype = ctypes.c_int
+        L.flashbev_launch_info.argtypes = [P(Features), P(GridSpec), P(ZBins),
+                                           P(ctypes.c_int64), P(ctypes.c_int32),
+                                           P(ctypes.c_int32), P(ctypes.c_int32),
+                                           P(ctypes.c_int32)]
+        L.flashbev_launch_info.restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return _lib().flashbev_status_string(int(status)).decode()
+
+
+def abi_version() -> int:
+    return int(_lib().flashbev_abi_version())
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    m = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported feature dtype {t.dtype}")
+    return DTYPE_CODES[m[t.dtype]]
+
+
+def _z_array(z_bins):
+    import numpy as np
+
+    if hasattr(z_bins, "detach"):
+        z_bins = z_bins.detach().cpu().numpy()
+    z = np.ascontiguousarray(np.asarray(z_bins, dtype=np.float32).reshape(-1))
+    return z
+
+
+def _structs(features_shape, dtype_code, data_ptr, img_hw, grid: BevGrid, z, reduce):
+    B, N, H, W, C = features_shape
+    f = Features(data_ptr, dtype_code, B, N, H, W, C, int(img_hw[0]), int(img_hw[1]))
+    g = GridSpec(grid.x_min, grid.dx, grid.X, grid.y_min, grid.dy, grid.Y, grid.depth_eps,
+                 REDUCE_CODES[reduce])
+    zb = ZBins(z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(z))
+    return f, g, zb
+
+
+def sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int],
+              out=None, reduce: str = "mean", stream=None):
+    """Fused Sampling-VT forward (Eq. 1) on the GPU.
+
+    features   CUDA tensor [B, N, H, W, C] (float32, float16 or bfloat16),
+               contiguous channel-last feature maps.
+    lidar2img  CUDA float32 tensor [B, N, 4, 4].
+    z_bins     heights in metres (host sequence, numpy array or tensor).
+    grid       BevGrid.
+    img_hw     (img_h, img_w) of the image lidar2img projects into.
+    out        optional CUDA float32 tensor [B, C, X, Y] to write into.
+    reduce     "mean" (Eq. 1, per-height valid mean) or "sum".
+    stream     torch.cuda.Stream or raw hipStream_t int; defaults to the
+               current stream.
+
+    Returns ``out`` ([B, C, X, Y] float32).  The call is asynchronous.
+    """
+    import torch
+
+    if features.dim() != 5:
+        raise ValueError("features must be [B, N, H, W, C]")
+    if not features.is_cuda or not lidar2img.is_cuda:
+        raise ValueError("features and lidar2img must be device tensors")
+    if not features.is_contiguous():
+        raise ValueError("features must be contiguous (channel-last NHWC)")
+    if lidar2img.dtype != torch.float32 or not lidar2img.is_contiguous():
+        raise ValueError("lidar2img must be a contiguous float32 tensor")
+    B, N, H, W, C = features.shape
+    if tuple(lidar2img.shape) != (B, N, 4, 4):
+        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
+    if out is None:
+        out = torch.empty((B, C, grid.X, grid.Y), dtype=torch.float32, device=features.device)
+    else:
+        if out.dtype != torch.float32 or not out.is_contiguous() or \
+                tuple(out.shape) != (B, C, grid.X, grid.Y):
+            raise ValueError(f"out must be a contiguous float32 tensor [{B}, {C}, {grid.X}, {grid.Y}]")
+    z = _z_array(z_bins)
+    f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
+                        grid, z, reduce)
+    if stream is None:
+        s = torch.cuda.current_stream(features.device).cuda_stream
+    elif isinstance(stream, int):
+        s = stream
+    else:
+        s = stream.cuda_stream
+    rc = _lib().flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
+                                   ctypes.byref(g), ctypes.byref(zb),
+                                   ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
+    if rc != 0:
+        raise FlashBevError(rc)
+    return out
+
+
+def sample_vt_raw(features_ptr: int, dtype: str, shape, lidar2img_ptr: int, z_bins,
+                  grid: BevGrid, img_hw, out_ptr: int, reduce: str = "mean",
+                  stream: int = 0) -> int:
+    """The C entry point with raw device addresses; returns the status code."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], features_ptr, img_hw, grid, z, reduce)
+    return int(_lib().flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr),
+                                         ctypes.byref(g), ctypes.byref(zb),
+                                         ctypes.c_void_p(out_ptr), ctypes.c_void_p(stream)))
+
+
+def launch_info(shape, dtype: str, z_bins, grid: BevGrid, img_hw, reduce: str = "mean",
+                data_ptr: int = 0) -> dict:
+    """Launch geometry for these arguments (no HIP call)."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], data_ptr, img_hw, grid, z, reduce)
+    wg = ctypes.c_int64()
+    thr = ctypes.c_int32()
+    lds = ctypes.c_int32()
+    cpw = ctypes.c_int32()
+    lpc = ctypes.c_int32()
+    rc = _lib().flashbev_launch_info(ctypes.byref(f), ctypes.byref(g), ctypes.byref(zb),
+                                     ctypes.byref(wg), ctypes.byref(thr), ctypes.byref(lds),
+                                     ctypes.byref(cpw), ctypes.byref(lpc))
+    if rc != 0:
+        raise FlashBevError(rc, "flashbev_launch_info")
+    return {"workgroups": wg.value, "threads": thr.value, "lds_bytes": lds.value,
+            "cells_per_wave": cpw.value, "lanes_per_cell": lpc.value}
+
+
+def grid_of(wl) -> BevGrid:
+    """BevGrid of a workload description with x_min/dx/X/y_min/dy/Y fields."""
+    return BevGrid(wl.x_min, wl.dx, wl.X, wl.y_min, wl.dy, wl.Y, wl.depth_eps)

@@ -1,0 +1,168 @@
+"""C-ABI library: exported symbols and argument checks (CPU only).
+
+Every argument check of flashbev_sample_vt runs before any HIP call, so the
+error paths are exercised here without a GPU.  Device pointers below are
+fake addresses that the library never dereferences because validation
+rejects the call first.
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2607_10071_amd as fb
+from paper_2607_10071_amd import Features, GridSpec, ZBins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashbev.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(flashbev_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"flashbev_sample_vt", "flashbev_status_string", "flashbev_abi_version",
+            "flashbev_launch_info"} <= set(names)
+    lib = ctypes.CDLL(fb.library_path())
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", fb.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (flashbev_\w+)", out))
+    assert set(names) <= exported
+    # nothing else with the prefix leaks out
+    assert exported <= set(names)
+
+
+def test_abi_version_and_status_strings():
+    assert fb.abi_version() == 1
+    for name, code in fb.STATUS.items():
+        s = fb.status_string(code)
+        assert s and s != "unknown status"
+    assert fb.status_string(12345) == "unknown status"
+
+
+def test_header_constants_match_binding():
+    src = open(HEADER).read()
+    for k, v in (("FLASHBEV_ZMAX", fb.ZMAX), ("FLASHBEV_NMAX", fb.NMAX),
+                 ("FLASHBEV_ROW_BYTES_MAX", fb.ROW_BYTES_MAX), ("FLASHBEV_ABI_VERSION", 1)):
+        assert re.search(rf"#define {k} {v}\b", src), k
+    for k, v in fb.STATUS.items():
+        assert re.search(rf"FLASHBEV_{k} = {v}\b", src), k
+
+
+FEAT = 0x7F0000000000  # fake, 256-byte aligned device addresses
+L2I = 0x7F1000000000
+OUT = 0x7F2000000000
+
+
+def call(shape=(1, 6, 32, 88, 80), dtype="f32", img=(256, 704), X=200, Y=200, z=None,
+         reduce="mean", feat=FEAT, l2i=L2I, out=OUT, grid=None, zptr_null=False, Z=None):
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32) if z is None else np.asarray(z, np.float32)
+    B, N, H, W, C = shape
+    f = Features(feat, fb.DTYPE_CODES.get(dtype, dtype) if isinstance(dtype, str) else dtype,
+                 B, N, H, W, C, img[0], img[1])
+    g = grid or GridSpec(-50.0, 0.5, X, -50.0, 0.5, Y, 1e-5, fb.REDUCE_CODES.get(reduce, reduce)
+                         if isinstance(reduce, str) else reduce)
+    zb = ZBins(None if zptr_null else z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+               len(z) if Z is None else Z)
+    lib = fb._lib()
+    return lib.flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(l2i), ctypes.byref(g),
+                                  ctypes.byref(zb), ctypes.c_void_p(out), ctypes.c_void_p(0))
+
+
+S = fb.STATUS
+
+
+def test_null_structs():
+    lib = fb._lib()
+    g = GridSpec(-50.0, 0.5, 4, -50.0, 0.5, 4, 1e-5, 0)
+    z = np.zeros(2, np.float32)
+    zb = ZBins(z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), 2)
+    f = Features(FEAT, 0, 1, 1, 2, 2, 4, 8, 8)
+    assert lib.flashbev_sample_vt(None, ctypes.c_void_p(L2I), ctypes.byref(g), ctypes.byref(zb),
+                                  ctypes.c_void_p(OUT), None) == S["ERR_NULLPTR"]
+    assert lib.flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(L2I), None, ctypes.byref(zb),
+                                  ctypes.c_void_p(OUT), None) == S["ERR_NULLPTR"]
+    assert lib.flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(L2I), ctypes.byref(g), None,
+                                  ctypes.c_void_p(OUT), None) == S["ERR_NULLPTR"]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(out=0), "ERR_NULLPTR"),
+    (dict(feat=0), "ERR_NULLPTR"),
+    (dict(l2i=0), "ERR_NULLPTR"),
+    (dict(zptr_null=True), "ERR_NULLPTR"),
+    (dict(dtype=7), "ERR_DTYPE"),
+    (dict(dtype=-1), "ERR_DTYPE"),
+    (dict(shape=(1, 6, 32, 88, 0)), "ERR_SHAPE"),
+    (dict(shape=(-1, 6, 32, 88, 8)), "ERR_SHAPE"),
+    (dict(shape=(1, -6, 32, 88, 8)), "ERR_SHAPE"),
+    (dict(shape=(1, 6, 0, 88, 8)), "ERR_SHAPE"),
+    (dict(shape=(1, 6, 32, 0, 8)), "ERR_SHAPE"),
+    (dict(img=(0, 704)), "ERR_SHAPE"),
+    (dict(img=(256, -1)), "ERR_SHAPE"),
+    (dict(X=-1), "ERR_SHAPE"),
+    (dict(Y=-3), "ERR_SHAPE"),
+    (dict(Z=-1), "ERR_SHAPE"),
+    (dict(z=np.zeros(257)), "ERR_UNSUPPORTED"),
+    (dict(shape=(1, 65, 32, 88, 8)), "ERR_UNSUPPORTED"),
+    (dict(shape=(1, 6, 32, 88, 1025)), "ERR_UNSUPPORTED"),
+    (dict(shape=(1, 6, 32, 88, 2049), dtype="bf16"), "ERR_UNSUPPORTED"),
+    (dict(shape=(64, 64, 128, 128, 64)), "ERR_UNSUPPORTED"),  # 17 GB of features
+    (dict(shape=(1, 64, 128, 256, 256)), "ERR_UNSUPPORTED"),  # 2.1 GB of features
+    (dict(X=50000, Y=50000), "ERR_UNSUPPORTED"),
+    (dict(reduce=2), "ERR_VALUE"),
+    (dict(grid=GridSpec(float("nan"), 0.5, 4, -1.0, 0.5, 4, 1e-5, 0)), "ERR_VALUE"),
+    (dict(grid=GridSpec(-1.0, float("inf"), 4, -1.0, 0.5, 4, 1e-5, 0)), "ERR_VALUE"),
+    (dict(grid=GridSpec(-1.0, 0.5, 4, -1.0, 0.5, 4, float("nan"), 0)), "ERR_VALUE"),
+    (dict(feat=FEAT + 2), "ERR_ALIGN"),
+    (dict(feat=FEAT + 1, dtype="bf16"), "ERR_ALIGN"),
+    (dict(l2i=L2I + 2), "ERR_ALIGN"),
+    (dict(out=OUT + 1), "ERR_ALIGN"),
+    (dict(out=FEAT + 64), "ERR_ALIAS"),
+    (dict(out=FEAT - 1024), "ERR_ALIAS"),
+    (dict(out=L2I - 4), "ERR_ALIAS"),
+])
+def test_argument_errors_before_any_hip_call(kw, status):
+    assert call(**kw) == S[status]
+
+
+def test_empty_outputs_enqueue_nothing():
+    # nothing to write: returns OK without touching HIP (this box has no GPU)
+    assert call(X=0) == S["OK"]
+    assert call(Y=0) == S["OK"]
+    assert call(shape=(0, 6, 32, 88, 80)) == S["OK"]
+    assert call(X=0, out=0, feat=0, l2i=0) == S["OK"]
+
+
+def test_launch_info_geometry():
+    for dtype, C, cpw, lpc in (("f32", 80, 3, 20), ("bf16", 128, 4, 16), ("f16", 64, 8, 8),
+                               ("bf16", 64, 8, 8), ("f32", 32, 8, 8), ("f32", 4, 8, 1),
+                               ("f32", 136, 1, 34), ("f32", 1024, 1, 64), ("bf16", 5, 8, 5)):
+        info = fb.launch_info((1, 6, 32, 88, C), dtype, np.zeros(8), fb.BevGrid(-50, .5, 200, -50, .5, 200),
+                              (256, 704))
+        assert info["cells_per_wave"] == cpw and info["lanes_per_cell"] == lpc, (dtype, C, info)
+        assert info["threads"] == 256
+        cells_per_wg = 4 * cpw
+        assert info["workgroups"] == math.ceil(40000 / cells_per_wg)
+        assert info["lds_bytes"] <= 64 * 1024
+    with pytest.raises(fb.FlashBevError):
+        fb.launch_info((1, 6, 32, 88, 80), "f32", np.zeros(300), fb.BevGrid(-50, .5, 200, -50, .5, 200),
+                       (256, 704))
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    f = torch.zeros(1, 1, 2, 2, 4)
+    m = torch.zeros(1, 1, 4, 4)
+    with pytest.raises(ValueError):
+        fb.sample_vt(f, m, [0.0], fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8))

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP library against the CPU oracle, element by element.
+
+Bar (per output element): |gpu - oracle| <= rtol * S, where S is the
+oracle's magnitude scale (sum of |weighted terms| divided by the per-height
+camera count, S >= |oracle|); rtol = 1e-5 for float32 features and 2e-3 for
+float16/bfloat16 features.  Where S = 0 the GPU must give exactly 0.  All
+calls go through the C ABI via the thin binding.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f32": 1e-5, "f16": 2e-3, "bf16": 2e-3}
+
+
+@pytest.fixture(scope="module")
+def fb():
+    import paper_2607_10071_amd as m
+    return m
+
+
+def to_dev(inst, device):
+    import torch
+    ft = synth.to_storage(inst.features, inst.wl.dtype).to(device)
+    l2i = torch.from_numpy(np.ascontiguousarray(inst.lidar2img)).to(device)
+    return ft, l2i
+
+
+def gpu_run(fb, inst, device, reduce="mean"):
+    import torch
+    wl = inst.wl
+    ft, l2i = to_dev(inst, device)
+    out = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w), reduce=reduce)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def stats(g, r, s):
+    g = g.astype(np.float64)
+    err = np.abs(g - r)
+    nz = s > 0
+    cos = float(np.dot(g.ravel(), r.ravel()) /
+                max(np.linalg.norm(g) * np.linalg.norm(r), 1e-300))
+    return {"max_abs": float(err.max(initial=0)), "mean_abs": float(err.mean()) if err.size else 0.0,
+            "max_scaled": float((err[nz] / s[nz]).max(initial=0)),
+            "mean_rel": float((err[nz] / np.maximum(np.abs(r[nz]), 1e-12)).mean()) if nz.any() else 0.0,
+            "cosine": cos}
+
+
+def assert_parity(g, r, s, rtol, what=""):
+    g = g.astype(np.float64)
+    err = np.abs(g - r)
+    bad = err > rtol * s
+    st = stats(g, r, s)
+    print(f"[parity] {what} {st}", flush=True)
+    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} elements off; {st}"
+
+
+def check_instance(fb, inst, device, reduce="mean", what=""):
+    print(f"[case] {what} shape={inst.features.shape} dtype={inst.wl.dtype} "
+          f"X={inst.wl.X} Y={inst.wl.Y} Z={len(inst.z)} reduce={reduce}", flush=True)
+    g = gpu_run(fb, inst, device, reduce)
+    r, s, cnt = oracle.run_instance(inst, reduce)
+    assert g.shape == r.shape
+    assert_parity(g, r, s, RTOL[inst.wl.dtype], what)
+    return g, r, s, cnt
+
+
+# ---------------------------------------------------------------------------
+# the benchmark workloads at full size (every Z of the height sweep)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("wl", synth.all_parity_workloads(), ids=lambda w: f"{w.name}-Z{w.Z}")
+def test_benchmark_workloads_full(fb, device, wl):
+    inst = synth.make_workload(wl)
+    g, r, s, cnt = check_instance(fb, inst, device, what=f"{wl.name} Z={wl.Z}")
+    assert cnt["valid_samples"] > 0.1 * wl.samples
+    # cells nobody sees are exactly +0.0
+    zero = s == 0
+    assert np.all(g[zero] == 0.0)
+
+
+def test_paper_reference_setting(fb, device):
+    check_instance(fb, synth.make_workload(synth.config("paper_ref")), device, what="paper_ref")
+
+
+@pytest.mark.parametrize("reduce", ["sum"])
+def test_sum_mode(fb, device, reduce):
+    check_instance(fb, synth.make_workload(synth.config("tiny")), device, reduce, "tiny sum")
+    check_instance(fb, synth.make_workload(synth.config("rep").with_(dtype="bf16", C=64)),
+                   device, reduce, "rep bf16 sum")
+
+
+# ---------------------------------------------------------------------------
+# ragged and edge shapes
+# ---------------------------------------------------------------------------
+def small(B=1, N=6, img=(256, 704), stride=16, C=32, dtype="f32", X=37, Y=29, half=25.0, Z=4,
+          cfg_id=50, z_lo=-5.0, z_hi=3.0):
+    wl = synth.Workload(name="edge", cfg_id=cfg_id, B=B, N=N, img_h=img[0], img_w=img[1],
+                        H=max(1, img[0] // stride), W=max(1, img[1] // stride), C=C, dtype=dtype,
+                        X=X, Y=Y, x_min=-half, dx=2 * half / X, y_min=-half, dy=2 * half / Y,
+                        z_lo=z_lo, z_hi=z_hi, Z=Z)
+    return synth.make_workload(wl)
+
+
+@pytest.mark.parametrize("dtype,C", [
+    ("f32", 4), ("f32", 20), ("f32", 80), ("f32", 136), ("f32", 3), ("f32", 6), ("f32", 300),
+    ("f32", 1024), ("bf16", 5), ("bf16", 12), ("bf16", 40), ("bf16", 128), ("bf16", 2048),
+    ("f16", 6), ("f16", 1), ("f16", 64), ("f16", 200),
+])
+def test_channel_counts_and_vector_widths(fb, device, dtype, C):
+    # covers 16/8/4/2-byte vectors, one to four vectors per lane, 1..8
+    # cells per wavefront, and the largest row (4096 bytes)
+    inst = small(C=C, dtype=dtype, cfg_id=60 + C % 17)
+    check_instance(fb, inst, device, what=f"C={C} {dtype}")
+
+
+@pytest.mark.parametrize("X,Y", [(1, 1), (1, 37), (53, 1), (7, 5), (64, 64), (65, 63)])
+def test_grid_shapes(fb, device, X, Y):
+    check_instance(fb, small(X=X, Y=Y, half=20.0), device, what=f"grid {X}x{Y}")
+
+
+def test_batch_with_distinct_rigs(fb, device):
+    inst = small(B=3, C=16, dtype="bf16", X=40, Y=33)
+    assert not np.array_equal(inst.lidar2img[0], inst.lidar2img[1])
+    check_instance(fb, inst, device, what="B=3")
+
+
+@pytest.mark.parametrize("N,Z", [(1, 1), (1, 8), (2, 3), (8, 64), (64, 3), (6, 256), (7, 9)])
+def test_camera_and_height_counts(fb, device, N, Z):
+    inst = small(N=N, Z=Z, C=8, X=24, Y=20, cfg_id=70 + N)
+    check_instance(fb, inst, device, what=f"N={N} Z={Z}")
+
+
+def test_tiny_feature_maps(fb, device):
+    # 1-pixel-wide and 1-pixel-high maps: both taps of an axis on one pixel
+    for img, stride in (((16, 704), 16), ((256, 16), 16), ((16, 16), 16), ((32, 48), 16)):
+        inst = small(img=img, stride=stride, C=8, X=30, Y=30)
+        check_instance(fb, inst, device, what=f"map {inst.wl.H}x{inst.wl.W}")
+
+
+def test_nobody_sees_anything(fb, device):
+    inst = small(C=8)
+    up = np.array([[1, 0, 0, 0], [0, 1, 0, 0], [0, 0, 1, -100], [0, 0, 0, 1]], np.float32)
+    inst.lidar2img = np.ascontiguousarray(np.broadcast_to(up, inst.lidar2img.shape))
+    g = gpu_run(fb, inst, device)
+    assert np.all(g == 0.0) and not np.any(np.signbit(g))
+
+
+def test_no_heights_and_no_cameras_give_zeros(fb, device):
+    import torch
+    inst = small(C=8)
+    inst.z = inst.z[:0]
+    g = gpu_run(fb, inst, device)
+    assert g.shape == (1, 8, 37, 29) and np.all(g == 0.0)
+    inst = small(C=8)
+    wl = inst.wl.with_(N=0)
+    e = synth.Instance(wl=wl, features=np.zeros((1, 0, wl.H, wl.W, 8), np.float32),
+                       lidar2img=np.zeros((1, 0, 4, 4), np.float32), z=inst.z)
+    g = gpu_run(fb, e, device)
+    assert np.all(g == 0.0)
+
+
+def test_out_is_fully_overwritten(fb, device):
+    import torch
+    inst = small(C=16)
+    ft, l2i = to_dev(inst, device)
+    wl = inst.wl
+    out = torch.full((1, 16, wl.X, wl.Y), float("nan"), device=device)
+    fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w), out=out)
+    torch.cuda.synchronize()
+    r, s, _ = oracle.run_instance(inst)
+    assert_parity(out.cpu().numpy(), r, s, RTOL["f32"], "prefilled NaN")
+
+
+def test_unaligned_feature_base_uses_narrower_vectors(fb, device):
+    import torch
+    inst = small(C=16)
+    wl = inst.wl
+    n = inst.features.size
+    buf = torch.empty(n + 1, dtype=torch.float32, device=device)
+    view = buf[1:].view(inst.features.shape)  # 4-byte but not 16-byte aligned
+    view.copy_(torch.from_numpy(inst.features))
+    assert view.data_ptr() % 16 != 0
+    l2i = torch.from_numpy(inst.lidar2img).to(device)
+    out = fb.sample_vt(view, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    torch.cuda.synchronize()
+    r, s, _ = oracle.run_instance(inst)
+    assert_parity(out.cpu().numpy(), r, s, RTOL["f32"], "unaligned base")
+
+
+def test_run_to_run_bitwise_determinism(fb, device):
+    import torch
+    inst = synth.make_workload(synth.config("rep"))
+    wl = inst.wl
+    ft, l2i = to_dev(inst, device)
+    a = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    b = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_non_default_stream(fb, device):
+    import torch
+    inst = small(C=24)
+    wl = inst.wl
+    ft, l2i = to_dev(inst, device)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        out = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    s.synchronize()
+    r, sc, _ = oracle.run_instance(inst)
+    assert_parity(out.cpu().numpy(), r, sc, RTOL["f32"], "side stream")
+
+
+@pytest.mark.parametrize("Z", [4, 64])
+def test_peak_operator_memory_is_the_output(fb, device, Z):
+    import torch
+    inst = synth.make_workload(synth.config("z_sweep", Z=Z))
+    wl = inst.wl
+    ft, l2i = to_dev(inst, device)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    out = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated() - base
+    out_bytes = out.numel() * 4
+    assert out_bytes <= peak <= out_bytes + 2 * 1024 * 1024, (peak, out_bytes)
