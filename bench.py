@@ -173,6 +173,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the secondary workloads reported for context")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB three times "
+                         "(a plain copy of known size that scales the HBM byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -188,6 +191,15 @@ def main(argv=None) -> int:
     if not os.path.exists(fb.library_path()):
         raise SystemExit("libflashbev.so is not built: run `python -m paper_2607_10071_amd.build`")
     device = torch.device("cuda:0")
+    if args.copy_calibration_mb > 0:
+        n = args.copy_calibration_mb * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=device)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wl = synth.config(args.workload)
     inst = synth.make_workload(wl)
     fn, feats, l2i, out, stream = make_call(wl, inst, device)

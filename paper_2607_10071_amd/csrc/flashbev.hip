@@ -3,24 +3,30 @@
 //
 // Execution design (MI355X-first; the paper's one-thread-per-(b,x,y,c)
 // mapping is not used):
-//   * A wavefront owns `cpw` consecutive BEV cells of one batch element.
-//     Lanes span the channels of a cell: each lane holds LW-byte vectors of
-//     the channel-last feature row, so the four bilinear taps of a sample
-//     are fully coalesced row loads across the lanes of a cell.
-//   * Projection, masking and bilinear set-up are done once per
+//   * A workgroup (4 wavefronts) owns a tile of `tile_cells` consecutive BEV
+//     cells (row-major over (x, y)) of one batch element.  Each wavefront
+//     covers `rounds` groups of `cpw` cells.  Within a group, lanes span the
+//     channels of a cell: a lane holds LW-byte vectors of the channel-last
+//     feature row, so the four bilinear taps of a sample are coalesced row
+//     loads across the lanes of a cell.
+//   * Projection, masking and bilinear set-up run once per
 //     (cell, height, camera), not once per channel (the paper recomputes
 //     them per channel, Sec. 3.3.3).  One pass maps the 64 lanes to
-//     (height, camera) pairs of one cell; a ballot gives the per-height
+//     (height, camera) pairs of one cell; a ballot yields the per-height
 //     camera count den_z and a deterministic compaction of the valid
-//     samples into a per-wave LDS list.
+//     samples into a per-wavefront LDS list.
 //   * The per-height valid mean is folded into the tap weights
-//     (w / max(1, den_z)), so the gather loop is one flat weighted sum over
-//     the cell's valid samples held in float32 registers (Eq. 1
-//     re-associated; only rounding changes).
-//   * Camera matrices and heights are staged in LDS once per workgroup.
+//     (w / max(1, den_z)), so the gather is one flat weighted sum over the
+//     cell's valid samples in float32 registers (Eq. 1 re-associated; only
+//     the rounding changes).
+//   * Results go through an LDS tile [C][tile_cells] and leave as 16-byte
+//     stores that cover whole runs of each channel plane of out[B,C,X,Y].
+//     Tiles are numbered so that neighbouring tiles run on the same XCD
+//     (workgroups are dispatched to the 8 XCDs round-robin), which keeps the
+//     partial cache lines at tile edges inside one L2.
 //   * Tap loads are raw buffer loads with 32-bit offsets; every address is
-//     inside the feature tensor by construction (out-of-range taps get
-//     weight zero on an in-range pixel), and the buffer descriptor bounds
+//     inside the feature tensor by construction (an out-of-range tap gets
+//     weight zero on an in-range pixel) and the buffer descriptor bounds
 //     them as well.
 //   * Each output element is written exactly once; no atomics, no
 //     workspace, one launch.
@@ -42,15 +48,19 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kWaves = 4;                 // wavefronts per workgroup
 constexpr int kThreads = kWave * kWaves;  // 256
-constexpr int kCpwMax = 8;                // BEV cells per wavefront (upper bound)
+constexpr int kCpwMax = 8;                // cells per wavefront group (upper bound)
+constexpr int kCellsPerWave = 8;          // a wavefront covers at least this many cells per tile
 constexpr int kRecCap = 64;               // valid samples per (cell, projection pass)
+constexpr int kRecStride = kRecCap + 1;   // odd stride: cells' lists start in different banks
 constexpr int kUnroll = 2;                // samples gathered per loop iteration
+constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
 // Offset of a tap that is not loaded: feature tensors are smaller than
 // 2 GiB and the tap steps are smaller than the tensor, so this offset plus
 // any step stays past the buffer (no 32-bit wrap) and the load returns zero
 // without touching memory.
 constexpr uint32_t kNoTap = 0x80000000u;
 constexpr uint64_t kFeatBytesMax = 0x7FFFFFFFull;
+constexpr uint32_t kLdsBudget = 64u * 1024u;   // dynamic LDS per workgroup
 
 struct Params {
     const void *feat;
@@ -59,7 +69,9 @@ struct Params {
     uint32_t feat_bytes;   // buffer size for the descriptor
     int32_t B, N, H, W, C, X, Y, Z;
     int32_t XY;
-    int32_t tiles_per_b;   // workgroups per batch element
+    int32_t tiles_per_b;   // tiles per batch element
+    int32_t tile_cells;    // cells per tile = kWaves * rounds * cpw
+    int32_t rounds;        // cell groups per wavefront per tile
     float img_w, img_h;    // image size as float
     float sx, sy;          // W / img_w, H / img_h (float32, computed once)
     float x_min, dx, y_min, dy, depth_eps;
@@ -69,8 +81,11 @@ struct Params {
     uint32_t step_y;       // byte step to the lower tap (0 if H == 1)
     int32_t nvec;          // LW-byte vectors per feature row
     int32_t lpc;           // lanes per cell
-    int32_t cpw;           // cells per wavefront
+    int32_t cpw;           // cells per wavefront group
     int32_t zc;            // heights per projection pass
+    int32_t otile_ld;      // row pitch (floats) of the LDS output tile, odd
+    // LDS layout (byte offsets)
+    uint32_t lds_z, lds_w, lds_off, lds_otile;
     float z[FLASHBEV_ZMAX];
 };
 
@@ -81,15 +96,7 @@ template <int DT>
 struct ElemSize { static constexpr int value = (DT == FLASHBEV_F32) ? 4 : 2; };
 
 template <int LW>
-struct Raw;
-template <>
-struct Raw<16> { uint32_t w[4]; };
-template <>
-struct Raw<8> { uint32_t w[2]; };
-template <>
-struct Raw<4> { uint32_t w[1]; };
-template <>
-struct Raw<2> { uint32_t w[1]; };
+struct Raw { uint32_t w[LW >= 4 ? LW / 4 : 1]; };
 
 template <int LW>
 __device__ __forceinline__ Raw<LW> load_vec(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
@@ -117,12 +124,12 @@ __device__ __forceinline__ float elem(const Raw<LW> &r, int e)
     if constexpr (DT == FLASHBEV_F32) {
         return __builtin_bit_cast(float, r.w[e]);
     } else if constexpr (DT == FLASHBEV_BF16) {
-        uint32_t w = r.w[e >> 1];
-        uint32_t bits = (e & 1) ? (w & 0xffff0000u) : (w << 16);
+        const uint32_t w = r.w[e >> 1];
+        const uint32_t bits = (e & 1) ? (w & 0xffff0000u) : (w << 16);
         return __builtin_bit_cast(float, bits);
     } else {
-        uint32_t w = r.w[e >> 1];
-        uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
+        const uint32_t w = r.w[e >> 1];
+        const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
         return (float)__builtin_bit_cast(_Float16, h);
     }
 }
@@ -136,34 +143,34 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Dynamic LDS layout of one workgroup.
-struct Lds {
-    float *mat;      // [N][12]   rows 0..2 of each camera matrix
-    float *z;        // [Z]
-    int *cnt;        // [kWaves][kCpwMax] valid samples per cell in this pass
-    float4 *w;       // [kWaves][cpw][kRecCap] tap weights (den folded in)
-    uint32_t *off;   // [kWaves][cpw][kRecCap] byte offset of the top-left tap
-};
-
-__host__ __device__ inline size_t lds_bytes_for(int cpw)
+__device__ __forceinline__ float bcast(float v, int lane)
 {
-    size_t b = 0;
-    b += sizeof(float) * FLASHBEV_NMAX * 12;
-    b += sizeof(float) * FLASHBEV_ZMAX;
-    b += sizeof(int) * kWaves * kCpwMax;
-    b += sizeof(float4) * (size_t)kWaves * cpw * kRecCap;
-    b += sizeof(uint32_t) * (size_t)kWaves * cpw * kRecCap;
-    return b;
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
 }
 
-__device__ inline Lds carve(unsigned char *base, int cpw)
+// LDS layout of one workgroup: camera matrices [N][12], heights [Z], sample
+// records [kWaves][cpw][kRecStride] (weights as float4, offsets as u32), and
+// the output tile [C][otile_ld].  The record stride and the tile pitch are
+// odd so that different cells and channels fall into different LDS banks.
+struct LdsLayout {
+    uint32_t z, w, off, otile, total;
+};
+
+__host__ __device__ inline uint32_t align16(uint32_t v) { return (v + 15u) & ~15u; }
+
+__host__ __device__ inline LdsLayout lds_layout(int N, int Z, int cpw, int C, int otile_ld)
 {
-    Lds l;
-    l.mat = reinterpret_cast<float *>(base);
-    l.z = l.mat + FLASHBEV_NMAX * 12;
-    l.cnt = reinterpret_cast<int *>(l.z + FLASHBEV_ZMAX);
-    l.w = reinterpret_cast<float4 *>(l.cnt + kWaves * kCpwMax);
-    l.off = reinterpret_cast<uint32_t *>(l.w + (size_t)kWaves * cpw * kRecCap);
+    LdsLayout l;
+    uint32_t o = align16((uint32_t)N * 12u * 4u);
+    l.z = o;
+    o = align16(o + (uint32_t)Z * 4u);
+    l.w = o;
+    o = align16(o + (uint32_t)kWaves * cpw * kRecStride * 16u);
+    l.off = o;
+    o = align16(o + (uint32_t)kWaves * cpw * kRecStride * 4u);
+    l.otile = o;
+    o = align16(o + (uint32_t)C * otile_ld * 4u);
+    l.total = o;
     return l;
 }
 
@@ -177,196 +184,257 @@ sample_vt_fwd(const Params p)
     constexpr int ES = ElemSize<DT>::value;
     constexpr int EPV = LW / ES;  // elements per vector
     extern __shared__ __align__(16) unsigned char smem[];
-    const int cpw = p.cpw;
-    Lds lds = carve(smem, cpw);
+    float *s_mat = reinterpret_cast<float *>(smem);
+    float *s_z = reinterpret_cast<float *>(smem + p.lds_z);
+    float4 *s_w = reinterpret_cast<float4 *>(smem + p.lds_w);
+    uint32_t *s_off = reinterpret_cast<uint32_t *>(smem + p.lds_off);
+    float *s_tile = reinterpret_cast<float *>(smem + p.lds_otile);
 
+    const int cpw = p.cpw;
     const int tid = threadIdx.x;
     const int wave = tid / kWave;
     const int lane = tid % kWave;
-    const int b = blockIdx.x / p.tiles_per_b;
-    const int tile = blockIdx.x - b * p.tiles_per_b;
     const int N = p.N;
+
+    // XCD-aware tile order: the k-th workgroup dispatched to XCD x takes
+    // tile start(x) + k, so every XCD works on one contiguous tile range.
+    const int G = gridDim.x;
+    const int g = blockIdx.x;
+    const int gq = G / kXcds, gr = G % kXcds;
+    const int xcd = g % kXcds;
+    const int tile = xcd * gq + (xcd < gr ? xcd : gr) + g / kXcds;
+    const int b = tile / p.tiles_per_b;
+    const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
 
     // stage camera matrices (rows 0..2) and heights
     for (int t = tid; t < N * 12; t += kThreads) {
-        int n = t / 12, r = t - n * 12;
-        lds.mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
+        const int n = t / 12, r = t - n * 12;
+        s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
     }
-    for (int t = tid; t < p.Z; t += kThreads) lds.z[t] = p.z[t];
+    for (int t = tid; t < p.Z; t += kThreads) s_z[t] = p.z[t];
     __syncthreads();
 
-    const int q0 = (tile * kWaves + wave) * cpw;  // first cell of this wave
-
-    // gather role: cell m_g, channel-vector slot `slot`
-    const int L = p.lpc;
-    const int m_g = lane / L;
-    const int slot = lane - m_g * L;
-    const bool g_active = (m_g < cpw) && (q0 + m_g < p.XY);
-    const int m_lds = m_g < cpw ? m_g : 0;  // idle lanes address cell 0's list
-
-    // projection role: height zl of the pass, camera n
+    // projection role: height zl of a pass, camera n_p
     const int Nd = N > 0 ? N : 1;
     const int zl = lane / Nd;
     const int n_p = lane - zl * Nd;
+    const bool p_role = (N > 0) && (zl < p.zc);
+    const int zshift = p_role ? zl * N : 0;
     const uint64_t nmask = (N >= 64) ? ~0ull : ((1ull << N) - 1ull);
-    const float *mrow = lds.mat + n_p * 12;
+    float mr[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) mr[k] = p_role ? s_mat[n_p * 12 + k] : 0.0f;
+
+    // gather role: cell m_g of the group, channel-vector slot `slot`
+    const int L = p.lpc;
+    const int m_g = lane / L;
+    const int slot = lane - m_g * L;
+    const bool in_group = m_g < cpw;
+    const int m_lds = in_group ? m_g : 0;
 
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p.feat), (short)0,
                                           (int)p.feat_bytes, 0x00020000);
-    const uint32_t cam_base = (uint32_t)b * (uint32_t)N;
 
-    float acc[VPL][EPV];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v)
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) acc[v][e] = 0.0f;
+    float4 *wl = s_w + (size_t)wave * cpw * kRecStride;
+    uint32_t *ol = s_off + (size_t)wave * cpw * kRecStride;
+    const int wcells = p.rounds * cpw;
+    const int q_wave = q_tile + wave * wcells;
+    const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
 
-    float4 *wl = lds.w + (size_t)wave * cpw * kRecCap;
-    uint32_t *ol = lds.off + (size_t)wave * cpw * kRecCap;
-    int *cl = lds.cnt + wave * kCpwMax;
-
-    for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
-        // ---- phase 1: project (cell, height, camera), compact valid samples
-        int maxcnt = 0;
-        for (int m = 0; m < cpw; ++m) {
-            const int q = q0 + m;
-            if (q >= p.XY) {
-                if (lane == 0) cl[m] = 0;
-                continue;
-            }
+    for (int r = 0; r < p.rounds; ++r) {
+        const int q_grp = q_wave + r * cpw;
+        // cells of this group inside the grid (<= 0 past the end of the last tile)
+        const int ncell = (p.XY - q_grp) < cpw ? (p.XY - q_grp) : cpw;
+        // voxel centres of this group's cells (Alg. 2: "compute voxel
+        // center"), one cell per lane, broadcast with readlane below
+        float xs = 0.0f, ys = 0.0f;
+        if (lane < ncell) {
+            const int q = q_grp + lane;
             const int i = q / p.Y;
             const int j = q - i * p.Y;
-            // voxel centre (Alg. 2: "compute voxel center")
-            const float x = p.x_min + ((float)i + 0.5f) * p.dx;
-            const float y = p.y_min + ((float)j + 0.5f) * p.dy;
-            const int zi = z0 + zl;
-            bool ok = false;
-            float xf = 0.0f, yf = 0.0f;
-            if (N > 0 && zl < p.zc && zi < p.Z) {
-                const float z = lds.z[zi];
-                float a, bb, c;
-                a = mrow[0] * x; bb = mrow[1] * y; c = mrow[2] * z;
-                const float up = ((a + bb) + c) + mrow[3];
-                a = mrow[4] * x; bb = mrow[5] * y; c = mrow[6] * z;
-                const float vp = ((a + bb) + c) + mrow[7];
-                a = mrow[8] * x; bb = mrow[9] * y; c = mrow[10] * z;
-                const float d = ((a + bb) + c) + mrow[11];
-                if (d > p.depth_eps) {
-                    const float u = up / d;
-                    const float v = vp / d;
-                    if (u >= 0.0f && u < p.img_w && v >= 0.0f && v < p.img_h) {
-                        ok = true;
-                        xf = u * p.sx - 0.5f;
-                        yf = v * p.sy - 0.5f;
-                    }
-                }
-            }
-            const uint64_t mask = __ballot(ok);
-            if (ok) {
-                const int den = __popcll((mask >> (zl * N)) & nmask);
-                const float inv = (p.reduce == 0) ? 1.0f / (float)den : 1.0f;
-                const float x0f = floorf(xf), y0f = floorf(yf);
-                const float ax = xf - x0f, ay = yf - y0f;
-                int xa = (int)x0f, ya = (int)y0f;
-                float wxa = 1.0f - ax, wxb = ax;
-                float wya = 1.0f - ay, wyb = ay;
-                // keep both taps of each axis on in-range pixels; an
-                // out-of-range tap gets weight zero (zero padding)
-                if (xa < 0) {
-                    xa = 0; wxa = ax; wxb = 0.0f;
-                } else if (xa >= p.W - 1) {
-                    if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
-                    else { xa = 0; wxb = 0.0f; }
-                }
-                if (ya < 0) {
-                    ya = 0; wya = ay; wyb = 0.0f;
-                } else if (ya >= p.H - 1) {
-                    if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
-                    else { ya = 0; wyb = 0.0f; }
-                }
-                const uint32_t pix = ((cam_base + (uint32_t)n_p) * (uint32_t)p.H + (uint32_t)ya) *
-                                         (uint32_t)p.W + (uint32_t)xa;
-                const int pos = __builtin_amdgcn_mbcnt_hi(
-                    (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                const int r = m * kRecCap + pos;
-                wl[r] = make_float4((wxa * wya) * inv, (wxb * wya) * inv, (wxa * wyb) * inv,
-                                    (wxb * wyb) * inv);
-                ol[r] = pix * p.row_bytes;
-            }
-            const int cnt = __popcll(mask);
-            if (lane == 0) cl[m] = cnt;
-            maxcnt = cnt > maxcnt ? cnt : maxcnt;
+            xs = p.x_min + ((float)i + 0.5f) * p.dx;
+            ys = p.y_min + ((float)j + 0.5f) * p.dy;
         }
-        wave_lds_sync();
+        const bool g_active = m_g < ncell;
 
-        // ---- phase 2: gather-reduce over the compacted samples
-        const int my_cnt = g_active ? cl[m_g] : 0;
-        const float4 *wv = wl + m_lds * kRecCap;
-        const uint32_t *ov = ol + m_lds * kRecCap;
-        // kUnroll samples per iteration so that 4*kUnroll tap loads are in
-        // flight per wavefront; lanes past their cell's count load nothing
-        // (offset beyond the buffer) with weight zero.
-        for (int k = 0; k < maxcnt; k += kUnroll) {
-            float4 w[kUnroll];
-            uint32_t base[kUnroll];
-            bool act[kUnroll];
+        float acc[VPL][EPV];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int kk = k + u;
-                const int kr = kk < kRecCap ? kk : kRecCap - 1;
-                act[u] = kk < my_cnt;
-                const float4 wr = wv[kr];
-                const uint32_t br = ov[kr];
-                w[u] = act[u] ? wr : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                base[u] = br;
+        for (int v = 0; v < VPL; ++v)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[v][e] = 0.0f;
+
+        for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
+            // ---- phase 1a: project every (height, camera) pair of each
+            // cell, apply the mask M_n, and compact the valid samples as
+            // (u, v, camera, den_z) in the cell's record list
+            const int zi = z0 + zl;
+            const bool l_ok = p_role && zi < p.Z;
+            const float zv = l_ok ? s_z[zi] : 0.0f;
+            const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
+            int total = 0, maxcnt = 0;
+            int cnt_lane = 0, pre_lane = 0;  // lane m holds cell m's count and prefix
+            for (int m = 0; m < ncell; ++m) {
+                const float x = bcast(xs, m);
+                const float y = bcast(ys, m);
+                // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
+                const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
+                const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
+                const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
+                const float u = up / d;
+                const float v = vp / d;
+                // M_n: positive depth, inside the image (half-open box)
+                const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
+                                (v >= 0.0f) && (v < p.img_h);
+                const uint64_t mask = __ballot(ok);
+                if (ok) {
+                    const int den = __popcll((mask >> zshift) & nmask);
+                    const int pos = __builtin_amdgcn_mbcnt_hi(
+                        (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                    wl[m * kRecStride + pos] =
+                        make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
+                }
+                const int cnt = __popcll(mask);
+                cnt_lane = lane == m ? cnt : cnt_lane;
+                pre_lane = lane == m ? total : pre_lane;
+                total += cnt;
+                maxcnt = cnt > maxcnt ? cnt : maxcnt;
             }
-#pragma unroll
-            for (int v = 0; v < VPL; ++v) {
-                const int vi = slot + L * v;
-                if (VPL == 1 || vi < p.nvec) {
-                    Raw<LW> t[kUnroll][4];
+            const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
+            wave_lds_sync();
+
+            // ---- phase 1b: for all valid samples of the group at once,
+            // bilinear set-up: feature coordinates, tap weights with
+            // 1 / max(1, den_z) folded in, byte offset of the first tap
+            for (int base = 0; base < total; base += kWave) {
+                const int idx = base + lane;
+                int m = 0, pm = 0;  // cell of sample idx and that cell's first index
+                for (int mm = 1; mm < ncell; ++mm) {
+                    const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
+                    const bool ge = idx >= pf;
+                    m = ge ? mm : m;
+                    pm = ge ? pf : pm;
+                }
+                if (idx < total) {
+                    const int slotk = m * kRecStride + (idx - pm);
+                    const float4 pr = wl[slotk];
+                    const float u = pr.x, v = pr.y;
+                    const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
+                    const int den = __builtin_bit_cast(int, pr.w);
+                    const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+                    const float xf = u * p.sx - 0.5f;
+                    const float yf = v * p.sy - 0.5f;
+                    const float x0f = floorf(xf), y0f = floorf(yf);
+                    const float ax = xf - x0f, ay = yf - y0f;
+                    int xa = (int)x0f, ya = (int)y0f;
+                    float wxa = 1.0f - ax, wxb = ax;
+                    float wya = 1.0f - ay, wyb = ay;
+                    // keep both taps of each axis on in-range pixels; an
+                    // out-of-range tap gets weight zero (zero padding)
+                    if (xa < 0) {
+                        xa = 0; wxa = ax; wxb = 0.0f;
+                    } else if (xa >= p.W - 1) {
+                        if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
+                        else { xa = 0; wxb = 0.0f; }
+                    }
+                    if (ya < 0) {
+                        ya = 0; wya = ay; wyb = 0.0f;
+                    } else if (ya >= p.H - 1) {
+                        if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
+                        else { ya = 0; wyb = 0.0f; }
+                    }
+                    wya *= inv;
+                    wyb *= inv;
+                    const uint32_t pix = ((cam0 + n) * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W +
+                                         (uint32_t)xa;
+                    wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
+                    ol[slotk] = pix * p.row_bytes;
+                }
+            }
+            // records past a cell's count, up to the padded loop length,
+            // carry zero weights and no tap
+            for (int m = 0; m < ncell; ++m) {
+                const int c = __builtin_amdgcn_readlane(cnt_lane, m);
+                if (lane >= c && lane < maxpad) {
+                    wl[m * kRecStride + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    ol[m * kRecStride + lane] = kNoTap;
+                }
+            }
+            wave_lds_sync();
+
+            // ---- phase 2: gather-reduce over the compacted samples.
+            // kUnroll samples per iteration keep 4*kUnroll tap loads in
+            // flight per lane.
+            if (g_active) {
+                const float4 *wv = wl + m_lds * kRecStride;
+                const uint32_t *ov = ol + m_lds * kRecStride;
+                for (int k = 0; k < maxpad; k += kUnroll) {
+                    float4 w[kUnroll];
+                    uint32_t base[kUnroll];
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) {
-                        const uint32_t vo = act[u] ? base[u] + (uint32_t)vi * LW : kNoTap;
-                        t[u][0] = load_vec<LW>(rsrc, vo, 0u);
-                        t[u][1] = load_vec<LW>(rsrc, vo, p.step_x);
-                        t[u][2] = load_vec<LW>(rsrc, vo, p.step_y);
-                        t[u][3] = load_vec<LW>(rsrc, vo, p.step_x + p.step_y);
+                        w[u] = wv[k + u];
+                        base[u] = ov[k + u];
                     }
 #pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) {
+                    for (int v = 0; v < VPL; ++v) {
+                        const int vi = slot + L * v;
+                        if (VPL == 1 || vi < p.nvec) {
+                            Raw<LW> t[kUnroll][4];
 #pragma unroll
-                        for (int e = 0; e < EPV; ++e) {
-                            float s = acc[v][e];
-                            s = fmaf(w[u].x, elem<DT, LW>(t[u][0], e), s);
-                            s = fmaf(w[u].y, elem<DT, LW>(t[u][1], e), s);
-                            s = fmaf(w[u].z, elem<DT, LW>(t[u][2], e), s);
-                            s = fmaf(w[u].w, elem<DT, LW>(t[u][3], e), s);
-                            acc[v][e] = s;
+                            for (int u = 0; u < kUnroll; ++u) {
+                                const uint32_t vo = base[u] + (uint32_t)vi * LW;
+                                t[u][0] = load_vec<LW>(rsrc, vo, 0u);
+                                t[u][1] = load_vec<LW>(rsrc, vo, p.step_x);
+                                t[u][2] = load_vec<LW>(rsrc, vo, p.step_y);
+                                t[u][3] = load_vec<LW>(rsrc, vo, p.step_x + p.step_y);
+                            }
+#pragma unroll
+                            for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+                                for (int e = 0; e < EPV; ++e) {
+                                    float s = acc[v][e];
+                                    s = fmaf(w[u].x, elem<DT, LW>(t[u][0], e), s);
+                                    s = fmaf(w[u].y, elem<DT, LW>(t[u][1], e), s);
+                                    s = fmaf(w[u].z, elem<DT, LW>(t[u][2], e), s);
+                                    s = fmaf(w[u].w, elem<DT, LW>(t[u][3], e), s);
+                                    acc[v][e] = s;
+                                }
+                            }
                         }
                     }
                 }
             }
+            wave_lds_sync();
         }
-        wave_lds_sync();
-    }
 
-    // ---- single write of out[b, c, i, j] (Alg. 2: write once)
-    if (g_active) {
-        const size_t q = (size_t)(q0 + m_g);
-        float *ob = p.out + (size_t)b * p.C * p.XY + q;
+        // stash this group's results in the output tile
+        if (g_active) {
+            const int col = wave * wcells + r * cpw + m_g;
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) {
-            const int vi = slot + L * v;
-            if (VPL == 1 || vi < p.nvec) {
+            for (int v = 0; v < VPL; ++v) {
+                const int vi = slot + L * v;
+                if (VPL == 1 || vi < p.nvec) {
 #pragma unroll
-                for (int e = 0; e < EPV; ++e) {
-                    const int c = vi * EPV + e;
-                    ob[(size_t)c * p.XY] = acc[v][e];
+                    for (int e = 0; e < EPV; ++e)
+                        s_tile[(vi * EPV + e) * p.otile_ld + col] = acc[v][e];
                 }
             }
         }
+    }
+    __syncthreads();
+
+    // ---- single write of out[b, c, tile cells] (Alg. 2: write once):
+    // consecutive threads write consecutive cells of one channel plane
+    const int T = p.tile_cells;
+    const int rem = p.XY - q_tile;
+    const int nq = rem < T ? rem : T;
+    float *ob = p.out + (size_t)b * p.C * p.XY + q_tile;
+    const int rows = kThreads / nq;  // channel rows written per sweep (>= 1)
+    const int c0 = tid / nq;
+    const int k = tid - c0 * nq;
+    if (c0 < rows) {
+        for (int c = c0; c < p.C; c += rows) ob[(size_t)c * p.XY + k] = s_tile[c * p.otile_ld + k];
     }
 }
 
@@ -420,7 +488,7 @@ bool finite(float v) { return v == v && v - v == 0.0f; }
 bool overlaps(const void *a, size_t na, const void *b, size_t nb)
 {
     if (!na || !nb) return false;
-    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
     return a0 < b0 + nb && b0 < a0 + na;
 }
 
@@ -473,6 +541,18 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     if (lpc > kWave) return FLASHBEV_ERR_UNSUPPORTED;
     int cpw = kWave / lpc;
     if (cpw > kCpwMax) cpw = kCpwMax;
+    // tile: at least kCellsPerWave cells per wavefront, fewer if the output
+    // tile would not fit the LDS budget (very wide rows)
+    int rounds = (kCellsPerWave + cpw - 1) / cpw;
+    auto pitch = [&](int r) { return (kWaves * r * cpw) | 1; };
+    LdsLayout lay = lds_layout(f->N, zb->Z, cpw, f->C, pitch(rounds));
+    while (lay.total > kLdsBudget && rounds > 1) {
+        --rounds;
+        lay = lds_layout(f->N, zb->Z, cpw, f->C, pitch(rounds));
+    }
+    if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
+    const int tile_cells = kWaves * rounds * cpw;
+    const int otile_ld = pitch(rounds);
 
     Params &p = pl->prm;
     memset(&p, 0, sizeof(p));
@@ -483,8 +563,9 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.B = f->B; p.N = f->N; p.H = f->H; p.W = f->W; p.C = f->C;
     p.X = s->X; p.Y = s->Y; p.Z = zb->Z;
     p.XY = (int32_t)XY;
-    const int cells_per_wg = kWaves * cpw;
-    p.tiles_per_b = (int32_t)((XY + cells_per_wg - 1) / cells_per_wg);
+    p.tile_cells = tile_cells;
+    p.rounds = rounds;
+    p.tiles_per_b = (int32_t)((XY + tile_cells - 1) / tile_cells);
     p.img_w = (float)f->img_w;
     p.img_h = (float)f->img_h;
     p.sx = (float)f->W / (float)f->img_w;
@@ -501,11 +582,16 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
     p.zc = zc < 1 ? 1 : zc;
+    p.otile_ld = otile_ld;
+    p.lds_z = lay.z;
+    p.lds_w = lay.w;
+    p.lds_off = lay.off;
+    p.lds_otile = lay.otile;
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
     pl->workgroups = empty ? 0 : (int64_t)f->B * p.tiles_per_b;
     if (pl->workgroups > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
-    pl->lds = lds_bytes_for(cpw);
+    pl->lds = lay.total;
     pl->lw = lw;
     pl->vpl = vpl;
     pl->empty = empty;
@@ -540,7 +626,7 @@ int flashbev_launch_info(const flashbev_features *features, const flashbev_bev_g
                          int32_t *cells_per_wave, int32_t *lanes_per_cell)
 {
     Plan pl;
-    int rc = make_plan(features, nullptr, spec, z_bins, nullptr, false, &pl);
+    const int rc = make_plan(features, nullptr, spec, z_bins, nullptr, false, &pl);
     if (rc) return rc;
     if (workgroups) *workgroups = pl.workgroups;
     if (threads_per_workgroup) *threads_per_workgroup = kThreads;
@@ -555,15 +641,15 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
                        float *out, void *stream)
 {
     Plan pl;
-    int rc = make_plan(features, lidar2img, spec, z_bins, out, true, &pl);
+    const int rc = make_plan(features, lidar2img, spec, z_bins, out, true, &pl);
     if (rc) return rc;
     if (pl.empty) return FLASHBEV_OK;
-    KernelFn fn = pick_kernel(features->dtype, pl.lw, pl.vpl);
+    const KernelFn fn = pick_kernel(features->dtype, pl.lw, pl.vpl);
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
     void *args[] = {&pl.prm};
-    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),
-                                   dim3((unsigned)pl.workgroups), dim3(kThreads), args, pl.lds,
-                                   reinterpret_cast<hipStream_t>(stream));
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),
+                                         dim3((unsigned)pl.workgroups), dim3(kThreads), args,
+                                         pl.lds, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
 }
 
