@@ -78,31 +78,82 @@ def load_traffic(workload: str):
     return rec.get("bytes_per_launch")
 
 
+def settle(fn, seconds: float = 0.3) -> None:
+    """Untimed calls for a fixed time: the first ~0.1 s of GPU work in a
+    process runs at irregular speed (clock and power state)."""
+    import torch
+
+    t_end = time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
+
+
 def time_gpu(fn, steps: int, warmup: int, stream):
+    """W untimed calls, then exactly K back-to-back calls between two HIP
+    events recorded on the launch stream (synchronized on both sides)."""
     import torch
 
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record(stream)
-    for k in range(steps):
-        starts[k].record(stream)
+    for _ in range(steps):
         fn()
-        ends[k].record(stream)
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     total_ms = t0.elapsed_time(t1)
-    return {"total_ms": total_ms, "ms_per_step": total_ms / steps, "launch_ms_mean": statistics.fmean(per),
-            "launch_ms_median": statistics.median(per),
-            "launch_ms_std": statistics.pstdev(per), "wall_s": wall}
+    return {"total_ms": total_ms, "ms_per_step": total_ms / steps, "wall_s": wall}
+
+
+def ceilings(row_bytes: int, device) -> dict:
+    """Measured memory ceilings of this GPU: the gather access shape on an
+    L2-resident (2 MiB) and an L1-resident (16 KiB) buffer, and a 1 GiB
+    coalesced HBM read stream (GB/s, best of 5)."""
+    import torch
+
+    from paper_2607_10071_amd import membench
+
+    stream = torch.cuda.current_stream(device)
+    out = {}
+    for name, nbytes, pitch in (("gather_l2", 2 << 20, 88), ("gather_l1", 16 << 10, 8)):
+        buf = torch.ones(nbytes // 4, dtype=torch.float32, device=device)
+        wgs, iters = 4096, 64
+        sink = torch.empty(wgs * 256, dtype=torch.float32, device=device)
+        membench.gather(buf, row_bytes, pitch, iters, wgs, sink, stream.cuda_stream)
+        best = float("inf")
+        for _ in range(5):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            membench.gather(buf, row_bytes, pitch, iters, wgs, sink, stream.cuda_stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b) * 1e-3)
+        out[name] = membench.gather_bytes(wgs, row_bytes, iters) / best / 1e9
+    nbytes = 1 << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=device)
+    wgs = 256 * 16
+    sink = torch.empty(wgs * 256, dtype=torch.float32, device=device)
+    membench.stream_read(buf, wgs, sink, stream.cuda_stream)
+    best = float("inf")
+    for _ in range(5):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        membench.stream_read(buf, wgs, sink, stream.cuda_stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b) * 1e-3)
+    out["hbm_read"] = nbytes / best / 1e9
+    del buf, sink
+    torch.cuda.empty_cache()
+    return {k: round(v, 1) for k, v in out.items()}
 
 
 def make_call(wl, inst, device):
@@ -149,9 +200,9 @@ def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
     import oracle
 
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    oracle.run_instance(inst, nthreads=threads)  # warm-up
+    _, _, counters = oracle.run_instance(inst, nthreads=threads)  # warm-up
     reps, t = 0, 0.0
-    while t < min_seconds and reps < 1000:
+    while t < min_seconds and reps < 5000:
         t0 = time.perf_counter()
         oracle.run_instance(inst, nthreads=threads)
         t += time.perf_counter() - t0
@@ -160,7 +211,8 @@ def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
     return {"value": inst.wl.samples / per / 1e9, "unit": "Gsamples/s", "cores": threads,
             "kind": "oracle", "ms_per_call": per * 1e3,
             "sample": f"the whole {inst.wl.name} workload ({inst.wl.samples} samples) "
-                      f"evaluated {reps} times in {t:.1f} s"}
+                      f"evaluated {reps} times in {t:.1f} s",
+            "counters": counters}
 
 
 def main(argv=None) -> int:
@@ -203,10 +255,11 @@ def main(argv=None) -> int:
     wl = synth.config(args.workload)
     inst = synth.make_workload(wl)
     fn, feats, l2i, out, stream = make_call(wl, inst, device)
+    settle(fn)
     t = time_gpu(fn, args.steps, args.warmup, stream)
-    launch_s = t["launch_ms_mean"] * 1e-3
+    launch_s = t["ms_per_step"] * 1e-3  # average launch duration over the timed region
     samples = wl.samples
-    value = samples / (t["ms_per_step"] * 1e-3) / 1e9
+    value = samples / launch_s / 1e9
     alg = algorithmic_bytes(wl)
     achieved = alg / launch_s / 1e9
     traffic = load_traffic(wl.name)
@@ -214,6 +267,7 @@ def main(argv=None) -> int:
                           (wl.img_h, wl.img_w), data_ptr=feats.data_ptr())
     peak_mem = peak_operator_memory(wl, inst, device)
     del fn, feats, l2i, out
+    row_bytes = wl.C * elem_size(wl.dtype)
 
     rec = {
         "metric": "fused Sampling-VT latency (ms) & Gsamples/s at 200x200x8; peak op memory",
@@ -232,8 +286,7 @@ def main(argv=None) -> int:
                                f"BEV {wl.X}x{wl.Y} Z={wl.Z}",
                    "B": wl.B, "N": wl.N, "H": wl.H, "W": wl.W, "C": wl.C, "X": wl.X, "Y": wl.Y,
                    "Z": wl.Z, "feature_dtype": wl.dtype, "samples_per_step": samples},
-        "latency_ms": {"mean": round(t["launch_ms_mean"], 5), "median": round(t["launch_ms_median"], 5),
-                       "std": round(t["launch_ms_std"], 5)},
+        "latency_ms": round(t["ms_per_step"], 5),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
                      "traffic": traffic, "algorithmic_bytes_per_launch": alg,
@@ -250,10 +303,11 @@ def main(argv=None) -> int:
             w2 = synth.config(name)
             i2 = synth.make_workload(w2)
             f2, a, b_, c_, s2 = make_call(w2, i2, device)
+            settle(f2, 0.1)
             t2 = time_gpu(f2, max(20, args.steps // 2), args.warmup, s2)
-            extra[name] = {"ms": round(t2["launch_ms_mean"], 5),
+            extra[name] = {"ms": round(t2["ms_per_step"], 5),
                            "gsamples_per_s": round(w2.samples / (t2["ms_per_step"] * 1e-3) / 1e9, 3),
-                           "hbm_frac": round(algorithmic_bytes(w2) / (t2["launch_ms_mean"] * 1e-3) / 1e9
+                           "hbm_frac": round(algorithmic_bytes(w2) / (t2["ms_per_step"] * 1e-3) / 1e9
                                              / HBM_PEAK_GBS, 5)}
             del f2, a, b_, c_
         extra["paper_context"] = {
@@ -261,9 +315,23 @@ def main(argv=None) -> int:
             "flashbev_a6000_forward_ms": 1.77, "tensorized_a6000_forward_ms": 9.18,
             "flashbev_trt_4070tis_forward_ms_z8": 1.128}
         rec["secondary"] = extra
+        rec["ceilings_GBs"] = ceilings(row_bytes, device)
 
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
+        cb = cpu_baseline(inst, args.cpu_seconds)
+        counters = cb.pop("counters")
+        rec["cpu_baseline"] = cb
+        # gather roofline: the in-range bilinear taps of the workload (counted
+        # by the oracle above) times the feature row, over the launch time,
+        # against the measured L2-resident gather ceiling
+        gather_bytes = counters["taps"] * row_bytes
+        g_ach = gather_bytes / launch_s / 1e9
+        peak = rec.get("ceilings_GBs", {}).get("gather_l2")
+        rec["gather_roofline"] = {
+            "bound": "l2_gather", "achieved": round(g_ach, 1), "peak": peak, "unit": "GB/s",
+            "frac": round(g_ach / peak, 4) if peak else None,
+            "gather_bytes_per_launch": gather_bytes,
+            "valid_samples": counters["valid_samples"], "taps": counters["taps"]}
 
     print(json.dumps(rec), flush=True)
     return 0

@@ -3,7 +3,9 @@
     python -m paper_2607_10071_amd.build
 
 Produces ``paper_2607_10071_amd/libflashbev.so`` (the fused Sampling-VT
-forward behind the C ABI of ``include/flashbev.h``).
+forward behind the C ABI of ``include/flashbev.h``) and
+``libflashbev_membench.so`` (the memory-ceiling micro-benchmarks of
+``include/flashbev_membench.h`` that bench.py uses).
 """
 from __future__ import annotations
 
@@ -16,6 +18,9 @@ ROOT = os.path.dirname(HERE)
 INCLUDE = os.path.join(ROOT, "include")
 SRC = os.path.join(HERE, "csrc", "flashbev.hip")
 LIB = os.path.join(HERE, "libflashbev.so")
+# memory-ceiling micro-benchmarks used by bench.py (not part of the operator)
+MEMBENCH_SRC = os.path.join(HERE, "csrc", "membench.hip")
+MEMBENCH_LIB = os.path.join(HERE, "libflashbev_membench.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -38,17 +43,23 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", SRC, "-o", tmp]
+def _compile(src: str, lib: str, verbose: bool) -> str:
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", src, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError(f"hipcc failed with status {r.returncode}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the operator library and the micro-benchmark library."""
+    _compile(MEMBENCH_SRC, MEMBENCH_LIB, verbose)
+    return _compile(SRC, LIB, verbose)
 
 
 if __name__ == "__main__":

@@ -49,11 +49,12 @@ constexpr int kWave = 64;
 constexpr int kWaves = 4;                 // wavefronts per workgroup
 constexpr int kThreads = kWave * kWaves;  // 256
 constexpr int kCpwMax = 8;                // cells per wavefront group (upper bound)
-constexpr int kCellsPerWave = 8;          // a wavefront covers at least this many cells per tile
+constexpr int kCellsPerWave = 6;          // a wavefront covers at least this many cells per tile
 constexpr int kRecCap = 64;               // valid samples per (cell, projection pass)
 constexpr int kRecStride = kRecCap + 1;   // odd stride: cells' lists start in different banks
 constexpr int kUnroll = 2;                // samples gathered per loop iteration
 constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr int kStripe = 16;               // consecutive tiles per XCD stripe
 // Offset of a tap that is not loaded: feature tensors are smaller than
 // 2 GiB and the tap steps are smaller than the tensor, so this offset plus
 // any step stays past the buffer (no 32-bit wrap) and the load returns zero
@@ -196,13 +197,20 @@ sample_vt_fwd(const Params p)
     const int lane = tid % kWave;
     const int N = p.N;
 
-    // XCD-aware tile order: the k-th workgroup dispatched to XCD x takes
-    // tile start(x) + k, so every XCD works on one contiguous tile range.
-    const int G = gridDim.x;
+    // XCD-aware tile order.  Workgroups go to the 8 XCDs round-robin; the
+    // k-th workgroup on XCD x takes tile (k / S) * 8S + x * S + k % S, so an
+    // XCD works through stripes of S consecutive tiles (neighbours share its
+    // L2, which merges their partial output lines) and the stripes of the 8
+    // XCDs interleave over the whole grid (each XCD sees a like mix of
+    // heavy and light regions).  A last partial block of 8S tiles keeps the
+    // dispatch order.
     const int g = blockIdx.x;
-    const int gq = G / kXcds, gr = G % kXcds;
-    const int xcd = g % kXcds;
-    const int tile = xcd * gq + (xcd < gr ? xcd : gr) + g / kXcds;
+    const int full = (int)(gridDim.x / (kXcds * kStripe)) * (kXcds * kStripe);
+    int tile = g;
+    if (g < full) {
+        const int xcd = g % kXcds, k = g / kXcds;
+        tile = (k / kStripe) * (kXcds * kStripe) + xcd * kStripe + k % kStripe;
+    }
     const int b = tile / p.tiles_per_b;
     const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
 
