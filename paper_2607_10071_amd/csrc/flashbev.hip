@@ -3,9 +3,9 @@
 //
 // Execution design (MI355X-first; the paper's one-thread-per-(b,x,y,c)
 // mapping is not used):
-//   * A workgroup (4 wavefronts) owns a tile of `tile_cells` consecutive BEV
-//     cells (row-major over (x, y)) of one batch element.  Each wavefront
-//     covers `rounds` groups of `cpw` cells.  Within a group, lanes span the
+//   * A workgroup (2 or 4 wavefronts) owns a tile of `tile_cells`
+//     consecutive BEV cells (row-major over (x, y)) of one batch element.
+//     Each wavefront covers `rounds` groups of `cpw` cells.  Within a group, lanes span the
 //     channels of a cell: a lane holds LW-byte vectors of the channel-last
 //     feature row, so the four bilinear taps of a sample are coalesced row
 //     loads across the lanes of a cell.
@@ -46,8 +46,8 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kWaves = 4;                 // wavefronts per workgroup
-constexpr int kThreads = kWave * kWaves;  // 256
+constexpr int kWavesMax = 4;                 // wavefronts per workgroup (2 or 4)
+constexpr int kThreadsMax = kWave * kWavesMax;  // 256
 constexpr int kCpwMax = 8;                // cells per wavefront group (upper bound)
 constexpr int kCellsPerWave = 6;          // a wavefront covers at least this many cells per tile
 constexpr int kRecCap = 64;               // valid samples per (cell, projection pass)
@@ -71,7 +71,7 @@ struct Params {
     int32_t B, N, H, W, C, X, Y, Z;
     int32_t XY;
     int32_t tiles_per_b;   // tiles per batch element
-    int32_t tile_cells;    // cells per tile = kWaves * rounds * cpw
+    int32_t tile_cells;    // cells per tile = waves * rounds * cpw
     int32_t rounds;        // cell groups per wavefront per tile
     float img_w, img_h;    // image size as float
     float sx, sy;          // W / img_w, H / img_h (float32, computed once)
@@ -83,6 +83,7 @@ struct Params {
     int32_t nvec;          // LW-byte vectors per feature row
     int32_t lpc;           // lanes per cell
     int32_t cpw;           // cells per wavefront group
+    float rcp_n, rcp_lpc;  // float32 1 / max(N, 1) and 1 / lpc
     int32_t zc;            // heights per projection pass
     int32_t otile_ld;      // row pitch (floats) of the LDS output tile, odd
     // LDS layout (byte offsets)
@@ -144,13 +145,25 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// a / d for 0 <= a < 2^22 and 1 <= d < 2^22, with rcp = float32(1 / d): the
+// float estimate is within one of the quotient and one correction step
+// each way makes it exact
+__device__ __forceinline__ int div_small(int a, int d, float rcp)
+{
+    int q = (int)((float)a * rcp);
+    const int r = a - q * d;
+    q += (r >= d) ? 1 : 0;
+    q -= (r < 0) ? 1 : 0;
+    return q;
+}
+
 __device__ __forceinline__ float bcast(float v, int lane)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
 }
 
 // LDS layout of one workgroup: camera matrices [N][12], heights [Z], sample
-// records [kWaves][cpw][kRecStride] (weights as float4, offsets as u32), and
+// records [waves][cpw][kRecStride] (weights as float4, offsets as u32), and
 // the output tile [C][otile_ld].  The record stride and the tile pitch are
 // odd so that different cells and channels fall into different LDS banks.
 struct LdsLayout {
@@ -159,16 +172,17 @@ struct LdsLayout {
 
 __host__ __device__ inline uint32_t align16(uint32_t v) { return (v + 15u) & ~15u; }
 
-__host__ __device__ inline LdsLayout lds_layout(int N, int Z, int cpw, int C, int otile_ld)
+__host__ __device__ inline LdsLayout lds_layout(int N, int Z, int waves, int cpw, int C,
+                                                int otile_ld)
 {
     LdsLayout l;
     uint32_t o = align16((uint32_t)N * 12u * 4u);
     l.z = o;
     o = align16(o + (uint32_t)Z * 4u);
     l.w = o;
-    o = align16(o + (uint32_t)kWaves * cpw * kRecStride * 16u);
+    o = align16(o + (uint32_t)waves * cpw * kRecStride * 16u);
     l.off = o;
-    o = align16(o + (uint32_t)kWaves * cpw * kRecStride * 4u);
+    o = align16(o + (uint32_t)waves * cpw * kRecStride * 4u);
     l.otile = o;
     o = align16(o + (uint32_t)C * otile_ld * 4u);
     l.total = o;
@@ -179,7 +193,7 @@ __host__ __device__ inline LdsLayout lds_layout(int N, int Z, int cpw, int C, in
 // the fused kernel
 // ---------------------------------------------------------------------------
 template <int DT, int LW, int VPL>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kThreadsMax)
 sample_vt_fwd(const Params p)
 {
     constexpr int ES = ElemSize<DT>::value;
@@ -193,6 +207,7 @@ sample_vt_fwd(const Params p)
 
     const int cpw = p.cpw;
     const int tid = threadIdx.x;
+    const int nthreads = blockDim.x;  // waves * 64
     const int wave = tid / kWave;
     const int lane = tid % kWave;
     const int N = p.N;
@@ -215,16 +230,16 @@ sample_vt_fwd(const Params p)
     const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
 
     // stage camera matrices (rows 0..2) and heights
-    for (int t = tid; t < N * 12; t += kThreads) {
+    for (int t = tid; t < N * 12; t += nthreads) {
         const int n = t / 12, r = t - n * 12;
         s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
     }
-    for (int t = tid; t < p.Z; t += kThreads) s_z[t] = p.z[t];
+    for (int t = tid; t < p.Z; t += nthreads) s_z[t] = p.z[t];
     __syncthreads();
 
     // projection role: height zl of a pass, camera n_p
     const int Nd = N > 0 ? N : 1;
-    const int zl = lane / Nd;
+    const int zl = div_small(lane, Nd, p.rcp_n);
     const int n_p = lane - zl * Nd;
     const bool p_role = (N > 0) && (zl < p.zc);
     const int zshift = p_role ? zl * N : 0;
@@ -235,7 +250,7 @@ sample_vt_fwd(const Params p)
 
     // gather role: cell m_g of the group, channel-vector slot `slot`
     const int L = p.lpc;
-    const int m_g = lane / L;
+    const int m_g = div_small(lane, L, p.rcp_lpc);
     const int slot = lane - m_g * L;
     const bool in_group = m_g < cpw;
     const int m_lds = in_group ? m_g : 0;
@@ -250,20 +265,21 @@ sample_vt_fwd(const Params p)
     const int q_wave = q_tile + wave * wcells;
     const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
 
+    // voxel centres of the wavefront's cells (Alg. 2: "compute voxel
+    // center"), one cell per lane, broadcast with readlane below
+    float xs = 0.0f, ys = 0.0f;
+    if (lane < wcells && q_wave + lane < p.XY) {
+        const int q = q_wave + lane;
+        const int i = q / p.Y;
+        const int j = q - i * p.Y;
+        xs = p.x_min + ((float)i + 0.5f) * p.dx;
+        ys = p.y_min + ((float)j + 0.5f) * p.dy;
+    }
+
     for (int r = 0; r < p.rounds; ++r) {
         const int q_grp = q_wave + r * cpw;
         // cells of this group inside the grid (<= 0 past the end of the last tile)
         const int ncell = (p.XY - q_grp) < cpw ? (p.XY - q_grp) : cpw;
-        // voxel centres of this group's cells (Alg. 2: "compute voxel
-        // center"), one cell per lane, broadcast with readlane below
-        float xs = 0.0f, ys = 0.0f;
-        if (lane < ncell) {
-            const int q = q_grp + lane;
-            const int i = q / p.Y;
-            const int j = q - i * p.Y;
-            xs = p.x_min + ((float)i + 0.5f) * p.dx;
-            ys = p.y_min + ((float)j + 0.5f) * p.dy;
-        }
         const bool g_active = m_g < ncell;
 
         float acc[VPL][EPV];
@@ -283,8 +299,8 @@ sample_vt_fwd(const Params p)
             int total = 0, maxcnt = 0;
             int cnt_lane = 0, pre_lane = 0;  // lane m holds cell m's count and prefix
             for (int m = 0; m < ncell; ++m) {
-                const float x = bcast(xs, m);
-                const float y = bcast(ys, m);
+                const float x = bcast(xs, r * cpw + m);
+                const float y = bcast(ys, r * cpw + m);
                 // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
                 const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
                 const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
@@ -438,8 +454,8 @@ sample_vt_fwd(const Params p)
     const int rem = p.XY - q_tile;
     const int nq = rem < T ? rem : T;
     float *ob = p.out + (size_t)b * p.C * p.XY + q_tile;
-    const int rows = kThreads / nq;  // channel rows written per sweep (>= 1)
-    const int c0 = tid / nq;
+    const int rows = nthreads / nq;  // channel rows written per sweep (>= 1)
+    const int c0 = div_small(tid, nq, 1.0f / (float)nq);
     const int k = tid - c0 * nq;
     if (c0 < rows) {
         for (int c = c0; c < p.C; c += rows) ob[(size_t)c * p.XY + k] = s_tile[c * p.otile_ld + k];
@@ -486,6 +502,7 @@ KernelFn pick_kernel(int dtype, int lw, int vpl)
 struct Plan {
     Params prm;
     int64_t workgroups;
+    int threads;
     size_t lds;
     int lw, vpl;
     bool empty;
@@ -549,17 +566,25 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     if (lpc > kWave) return FLASHBEV_ERR_UNSUPPORTED;
     int cpw = kWave / lpc;
     if (cpw > kCpwMax) cpw = kCpwMax;
+    // Workgroup size (measured on MI355X): with a full group of kCpwMax
+    // cells per pass a wavefront has enough work per tile and 4-wavefront
+    // workgroups are fastest; with fewer cells per pass (wider rows)
+    // 2-wavefront workgroups give twice the tiles and a shorter tail.
+    const int waves = cpw >= kCpwMax ? kWavesMax : 2;
     // tile: at least kCellsPerWave cells per wavefront, fewer if the output
     // tile would not fit the LDS budget (very wide rows)
     int rounds = (kCellsPerWave + cpw - 1) / cpw;
-    auto pitch = [&](int r) { return (kWaves * r * cpw) | 1; };
-    LdsLayout lay = lds_layout(f->N, zb->Z, cpw, f->C, pitch(rounds));
+    auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
+    LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
     while (lay.total > kLdsBudget && rounds > 1) {
         --rounds;
-        lay = lds_layout(f->N, zb->Z, cpw, f->C, pitch(rounds));
+        lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
     }
     if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
-    const int tile_cells = kWaves * rounds * cpw;
+    // a wavefront's cells fit its lanes (centre precompute) and a tile fits
+    // the workgroup's threads (output store)
+    if (rounds * cpw > kWave) return FLASHBEV_ERR_UNSUPPORTED;
+    const int tile_cells = waves * rounds * cpw;
     const int otile_ld = pitch(rounds);
 
     Params &p = pl->prm;
@@ -587,6 +612,8 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.nvec = nvec;
     p.lpc = lpc;
     p.cpw = cpw;
+    p.rcp_n = 1.0f / (float)(f->N > 0 ? f->N : 1);
+    p.rcp_lpc = 1.0f / (float)lpc;
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
     p.zc = zc < 1 ? 1 : zc;
@@ -599,6 +626,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
 
     pl->workgroups = empty ? 0 : (int64_t)f->B * p.tiles_per_b;
     if (pl->workgroups > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
+    pl->threads = waves * kWave;
     pl->lds = lay.total;
     pl->lw = lw;
     pl->vpl = vpl;
@@ -637,7 +665,7 @@ int flashbev_launch_info(const flashbev_features *features, const flashbev_bev_g
     const int rc = make_plan(features, nullptr, spec, z_bins, nullptr, false, &pl);
     if (rc) return rc;
     if (workgroups) *workgroups = pl.workgroups;
-    if (threads_per_workgroup) *threads_per_workgroup = kThreads;
+    if (threads_per_workgroup) *threads_per_workgroup = pl.threads;
     if (lds_bytes) *lds_bytes = (int32_t)pl.lds;
     if (cells_per_wave) *cells_per_wave = pl.prm.cpw;
     if (lanes_per_cell) *lanes_per_cell = pl.prm.lpc;
@@ -656,7 +684,7 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
     void *args[] = {&pl.prm};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),
-                                         dim3((unsigned)pl.workgroups), dim3(kThreads), args,
+                                         dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
                                          pl.lds, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
 }

@@ -21,10 +21,16 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "flashbev.h")
 
 
-def declared_functions():
-    src = open(HEADER).read()
+def declared_functions(header=HEADER):
+    src = open(header).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(flashbev_\w+)\s*\(", src)))
+
+
+def exported(lib_path):
+    out = subprocess.run(["nm", "-D", "--defined-only", lib_path],
+                         capture_output=True, text=True, check=True).stdout
+    return set(re.findall(r" T (flashbev_\w+)", out))
 
 
 def test_library_exports_every_declared_symbol():
@@ -34,12 +40,20 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(fb.library_path())
     for n in names:
         assert hasattr(lib, n), n
-    out = subprocess.run(["nm", "-D", "--defined-only", fb.library_path()],
-                         capture_output=True, text=True, check=True).stdout
-    exported = set(re.findall(r" T (flashbev_\w+)", out))
-    assert set(names) <= exported
-    # nothing else with the prefix leaks out
-    assert exported <= set(names)
+    # everything declared is exported, and nothing else with the prefix leaks
+    assert exported(fb.library_path()) == set(names)
+
+
+def test_every_header_maps_to_a_library_that_exports_it():
+    from paper_2607_10071_amd import membench
+    libs = {"flashbev.h": fb.library_path(), "flashbev_membench.h": membench._LIB_PATH}
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == sorted(libs)
+    for h in headers:
+        names = declared_functions(os.path.join(ROOT, "include", h))
+        assert names, h
+        ctypes.CDLL(libs[h])
+        assert exported(libs[h]) == set(names), h
 
 
 def test_abi_version_and_status_strings():
@@ -151,10 +165,12 @@ def test_launch_info_geometry():
         info = fb.launch_info((1, 6, 32, 88, C), dtype, np.zeros(8), fb.BevGrid(-50, .5, 200, -50, .5, 200),
                               (256, 704))
         assert info["cells_per_wave"] == cpw and info["lanes_per_cell"] == lpc, (dtype, C, info)
-        assert info["threads"] == 256
-        # a tile is 4 wavefronts x `rounds` groups of cpw cells, at least 6
-        # cells per wavefront unless the LDS budget forces fewer rounds
-        tiles = {math.ceil(40000 / (4 * r * cpw)): r for r in range(1, 9)}
+        # 4 wavefronts per workgroup with full 8-cell groups, else 2
+        waves = 4 if cpw == 8 else 2
+        assert info["threads"] == 64 * waves
+        # a tile is `waves` wavefronts x `rounds` groups of cpw cells, at
+        # least 6 cells per wavefront unless the LDS budget forces fewer
+        tiles = {math.ceil(40000 / (waves * r * cpw)): r for r in range(1, 9)}
         assert info["workgroups"] in tiles
         r = tiles[info["workgroups"]]
         assert r * cpw >= 6 or info["lds_bytes"] > 40 * 1024 or C >= 1024
