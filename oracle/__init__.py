@@ -58,6 +58,10 @@ def lib():
         L.oracle_project.argtypes = [P(Problem), ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         L.oracle_project.restype = ctypes.c_int
+        L.oracle_sample_vt_backward.argtypes = [P(Problem), ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+        L.oracle_sample_vt_backward.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -157,3 +161,43 @@ def cells_instance(inst, cells, reduce: str = "mean", nthreads: int = 0):
     return sample_cells(inst.features, inst.lidar2img, inst.z, (wl.img_h, wl.img_w), wl.X,
                         wl.Y, wl.x_min, wl.dx, wl.y_min, wl.dy, cells, wl.depth_eps, reduce,
                         nthreads)
+
+
+def sample_vt_backward(grad_out: np.ndarray, lidar2img: np.ndarray, z: np.ndarray,
+                       feat_shape, img_hw: Tuple[int, int], x_min: float, dx: float,
+                       y_min: float, dy: float, depth_eps: float = 1e-5,
+                       reduce: str = "mean", nthreads: int = 0):
+    """Gradient of Eq. 1 with respect to the feature maps, on the CPU.
+
+    ``grad_out`` is float32 ``[B, C, X, Y]``; ``feat_shape`` is
+    ``(B, N, H, W, C)``.  Returns ``(grad_feat, scale, terms)``:
+    ``grad_feat`` and ``scale`` are float64 ``[B, N, H, W, C]`` (``scale``
+    is the sum of |terms| per element), ``terms`` is int32 ``[B, N, H, W]``,
+    the number of (sample, tap) terms that reach each pixel.
+    """
+    g = np.ascontiguousarray(grad_out, dtype=np.float32)
+    m = np.ascontiguousarray(lidar2img, dtype=np.float32)
+    zz = np.ascontiguousarray(z, dtype=np.float32)
+    B, N, H, W, C = (int(v) for v in feat_shape)
+    assert g.ndim == 4 and g.shape[:2] == (B, C) and m.shape == (B, N, 4, 4)
+    X, Y = g.shape[2], g.shape[3]
+    p = Problem(B, N, H, W, C, int(img_hw[0]), int(img_hw[1]), X, Y, len(zz),
+                float(x_min), float(dx), float(y_min), float(dy), float(depth_eps),
+                REDUCE[reduce])
+    grad_feat = np.empty((B, N, H, W, C), dtype=np.float64)
+    scale = np.empty_like(grad_feat)
+    terms = np.empty((B, N, H, W), dtype=np.int32)
+    rc = lib().oracle_sample_vt_backward(ctypes.byref(p), _ptr(m), _ptr(zz), _ptr(g),
+                                         _ptr(grad_feat), _ptr(scale), _ptr(terms),
+                                         int(nthreads))
+    if rc:
+        raise ValueError(f"oracle_sample_vt_backward failed: {rc}")
+    return grad_feat, scale, terms
+
+
+def backward_instance(inst, grad_out, reduce: str = "mean", nthreads: int = 0):
+    """Backward oracle on a ``synth.Instance`` with output gradient ``grad_out``."""
+    wl = inst.wl
+    return sample_vt_backward(grad_out, inst.lidar2img, inst.z, inst.features.shape,
+                              (wl.img_h, wl.img_w), wl.x_min, wl.dx, wl.y_min, wl.dy,
+                              wl.depth_eps, reduce, nthreads)

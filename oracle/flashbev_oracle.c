@@ -18,6 +18,11 @@
  * per-height valid mean added to the running sum.  Here one call handles all
  * channels of a BEV cell at once, which changes nothing in the arithmetic.
  *
+ * It also computes the backward of Eq. 1 with respect to the feature maps
+ * (the gradient the paper measures in Sec. 4, Tables 2 and 4): the transpose
+ * of the forward's linear map, written as a scatter of each valid sample's
+ * weighted output gradient onto its bilinear taps.
+ *
  * Readings where the paper is silent (each one is also listed in the design doc):
  *   - coordinates follow one fixed float32 recipe: every product and sum is
  *     rounded on its own (no fused multiply-add), left to right, and the
@@ -109,6 +114,34 @@ static int project(const oracle_problem *p, const float *m, float x, float y, fl
 }
 
 /*
+ * Bilinear taps of a sample at feature coordinates (xf, yf) (Sec. 3.1, text
+ * after Eq. 1): the in-range pixels among the four neighbours and their
+ * weights.  Taps outside the map are left out (zero padding).  Returns the
+ * number of taps written to xt[], yt[], w[].
+ */
+static int bilinear_taps(const oracle_problem *p, float xf, float yf, int *xs, int *ys, double *ws)
+{
+    float x0f = floorf(xf), y0f = floorf(yf);
+    float ax = xf - x0f, ay = yf - y0f;
+    int x0 = (int)x0f, y0 = (int)y0f;
+    int n = 0;
+    for (int ty = 0; ty < 2; ++ty) {
+        for (int tx = 0; tx < 2; ++tx) {
+            int xt = x0 + tx, yt = y0 + ty;
+            if (xt < 0 || xt >= p->W || yt < 0 || yt >= p->H)
+                continue;
+            double wx = tx ? (double)ax : 1.0 - (double)ax;
+            double wy = ty ? (double)ay : 1.0 - (double)ay;
+            xs[n] = xt;
+            ys[n] = yt;
+            ws[n] = wx * wy;
+            ++n;
+        }
+    }
+    return n;
+}
+
+/*
  * All C channels of one BEV cell (b, i, j): Eq. 1 evaluated with heights
  * outer and cameras inner.  acc and scale receive C values each; num and mag
  * are C-sized scratch arrays.
@@ -131,24 +164,18 @@ static void one_cell(const oracle_problem *p, const float *feat, const float *l2
             if (!project(p, m, x, y, z, &xf, &yf))
                 continue;
             /* bilinear sample f_n (Sec. 3.1), zero padding outside the map */
-            float x0f = floorf(xf), y0f = floorf(yf);
-            float ax = xf - x0f, ay = yf - y0f;
-            int x0 = (int)x0f, y0 = (int)y0f;
-            for (int ty = 0; ty < 2; ++ty) {
-                for (int tx = 0; tx < 2; ++tx) {
-                    int xt = x0 + tx, yt = y0 + ty;
-                    if (xt < 0 || xt >= p->W || yt < 0 || yt >= p->H)
-                        continue;
-                    double wx = tx ? (double)ax : 1.0 - (double)ax;
-                    double wy = ty ? (double)ay : 1.0 - (double)ay;
-                    double w = wx * wy;
-                    const float *f = feat + ((((size_t)b * p->N + n) * p->H + yt) * p->W + xt) * C;
-                    for (int c = 0; c < C; ++c) {
-                        num[c] += w * (double)f[c];
-                        mag[c] += w * fabs((double)f[c]);
-                    }
-                    if (cnt) cnt->taps += 1;
+            int txs[4], tys[4];
+            double tws[4];
+            const int nt = bilinear_taps(p, xf, yf, txs, tys, tws);
+            for (int t = 0; t < nt; ++t) {
+                const int xt = txs[t], yt = tys[t];
+                const double w = tws[t];
+                const float *f = feat + ((((size_t)b * p->N + n) * p->H + yt) * p->W + xt) * C;
+                for (int c = 0; c < C; ++c) {
+                    num[c] += w * (double)f[c];
+                    mag[c] += w * fabs((double)f[c]);
                 }
+                if (cnt) cnt->taps += 1;
             }
             den += 1;                 /* num_z += M f ; den_z += M */
             if (cnt) cnt->valid_samples += 1;
@@ -279,5 +306,103 @@ int oracle_project(const oracle_problem *p, const float *l2i, const float *zs,
                         yf[o] = ok ? c : NAN;
                     }
             }
+    return 0;
+}
+
+/*
+ * Backward of Eq. 1 with respect to the camera feature maps F_n.
+ *
+ * Eq. 1 is linear in F: every valid sample (b, i, j, k, n) adds, for each
+ * in-range bilinear tap (xt, yt) with weight w, the term
+ * w / max(1, den_k) * F[b, n, yt, xt, c] to out[b, c, i, j] (den_k = number
+ * of cameras valid at height k; the divisor is 1 in sum mode).  The gradient
+ * of a loss with output gradient G = dL/d out is therefore the transpose of
+ * that map:
+ *
+ *   grad_feat[b, n, yt, xt, c] = sum over those (i, j, k, tap) of
+ *                                w / max(1, den_k) * G[b, c, i, j].
+ *
+ * It is computed as a scatter in two passes: first den_k for every
+ * (b, i, j, k), then, one camera (b, n) per task, the samples of that camera
+ * in the forward's order; a task writes only its own camera's slice, so the
+ * tasks never write the same element.  Accumulation is float64.
+ *
+ *   grad_out   [B, C, X, Y] float32
+ *   grad_feat  [B, N, H, W, C] float64 (fully written)
+ *   scale      [B, N, H, W, C] float64, sum of |terms| (may be NULL)
+ *   terms      [B, N, H, W] int32, number of (sample, tap) terms per pixel
+ *              (may be NULL)
+ */
+int oracle_sample_vt_backward(const oracle_problem *p, const float *l2i, const float *zs,
+                              const float *grad_out, double *grad_feat, double *scale,
+                              int32_t *terms, int nthreads)
+{
+    int rc = check(p);
+    if (rc) return rc;
+    const int C = p->C;
+    const size_t cells = (size_t)p->B * p->X * p->Y;
+    const size_t pix = (size_t)p->H * p->W;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    /* pass 1: number of valid cameras per (b, i, j, k) */
+    uint8_t *valid_count = (uint8_t *)malloc(cells * (size_t)(p->Z > 0 ? p->Z : 1));
+    if (!valid_count) return -4;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < (int64_t)p->B * p->X; ++r) {
+        const int b = (int)(r / p->X), i = (int)(r % p->X);
+        for (int j = 0; j < p->Y; ++j) {
+            float x, y;
+            voxel_centre(p, i, j, &x, &y);
+            for (int k = 0; k < p->Z; ++k) {
+                int seen = 0;
+                for (int n = 0; n < p->N; ++n) {
+                    float xf, yf;
+                    seen += project(p, l2i + ((size_t)b * p->N + n) * 16, x, y, zs[k], &xf, &yf);
+                }
+                valid_count[(((size_t)b * p->X + i) * p->Y + j) * p->Z + k] = (uint8_t)seen;
+            }
+        }
+    }
+    /* pass 2: scatter, one camera per task */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t bn = 0; bn < (int64_t)p->B * p->N; ++bn) {
+        const int b = (int)(bn / p->N);
+        const float *m = l2i + (size_t)bn * 16;
+        double *gf = grad_feat + (size_t)bn * pix * C;
+        double *sf = scale ? scale + (size_t)bn * pix * C : NULL;
+        int32_t *tf = terms ? terms + (size_t)bn * pix : NULL;
+        memset(gf, 0, sizeof(double) * pix * C);
+        if (sf) memset(sf, 0, sizeof(double) * pix * C);
+        if (tf) memset(tf, 0, sizeof(int32_t) * pix);
+        for (int i = 0; i < p->X; ++i)
+            for (int j = 0; j < p->Y; ++j) {
+                float x, y;
+                voxel_centre(p, i, j, &x, &y);
+                for (int k = 0; k < p->Z; ++k) {
+                    float xf, yf;
+                    if (!project(p, m, x, y, zs[k], &xf, &yf))
+                        continue;
+                    const int seen = valid_count[(((size_t)b * p->X + i) * p->Y + j) * p->Z + k];
+                    const double norm = (p->reduce == 0 && seen > 1) ? 1.0 / (double)seen : 1.0;
+                    int txs[4], tys[4];
+                    double tws[4];
+                    const int nt = bilinear_taps(p, xf, yf, txs, tys, tws);
+                    for (int t = 0; t < nt; ++t) {
+                        const size_t q = (size_t)tys[t] * p->W + txs[t];
+                        for (int c = 0; c < C; ++c) {
+                            const double g = (double)grad_out[(((size_t)b * C + c) * p->X + i) * p->Y + j];
+                            const double term = tws[t] * norm * g;
+                            gf[q * C + c] += term;
+                            if (sf) sf[q * C + c] += fabs(term);
+                        }
+                        if (tf) tf[q] += 1;
+                    }
+                }
+            }
+    }
+    free(valid_count);
     return 0;
 }

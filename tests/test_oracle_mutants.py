@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
+import test_oracle_backward_pins as bpins
 import test_oracle_pins as pins
 from oracle import build as obuild
 
@@ -34,6 +35,17 @@ MUTANTS = {
                         "float x0f = truncf(xf), y0f = truncf(yf);"),
     "den_counts_taps": ("den += 1;                 /* num_z", "den += 0;                 /* num_z"),
     "feature_row_col_swapped": ("* p->H + yt) * p->W + xt) * C;", "* p->H + xt % p->H) * p->W + yt) * C;"),
+    # backward
+    "bwd_no_valid_mean": ("? 1.0 / (double)seen : 1.0;", "? 1.0 : 1.0;"),
+    "bwd_grad_cell_transposed": ("* p->X + i) * p->Y + j];",
+                                 "* p->X + j % p->X) * p->Y + i % p->Y];"),
+    "bwd_den_counts_all_cameras": ("seen += project(p, l2i", "seen += 1 + 0 * project(p, l2i"),
+    "bwd_tap_row_col_swapped": ("const size_t q = (size_t)tys[t] * p->W + txs[t];",
+                                "const size_t q = (size_t)(txs[t] % p->H) * p->W + tys[t] % p->W;"),
+    "bwd_camera_of_first_batch": ("const float *m = l2i + (size_t)bn * 16;",
+                                  "const float *m = l2i + (size_t)(bn % p->N) * 16;"),
+    "bwd_weight_of_first_tap": ("const double term = tws[t] * norm * g;",
+                                "const double term = tws[0] * norm * g;"),
 }
 
 
@@ -50,6 +62,9 @@ def _pin_suite():
         ("behind", pins.test_hand_point_behind_camera_is_rejected),
         ("mean_and_sum", pins.test_hand_points_valid_mean_over_cameras_and_sum_over_heights),
         ("additivity", pins.test_height_subset_additivity),
+        ("bwd_jacobian", lambda: bpins.test_backward_is_transpose_of_brute_force_jacobian("mean")),
+        ("bwd_adjoint", lambda: bpins.test_adjoint_identity_with_forward_oracle("sum", "ragged")),
+        ("bwd_terms", bpins.test_term_counts_add_up_to_forward_taps),
     ]
 
 
@@ -76,7 +91,8 @@ def test_pins_catch_mutant(tmp_path, mutant):
     real = oracle.lib()
     saved = oracle._LIB
     mlib = ctypes.CDLL(path)
-    for fn in ("oracle_sample_vt", "oracle_sample_cells", "oracle_project"):
+    for fn in ("oracle_sample_vt", "oracle_sample_cells", "oracle_project",
+               "oracle_sample_vt_backward"):
         getattr(mlib, fn).argtypes = getattr(real, fn).argtypes
         getattr(mlib, fn).restype = getattr(real, fn).restype
     caught = []
