@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define FLASHBEV_ABI_VERSION 1
+#define FLASHBEV_ABI_VERSION 2
 /* Largest number of height bins per call (heights travel as kernel
  * arguments, so they cost no device memory). */
 #define FLASHBEV_ZMAX 256
@@ -129,6 +129,41 @@ typedef struct {
 int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img,
                        const flashbev_bev_grid_spec *spec, const flashbev_z_bins *z_bins,
                        float *out, void *stream);
+
+/*
+ * Backward of the fused Sampling-VT operator: the gradient of Eq. 1 with
+ * respect to the camera feature maps (the gradient the paper measures in
+ * Sec. 4, Tables 2 and 4).  Eq. 1 is linear in the features, so the
+ * gradient is the transpose of the forward's map: each valid sample
+ * (b, i, j, z, n) adds w_t / max(1, den_z) * grad_out[b, c, i, j] to channel
+ * c of each of its in-range bilinear taps t (divisor 1 in sum mode).  The
+ * projection, mask, den_z, feature coordinates and weights are the
+ * forward's, computed the same way.  The projection matrices get no
+ * gradient.
+ *
+ *   features       shapes only: B, N, H, W, C, img_h, img_w and a valid
+ *                  dtype are read; `data` is not used and may be NULL.
+ *   lidar2img      device, [B, N, 4, 4] float32, as in flashbev_sample_vt.
+ *   spec, z_bins   as in flashbev_sample_vt.
+ *   grad_out       device, [B, C, X, Y] float32, 4-byte aligned: the
+ *                  gradient of the loss with respect to `out`.
+ *   grad_features  device, [B, N, H, W, C] float32 (whatever the feature
+ *                  dtype), caller-allocated, 4-byte aligned, must not
+ *                  overlap grad_out or lidar2img.  Fully overwritten (a
+ *                  fill kernel zeroes it first, on the same stream).
+ *   stream         hipStream_t; NULL means the default stream.
+ *
+ * The sum over samples uses float32 atomic adds, so its rounding order (not
+ * its terms) varies from run to run.  Limits: those of flashbev_sample_vt,
+ * plus B N H W C < 2^31.  Returns FLASHBEV_OK once enqueued or a negative
+ * flashbev_status; argument errors are reported before any HIP call.
+ * Nothing is enqueued when B, N, H, W or C is zero; only the fill runs
+ * when X, Y or Z is zero.
+ */
+int flashbev_sample_vt_backward(const flashbev_features *features, const float *lidar2img,
+                                const flashbev_bev_grid_spec *spec,
+                                const flashbev_z_bins *z_bins, const float *grad_out,
+                                float *grad_features, void *stream);
 
 /* Static, human-readable text for a status code (never NULL). */
 const char *flashbev_status_string(int status);

@@ -14,7 +14,7 @@ import os
 from typing import Optional, Sequence, Tuple
 
 __all__ = [
-    "BevGrid", "sample_vt", "launch_info", "status_string", "abi_version", "library_path",
+    "BevGrid", "sample_vt", "sample_vt_backward", "launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
 ]
 
@@ -28,6 +28,7 @@ STATUS = {
     "OK": 0, "ERR_NULLPTR": -1, "ERR_SHAPE": -2, "ERR_DTYPE": -3, "ERR_ALIGN": -4,
     "ERR_UNSUPPORTED": -5, "ERR_ALIAS": -6, "ERR_VALUE": -7, "ERR_HIP": -8,
 }
+ABI_VERSION = 2
 ZMAX = 256
 NMAX = 64
 ROW_BYTES_MAX = 4096
@@ -93,6 +94,10 @@ def _lib():
                                            P(ctypes.c_int32), P(ctypes.c_int32),
                                            P(ctypes.c_int32)]
         L.flashbev_launch_info.restype = ctypes.c_int
+        L.flashbev_sample_vt_backward.argtypes = [P(Features), ctypes.c_void_p, P(GridSpec),
+                                                  P(ZBins), ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p]
+        L.flashbev_sample_vt_backward.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -171,18 +176,82 @@ def sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int
     z = _z_array(z_bins)
     f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
                         grid, z, reduce)
-    if stream is None:
-        s = torch.cuda.current_stream(features.device).cuda_stream
-    elif isinstance(stream, int):
-        s = stream
-    else:
-        s = stream.cuda_stream
+    s = _stream_handle(stream, features.device)
     rc = _lib().flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
                                    ctypes.byref(g), ctypes.byref(zb),
                                    ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
     if rc != 0:
         raise FlashBevError(rc)
     return out
+
+
+def _stream_handle(stream, device):
+    import torch
+
+    if stream is None:
+        return torch.cuda.current_stream(device).cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int],
+                       features_shape, features_dtype="f32", grad_features=None,
+                       reduce: str = "mean", stream=None):
+    """Gradient of the fused Sampling-VT forward with respect to the features.
+
+    grad_out        CUDA float32 tensor [B, C, X, Y] (gradient w.r.t. ``out``).
+    lidar2img       CUDA float32 tensor [B, N, 4, 4].
+    features_shape  (B, N, H, W, C) of the features of the forward call.
+    features_dtype  their dtype ("f32", "f16", "bf16" or a torch dtype).
+    grad_features   optional CUDA float32 tensor [B, N, H, W, C] to write.
+
+    Returns ``grad_features`` (float32, channel-last).  Asynchronous.
+    """
+    import torch
+
+    if not grad_out.is_cuda or not lidar2img.is_cuda:
+        raise ValueError("grad_out and lidar2img must be device tensors")
+    if grad_out.dtype != torch.float32 or not grad_out.is_contiguous():
+        raise ValueError("grad_out must be a contiguous float32 tensor")
+    if lidar2img.dtype != torch.float32 or not lidar2img.is_contiguous():
+        raise ValueError("lidar2img must be a contiguous float32 tensor")
+    B, N, H, W, C = (int(v) for v in features_shape)
+    if tuple(grad_out.shape) != (B, C, grid.X, grid.Y):
+        raise ValueError(f"grad_out must be [{B}, {C}, {grid.X}, {grid.Y}]")
+    if tuple(lidar2img.shape) != (B, N, 4, 4):
+        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
+    if grad_features is None:
+        grad_features = torch.empty((B, N, H, W, C), dtype=torch.float32, device=grad_out.device)
+    elif grad_features.dtype != torch.float32 or not grad_features.is_contiguous() or \
+            tuple(grad_features.shape) != (B, N, H, W, C):
+        raise ValueError(f"grad_features must be a contiguous float32 tensor [{B}, {N}, {H}, {W}, {C}]")
+    if not isinstance(features_dtype, str):
+        features_dtype = {torch.float32: "f32", torch.float16: "f16",
+                          torch.bfloat16: "bf16"}[features_dtype]
+    z = _z_array(z_bins)
+    f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
+    s = _stream_handle(stream, grad_out.device)
+    rc = _lib().flashbev_sample_vt_backward(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
+                                            ctypes.byref(g), ctypes.byref(zb),
+                                            ctypes.c_void_p(grad_out.data_ptr()),
+                                            ctypes.c_void_p(grad_features.data_ptr()),
+                                            ctypes.c_void_p(s))
+    if rc != 0:
+        raise FlashBevError(rc, "flashbev_sample_vt_backward")
+    return grad_features
+
+
+def sample_vt_backward_raw(shape, dtype: str, lidar2img_ptr: int, z_bins, grid: BevGrid,
+                           img_hw, grad_out_ptr: int, grad_features_ptr: int,
+                           reduce: str = "mean", stream: int = 0) -> int:
+    """The backward C entry point with raw device addresses; returns the status."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], 0, img_hw, grid, z, reduce)
+    return int(_lib().flashbev_sample_vt_backward(
+        ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr), ctypes.byref(g), ctypes.byref(zb),
+        ctypes.c_void_p(grad_out_ptr), ctypes.c_void_p(grad_features_ptr),
+        ctypes.c_void_p(stream)))
 
 
 def sample_vt_raw(features_ptr: int, dtype: str, shape, lidar2img_ptr: int, z_bins,

@@ -463,6 +463,262 @@ sample_vt_fwd(const Params p)
 }
 
 // ---------------------------------------------------------------------------
+// backward: gradient with respect to the feature maps
+// ---------------------------------------------------------------------------
+// Eq. 1 is linear in the features; its gradient is the transpose of the
+// forward's map: every valid sample scatters w_t / max(1, den_z) times the
+// output gradient of its cell onto the C channels of each of its four taps.
+// The kernel shares the forward's work split, projection pass and set-up
+// pass; in place of the gather it issues float atomic adds into a float32
+// channel-last gradient (zero-filled by a separate kernel before it).  Lane
+// `slot` of a cell owns channels slot, slot + L, slot + 2L, ..., so each
+// atomic instruction covers a contiguous run of a pixel row.
+struct BwdParams {
+    const float *l2i;
+    const float *gout;       // [B, C, X, Y]
+    float *gfeat;            // [B, N, H, W, C]
+    int32_t B, N, H, W, C, X, Y, Z;
+    int32_t XY;
+    int32_t tiles_per_b;
+    int32_t tile_cells;      // cells per tile = waves * rounds * cpw
+    int32_t rounds;
+    float img_w, img_h;
+    float sx, sy;
+    float x_min, dx, y_min, dy, depth_eps;
+    int32_t reduce;
+    uint32_t step_x;         // element step to the right-hand tap (0 if W == 1)
+    uint32_t step_y;         // element step to the lower tap (0 if H == 1)
+    int32_t lpc;             // lanes per cell
+    int32_t cpw;             // cells per wavefront group
+    float rcp_n, rcp_lpc;
+    int32_t zc;
+    int32_t gtile_ld;        // row pitch (floats) of the LDS output-gradient tile, odd
+    uint32_t lds_z, lds_w, lds_off, lds_gtile;
+    float z[FLASHBEV_ZMAX];
+};
+
+template <int KPL>
+__global__ void __launch_bounds__(kThreadsMax)
+sample_vt_bwd(const BwdParams p)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *s_mat = reinterpret_cast<float *>(smem);
+    float *s_z = reinterpret_cast<float *>(smem + p.lds_z);
+    float4 *s_w = reinterpret_cast<float4 *>(smem + p.lds_w);
+    uint32_t *s_off = reinterpret_cast<uint32_t *>(smem + p.lds_off);
+    float *s_g = reinterpret_cast<float *>(smem + p.lds_gtile);
+
+    const int cpw = p.cpw;
+    const int tid = threadIdx.x;
+    const int nthreads = blockDim.x;
+    const int wave = tid / kWave;
+    const int lane = tid % kWave;
+    const int N = p.N;
+    const int C = p.C;
+
+    // same XCD-aware tile order as the forward
+    const int g = blockIdx.x;
+    const int full = (int)(gridDim.x / (kXcds * kStripe)) * (kXcds * kStripe);
+    int tile = g;
+    if (g < full) {
+        const int xcd = g % kXcds, k = g / kXcds;
+        tile = (k / kStripe) * (kXcds * kStripe) + xcd * kStripe + k % kStripe;
+    }
+    const int b = tile / p.tiles_per_b;
+    const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
+
+    // stage camera matrices, heights and the tile's output gradient
+    // (consecutive threads read consecutive cells of one channel plane)
+    for (int t = tid; t < N * 12; t += nthreads) {
+        const int n = t / 12, r = t - n * 12;
+        s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
+    }
+    for (int t = tid; t < p.Z; t += nthreads) s_z[t] = p.z[t];
+    {
+        const int rem = p.XY - q_tile;
+        const int nq = rem < p.tile_cells ? rem : p.tile_cells;
+        const float *gb = p.gout + (size_t)b * C * p.XY + q_tile;
+        const int rows = nthreads / nq;  // >= 1: a tile has at most nthreads cells
+        const int c0 = div_small(tid, nq, 1.0f / (float)nq);
+        const int k = tid - c0 * nq;
+        if (c0 < rows)
+            for (int c = c0; c < C; c += rows) s_g[c * p.gtile_ld + k] = gb[(size_t)c * p.XY + k];
+    }
+    __syncthreads();
+
+    const int Nd = N > 0 ? N : 1;
+    const int zl = div_small(lane, Nd, p.rcp_n);
+    const int n_p = lane - zl * Nd;
+    const bool p_role = (N > 0) && (zl < p.zc);
+    const int zshift = p_role ? zl * N : 0;
+    const uint64_t nmask = (N >= 64) ? ~0ull : ((1ull << N) - 1ull);
+    float mr[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) mr[k] = p_role ? s_mat[n_p * 12 + k] : 0.0f;
+
+    // scatter role: cell m_g of the group, channels slot + L * kk
+    const int L = p.lpc;
+    const int m_g = div_small(lane, L, p.rcp_lpc);
+    const int slot = lane - m_g * L;
+    const bool in_group = m_g < cpw;
+    const int m_lds = in_group ? m_g : 0;
+
+    float4 *wl = s_w + (size_t)wave * cpw * kRecStride;
+    uint32_t *ol = s_off + (size_t)wave * cpw * kRecStride;
+    const int wcells = p.rounds * cpw;
+    const int q_wave = q_tile + wave * wcells;
+    const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
+
+    float xs = 0.0f, ys = 0.0f;
+    if (lane < wcells && q_wave + lane < p.XY) {
+        const int q = q_wave + lane;
+        const int i = q / p.Y;
+        const int j = q - i * p.Y;
+        xs = p.x_min + ((float)i + 0.5f) * p.dx;
+        ys = p.y_min + ((float)j + 0.5f) * p.dy;
+    }
+
+    for (int r = 0; r < p.rounds; ++r) {
+        const int q_grp = q_wave + r * cpw;
+        const int ncell = (p.XY - q_grp) < cpw ? (p.XY - q_grp) : cpw;
+        const bool g_active = m_g < ncell;
+
+        // this lane's share of the cell's output gradient
+        float gv[KPL];
+        {
+            const int col = wave * wcells + r * cpw + m_lds;
+#pragma unroll
+            for (int kk = 0; kk < KPL; ++kk) {
+                const int c = slot + L * kk;
+                gv[kk] = (g_active && c < C) ? s_g[c * p.gtile_ld + col] : 0.0f;
+            }
+        }
+
+        for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
+            // ---- projection, mask and compaction (as in the forward)
+            const int zi = z0 + zl;
+            const bool l_ok = p_role && zi < p.Z;
+            const float zv = l_ok ? s_z[zi] : 0.0f;
+            const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
+            int total = 0, maxcnt = 0;
+            int cnt_lane = 0, pre_lane = 0;
+            for (int m = 0; m < ncell; ++m) {
+                const float x = bcast(xs, r * cpw + m);
+                const float y = bcast(ys, r * cpw + m);
+                const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
+                const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
+                const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
+                const float u = up / d;
+                const float v = vp / d;
+                const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
+                                (v >= 0.0f) && (v < p.img_h);
+                const uint64_t mask = __ballot(ok);
+                if (ok) {
+                    const int den = __popcll((mask >> zshift) & nmask);
+                    const int pos = __builtin_amdgcn_mbcnt_hi(
+                        (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                    wl[m * kRecStride + pos] =
+                        make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
+                }
+                const int cnt = __popcll(mask);
+                cnt_lane = lane == m ? cnt : cnt_lane;
+                pre_lane = lane == m ? total : pre_lane;
+                total += cnt;
+                maxcnt = cnt > maxcnt ? cnt : maxcnt;
+            }
+            wave_lds_sync();
+
+            // ---- bilinear set-up, dense over the group's valid samples:
+            // tap weights with 1 / max(1, den_z) folded in, element index
+            // of the first tap in the gradient tensor
+            for (int base = 0; base < total; base += kWave) {
+                const int idx = base + lane;
+                int m = 0, pm = 0;
+                for (int mm = 1; mm < ncell; ++mm) {
+                    const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
+                    const bool ge = idx >= pf;
+                    m = ge ? mm : m;
+                    pm = ge ? pf : pm;
+                }
+                if (idx < total) {
+                    const int slotk = m * kRecStride + (idx - pm);
+                    const float4 pr = wl[slotk];
+                    const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
+                    const int den = __builtin_bit_cast(int, pr.w);
+                    const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+                    const float xf = pr.x * p.sx - 0.5f;
+                    const float yf = pr.y * p.sy - 0.5f;
+                    const float x0f = floorf(xf), y0f = floorf(yf);
+                    const float ax = xf - x0f, ay = yf - y0f;
+                    int xa = (int)x0f, ya = (int)y0f;
+                    float wxa = 1.0f - ax, wxb = ax;
+                    float wya = 1.0f - ay, wyb = ay;
+                    if (xa < 0) {
+                        xa = 0; wxa = ax; wxb = 0.0f;
+                    } else if (xa >= p.W - 1) {
+                        if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
+                        else { xa = 0; wxb = 0.0f; }
+                    }
+                    if (ya < 0) {
+                        ya = 0; wya = ay; wyb = 0.0f;
+                    } else if (ya >= p.H - 1) {
+                        if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
+                        else { ya = 0; wyb = 0.0f; }
+                    }
+                    wya *= inv;
+                    wyb *= inv;
+                    const uint32_t pix = ((cam0 + n) * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W +
+                                         (uint32_t)xa;
+                    wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
+                    ol[slotk] = pix * (uint32_t)C;
+                }
+            }
+            wave_lds_sync();
+
+            // ---- scatter: each lane adds its channels' terms to the four
+            // taps; lanes of cells with fewer samples sit out
+            const int mycnt = __shfl(cnt_lane, m_lds);
+            if (g_active) {
+                const float4 *wv = wl + m_lds * kRecStride;
+                const uint32_t *ov = ol + m_lds * kRecStride;
+                for (int k = 0; k < mycnt; ++k) {
+                    const float4 w = wv[k];
+                    float *d = p.gfeat + ov[k] + slot;
+#pragma unroll
+                    for (int kk = 0; kk < KPL; ++kk) {
+                        if (slot + L * kk < C) {
+                            float *dk = d + L * kk;
+                            unsafeAtomicAdd(dk, w.x * gv[kk]);
+                            unsafeAtomicAdd(dk + p.step_x, w.y * gv[kk]);
+                            unsafeAtomicAdd(dk + p.step_y, w.z * gv[kk]);
+                            unsafeAtomicAdd(dk + p.step_x + p.step_y, w.w * gv[kk]);
+                        }
+                    }
+                }
+            }
+            wave_lds_sync();
+        }
+    }
+}
+
+// Zero-fills n floats at dst (any 4-byte alignment): a 16-byte aligned body
+// with vector stores plus scalar head and tail.
+__global__ void __launch_bounds__(256) zero_fill(float *dst, uint64_t n)
+{
+    const uintptr_t a = (uintptr_t)dst;
+    uint64_t head = ((16u - (a & 15u)) & 15u) / 4u;
+    if (head > n) head = n;
+    const uint64_t n4 = (n - head) / 4u;
+    const uint64_t tail0 = head + n4 * 4u;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    const uint64_t t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    float4 *body = reinterpret_cast<float4 *>(dst + head);
+    for (uint64_t i = t0; i < n4; i += stride) body[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (t0 < head) dst[t0] = 0.0f;
+    if (t0 < n - tail0) dst[tail0 + t0] = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
 // host side: validation, geometry, dispatch
 // ---------------------------------------------------------------------------
 using KernelFn = void (*)(const Params);
@@ -634,6 +890,133 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     return FLASHBEV_OK;
 }
 
+// Backward launch plan.  The feature dims come in a flashbev_features whose
+// data pointer is not used; the gradient is float32 whatever the feature
+// dtype.
+struct BwdPlan {
+    BwdParams prm;
+    int64_t workgroups;   // scatter workgroups (0: nothing to scatter)
+    int threads;
+    size_t lds;
+    int kpl;
+    uint64_t gfeat_elems;
+};
+
+using BwdKernelFn = void (*)(const BwdParams);
+
+BwdKernelFn pick_bwd(int kpl)
+{
+    switch (kpl) {
+    case 4: return sample_vt_bwd<4>;
+    case 8: return sample_vt_bwd<8>;
+    case 16: return sample_vt_bwd<16>;
+    default: return sample_vt_bwd<32>;
+    }
+}
+
+int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_grid_spec *s,
+                  const flashbev_z_bins *zb, const float *gout, const float *gfeat, BwdPlan *pl)
+{
+    if (!f || !s || !zb) return FLASHBEV_ERR_NULLPTR;
+    if (f->dtype != FLASHBEV_F32 && f->dtype != FLASHBEV_F16 && f->dtype != FLASHBEV_BF16)
+        return FLASHBEV_ERR_DTYPE;
+    if (f->B < 0 || f->N < 0 || f->C < 1 || f->H < 1 || f->W < 1 || f->img_h < 1 ||
+        f->img_w < 1 || s->X < 0 || s->Y < 0 || zb->Z < 0)
+        return FLASHBEV_ERR_SHAPE;
+    if (zb->Z > FLASHBEV_ZMAX || f->N > FLASHBEV_NMAX) return FLASHBEV_ERR_UNSUPPORTED;
+    if (s->reduce != FLASHBEV_REDUCE_VALID_MEAN && s->reduce != FLASHBEV_REDUCE_SUM)
+        return FLASHBEV_ERR_VALUE;
+    if (!finite(s->x_min) || !finite(s->dx) || !finite(s->y_min) || !finite(s->dy) ||
+        !finite(s->depth_eps))
+        return FLASHBEV_ERR_VALUE;
+    const int es = (f->dtype == FLASHBEV_F32) ? 4 : 2;
+    if ((uint64_t)f->C * es > FLASHBEV_ROW_BYTES_MAX) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t gelems = (uint64_t)f->B * f->N * f->H * f->W * f->C;
+    if (gelems > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t XY = (uint64_t)s->X * s->Y;
+    if (XY > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t out_elems = (uint64_t)f->B * f->C * XY;
+    if (zb->Z > 0 && !zb->z) return FLASHBEV_ERR_NULLPTR;
+    if (gelems > 0) {
+        if (!gfeat) return FLASHBEV_ERR_NULLPTR;
+        if ((uintptr_t)gfeat % 4) return FLASHBEV_ERR_ALIGN;
+    }
+    const bool scatter = gelems > 0 && out_elems > 0 && zb->Z > 0;
+    if (scatter) {
+        if (!gout || !l2i) return FLASHBEV_ERR_NULLPTR;
+        if (((uintptr_t)gout % 4) || ((uintptr_t)l2i % 4)) return FLASHBEV_ERR_ALIGN;
+        const size_t gb = gelems * 4;
+        if (overlaps(gfeat, gb, gout, out_elems * 4) ||
+            overlaps(gfeat, gb, l2i, (size_t)f->B * f->N * 64))
+            return FLASHBEV_ERR_ALIAS;
+    }
+
+    // lanes per cell: one channel per lane and up to four lanes' worth of
+    // channels per lane for narrow rows, at most one wavefront per cell
+    int lpc = (f->C + 3) / 4;
+    if (lpc > kWave) lpc = kWave;
+    const int k_need = (f->C + lpc - 1) / lpc;
+    int kpl = 4;
+    while (kpl < k_need) kpl <<= 1;
+    if (kpl > 32) return FLASHBEV_ERR_UNSUPPORTED;
+    int cpw = kWave / lpc;
+    if (cpw > kCpwMax) cpw = kCpwMax;
+    const int waves = cpw >= kCpwMax ? kWavesMax : 2;
+    int rounds = (kCellsPerWave + cpw - 1) / cpw;
+    auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
+    // same LDS layout as the forward; the output tile holds the gradient
+    LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
+    while (lay.total > kLdsBudget && rounds > 1) {
+        --rounds;
+        lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
+    }
+    if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
+    if (rounds * cpw > kWave) return FLASHBEV_ERR_UNSUPPORTED;
+    const int tile_cells = waves * rounds * cpw;
+
+    BwdParams &p = pl->prm;
+    memset(&p, 0, sizeof(p));
+    p.l2i = l2i;
+    p.gout = gout;
+    p.gfeat = const_cast<float *>(gfeat);
+    p.B = f->B; p.N = f->N; p.H = f->H; p.W = f->W; p.C = f->C;
+    p.X = s->X; p.Y = s->Y; p.Z = zb->Z;
+    p.XY = (int32_t)XY;
+    p.tile_cells = tile_cells;
+    p.rounds = rounds;
+    p.tiles_per_b = (int32_t)((XY + tile_cells - 1) / tile_cells);
+    p.img_w = (float)f->img_w;
+    p.img_h = (float)f->img_h;
+    p.sx = (float)f->W / (float)f->img_w;
+    p.sy = (float)f->H / (float)f->img_h;
+    p.x_min = s->x_min; p.dx = s->dx; p.y_min = s->y_min; p.dy = s->dy;
+    p.depth_eps = s->depth_eps;
+    p.reduce = s->reduce;
+    p.step_x = f->W >= 2 ? (uint32_t)f->C : 0u;
+    p.step_y = f->H >= 2 ? (uint32_t)f->C * (uint32_t)f->W : 0u;
+    p.lpc = lpc;
+    p.cpw = cpw;
+    p.rcp_n = 1.0f / (float)(f->N > 0 ? f->N : 1);
+    p.rcp_lpc = 1.0f / (float)lpc;
+    int zc = f->N > 0 ? kWave / f->N : 1;
+    if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
+    p.zc = zc < 1 ? 1 : zc;
+    p.gtile_ld = pitch(rounds);
+    p.lds_z = lay.z;
+    p.lds_w = lay.w;
+    p.lds_off = lay.off;
+    p.lds_gtile = lay.otile;
+    for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
+
+    pl->workgroups = scatter ? (int64_t)f->B * p.tiles_per_b : 0;
+    if (pl->workgroups > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
+    pl->threads = waves * kWave;
+    pl->lds = lay.total;
+    pl->kpl = kpl;
+    pl->gfeat_elems = gelems;
+    return FLASHBEV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -690,3 +1073,28 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
 }
 
 }  // extern "C"
+
+extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
+                                           const float *lidar2img,
+                                           const flashbev_bev_grid_spec *spec,
+                                           const flashbev_z_bins *z_bins, const float *grad_out,
+                                           float *grad_features, void *stream)
+{
+    BwdPlan pl;
+    const int rc = make_bwd_plan(features, lidar2img, spec, z_bins, grad_out, grad_features, &pl);
+    if (rc) return rc;
+    if (pl.gfeat_elems == 0) return FLASHBEV_OK;
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    uint64_t blocks = (pl.gfeat_elems / 4 + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(zero_fill, dim3((unsigned)blocks), dim3(256), 0, st, grad_features,
+                       pl.gfeat_elems);
+    if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
+    if (pl.workgroups == 0) return FLASHBEV_OK;
+    void *args[] = {&pl.prm};
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(pick_bwd(pl.kpl)),
+                                         dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
+                                         pl.lds, st);
+    return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
+}

@@ -57,7 +57,7 @@ def test_every_header_maps_to_a_library_that_exports_it():
 
 
 def test_abi_version_and_status_strings():
-    assert fb.abi_version() == 1
+    assert fb.abi_version() == fb.ABI_VERSION
     for name, code in fb.STATUS.items():
         s = fb.status_string(code)
         assert s and s != "unknown status"
@@ -67,7 +67,7 @@ def test_abi_version_and_status_strings():
 def test_header_constants_match_binding():
     src = open(HEADER).read()
     for k, v in (("FLASHBEV_ZMAX", fb.ZMAX), ("FLASHBEV_NMAX", fb.NMAX),
-                 ("FLASHBEV_ROW_BYTES_MAX", fb.ROW_BYTES_MAX), ("FLASHBEV_ABI_VERSION", 1)):
+                 ("FLASHBEV_ROW_BYTES_MAX", fb.ROW_BYTES_MAX), ("FLASHBEV_ABI_VERSION", fb.ABI_VERSION)):
         assert re.search(rf"#define {k} {v}\b", src), k
     for k, v in fb.STATUS.items():
         assert re.search(rf"FLASHBEV_{k} = {v}\b", src), k
