@@ -14,7 +14,10 @@ Prints one JSON line with throughput (Gsamples/s, samples = B*X*Y*Z*N
 projected point-camera pairs per call), latency, the roofline of the kernel
 (algorithmic HBM bytes per launch over the measured launch duration, timed
 with HIP events on the launch stream), peak operator memory and the CPU
-oracle timed on the host as a reported baseline.
+oracle timed on the host as a reported baseline.  Unless --no-extra is
+given it also reports two more workloads, the measured memory ceilings and
+the backward (gradient w.r.t. the features) on this workload and on the
+paper's reference setting; --backward-only times just the backward.
 """
 from __future__ import annotations
 
@@ -176,6 +179,55 @@ def make_call(wl, inst, device):
     return fn, feats, l2i, out, stream
 
 
+def make_backward_call(wl, inst, device):
+    """One call of the backward (gradient w.r.t. the features): the fill of
+    the float32 gradient and the scatter kernel, on the current stream."""
+    import numpy as np
+    import torch
+
+    import paper_2607_10071_amd as fb
+
+    rng = np.random.default_rng([wl.cfg_id, 7])
+    gout = torch.from_numpy(rng.standard_normal((wl.B, wl.C, wl.X, wl.Y)).astype(np.float32)).to(device)
+    l2i = torch.from_numpy(inst.lidar2img).to(device)
+    gfeat = torch.empty(inst.features.shape, dtype=torch.float32, device=device)
+    grid = fb.grid_of(wl)
+    img = (wl.img_h, wl.img_w)
+    stream = torch.cuda.current_stream(device)
+    shape = inst.features.shape
+
+    def fn():
+        fb.sample_vt_backward(gout, l2i, inst.z, grid, img, shape, wl.dtype, grad_features=gfeat,
+                              stream=stream)
+
+    return fn, (gout, l2i, gfeat), stream
+
+
+def backward_bytes(wl) -> int:
+    """Compulsory HBM bytes of one backward call: read the output gradient
+    and the matrices once, write the float32 feature gradient once."""
+    return (wl.B * wl.C * wl.X * wl.Y * 4 + wl.B * wl.N * 16 * 4
+            + wl.B * wl.N * wl.H * wl.W * wl.C * 4)
+
+
+def measure_backward(wl, inst, device, steps, warmup, taps=None) -> dict:
+    fn, keep, stream = make_backward_call(wl, inst, device)
+    settle(fn, 0.1)
+    t = time_gpu(fn, steps, warmup, stream)
+    sec = t["ms_per_step"] * 1e-3
+    rec = {"ms": round(t["ms_per_step"], 5),
+           "gsamples_per_s": round(wl.samples / sec / 1e9, 3),
+           "hbm_bytes_per_call": backward_bytes(wl),
+           "hbm_frac": round(backward_bytes(wl) / sec / 1e9 / HBM_PEAK_GBS, 5)}
+    if taps is not None:
+        # every in-range tap adds C float32 terms atomically
+        ab = taps * wl.C * 4
+        rec["atomic_bytes_per_call"] = ab
+        rec["atomic_GBs"] = round(ab / sec / 1e9, 1)
+    del fn, keep
+    return rec
+
+
 def peak_operator_memory(wl, inst, device) -> int:
     import torch
 
@@ -225,6 +277,8 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the secondary workloads reported for context")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time only the backward (gradient w.r.t. the features) on the workload")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB three times "
                          "(a plain copy of known size that scales the HBM byte counters)")
@@ -254,6 +308,11 @@ def main(argv=None) -> int:
         del src, dst
     wl = synth.config(args.workload)
     inst = synth.make_workload(wl)
+    if args.backward_only:
+        rec = {"pass": "backward", "workload": wl.name,
+               **measure_backward(wl, inst, device, args.steps, args.warmup)}
+        print(json.dumps(rec), flush=True)
+        return 0
     fn, feats, l2i, out, stream = make_call(wl, inst, device)
     settle(fn)
     t = time_gpu(fn, args.steps, args.warmup, stream)
@@ -332,6 +391,19 @@ def main(argv=None) -> int:
             "frac": round(g_ach / peak, 4) if peak else None,
             "gather_bytes_per_launch": gather_bytes,
             "valid_samples": counters["valid_samples"], "taps": counters["taps"]}
+
+    if not args.no_extra:
+        # backward (gradient w.r.t. the features) on the same workload and on
+        # the paper's reference setting, whose backward the paper times
+        taps = rec.get("gather_roofline", {}).get("taps")
+        bwd = {wl.name: measure_backward(wl, inst, device, max(20, args.steps // 2), args.warmup,
+                                         taps)}
+        w3 = synth.config("paper_ref")
+        bwd["paper_ref"] = measure_backward(w3, synth.make_workload(w3), device,
+                                            max(20, args.steps // 2), args.warmup)
+        bwd["paper_context"] = {"flashbev_a6000_backward_ms": 3.27,
+                                "tensorized_a6000_backward_ms": 17.90}
+        rec["backward"] = bwd
 
     print(json.dumps(rec), flush=True)
     return 0

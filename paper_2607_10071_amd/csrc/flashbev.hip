@@ -468,11 +468,26 @@ sample_vt_fwd(const Params p)
 // Eq. 1 is linear in the features; its gradient is the transpose of the
 // forward's map: every valid sample scatters w_t / max(1, den_z) times the
 // output gradient of its cell onto the C channels of each of its four taps.
-// The kernel shares the forward's work split, projection pass and set-up
-// pass; in place of the gather it issues float atomic adds into a float32
-// channel-last gradient (zero-filled by a separate kernel before it).  Lane
-// `slot` of a cell owns channels slot, slot + L, slot + 2L, ..., so each
-// atomic instruction covers a contiguous run of a pixel row.
+// The kernel keeps the forward's projection pass and set-up pass; in place
+// of the gather it adds the terms into a float32 channel-last gradient
+// (zero-filled by a separate kernel first).  Lane `slot` of a cell owns
+// channels slot, slot + L, slot + 2L, ..., so each add covers a contiguous
+// run of a pixel row.
+//
+// Global float atomics are the cost: MI355X retires about 2e11 of them per
+// second, whatever the address spread.  In the tiled mode a workgroup owns a
+// 2-D tile of cells, whose samples share most of their taps, and first adds
+// into one LDS row per distinct pixel of the tile; a lock-free LDS hash table
+// maps pixels to rows.  At the end it adds each row to the gradient with one
+// global atomic per channel.  Taps that find the table full go straight to
+// global atomics.  The direct mode (no table) serves shapes whose rows or
+// pixel ids do not fit.
+constexpr uint32_t kSlotNone = 0xFFFFu;   // tap not in the tile's table
+constexpr uint32_t kPixNone = 0xFFFFFFFFu; // LDS row claimed but not used
+constexpr int kKeyBits = 20;              // pixel ids (plus one) per batch element < 2^20
+constexpr uint32_t kKeyMask = (1u << kKeyBits) - 1u;
+constexpr int kSlotMax = (1 << (32 - kKeyBits)) - 1;  // 4095 rows per tile
+
 struct BwdParams {
     const float *l2i;
     const float *gout;       // [B, C, X, Y]
@@ -494,10 +509,102 @@ struct BwdParams {
     int32_t zc;
     int32_t gtile_ld;        // row pitch (floats) of the LDS output-gradient tile, odd
     uint32_t lds_z, lds_w, lds_off, lds_gtile;
+    // tiled mode
+    int32_t tx, ty;          // tile rows (along x) and columns (along y)
+    int32_t tiles_y;         // tiles per tile row
+    float rcp_ty, rcp_c;
+    int32_t cap;             // LDS rows (distinct pixels) per tile
+    uint32_t tbl_mask;       // hash table entries - 1 (power of two >= 2 cap)
+    uint32_t lds_slot, lds_tbl, lds_spix, lds_acc, lds_cnt;
     float z[FLASHBEV_ZMAX];
 };
 
-template <int KPL>
+// Projection of one cell for one height pass (Alg. 2: compute the voxel
+// centre, project into camera n, check validity): lanes hold (height,
+// camera) pairs; valid samples are compacted into rec[] as (u, v, camera,
+// den_z).  Returns the number of valid samples.
+__device__ __forceinline__ int bwd_project_cell(const BwdParams &p, const float (&mr)[12], float t2u,
+                                                float t2v, float t2d, float x, float y, bool l_ok,
+                                                int zshift, uint64_t nmask, int n_p, float4 *rec)
+{
+    const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
+    const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
+    const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
+    const float u = up / d;
+    const float v = vp / d;
+    const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) && (v >= 0.0f) &&
+                    (v < p.img_h);
+    const uint64_t mask = __ballot(ok);
+    if (ok) {
+        const int den = __popcll((mask >> zshift) & nmask);
+        const int pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+        rec[pos] = make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
+    }
+    return __popcll(mask);
+}
+
+// Bilinear set-up of one valid sample (u, v): first tap (xa, ya) and the
+// four weights with 1 / max(1, den_z) folded in; out-of-range taps are moved
+// onto in-range pixels with weight zero (value selects only).
+__device__ __forceinline__ float4 bwd_setup(const BwdParams &p, float u, float v, int den, int &xa,
+                                            int &ya)
+{
+    const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+    const float xf = u * p.sx - 0.5f;
+    const float yf = v * p.sy - 0.5f;
+    const float x0f = floorf(xf), y0f = floorf(yf);
+    const float ax = xf - x0f, ay = yf - y0f;
+    const int xi = (int)x0f, yi = (int)y0f;
+    const bool xl = xi < 0, xh = !xl && xi >= p.W - 1, xw = p.W >= 2;
+    const bool yl = yi < 0, yh = !yl && yi >= p.H - 1, yw = p.H >= 2;
+    xa = xl ? 0 : (xh ? (xw ? p.W - 2 : 0) : xi);
+    ya = yl ? 0 : (yh ? (yw ? p.H - 2 : 0) : yi);
+    const float wxa = xl ? ax : ((xh && xw) ? 0.0f : 1.0f - ax);
+    const float wxb = xl ? 0.0f : (xh ? (xw ? 1.0f - ax : 0.0f) : ax);
+    const float wya = (yl ? ay : ((yh && yw) ? 0.0f : 1.0f - ay)) * inv;
+    const float wyb = (yl ? 0.0f : (yh ? (yw ? 1.0f - ay : 0.0f) : ay)) * inv;
+    return make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
+}
+
+// LDS row of pixel q of the tile (q < 2^20 - 1): find it in the open-
+// addressing table, or claim a row and insert it.  Entries pack
+// (q + 1) | row << 20; 0 is empty.  A row claimed by a lane that then loses
+// the insert race to the same pixel is marked unused.  Returns kSlotNone
+// once the tile has used all its rows (the caller adds to global memory).
+__device__ __forceinline__ uint32_t tile_row(uint32_t q, uint32_t *tbl, uint32_t *spix,
+                                             uint32_t *counter, uint32_t mask, int cap)
+{
+    const uint32_t key = q + 1u;
+    uint32_t h = (key * 0x9E3779B1u) >> 8;
+    uint32_t mine = kSlotNone;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        h &= mask;
+        uint32_t e = tbl[h];
+        if (e == 0u) {
+            if (mine == kSlotNone) {
+                const uint32_t r = atomicAdd(counter, 1u);
+                if (r >= (uint32_t)cap) return kSlotNone;  // full: nothing is inserted
+                mine = r;
+            }
+            e = atomicCAS(&tbl[h], 0u, key | (mine << kKeyBits));
+            if (e == 0u) {
+                spix[mine] = q;
+                return mine;
+            }
+        }
+        if ((e & kKeyMask) == key) {
+            if (mine != kSlotNone) spix[mine] = kPixNone;
+            return e >> kKeyBits;
+        }
+        ++h;
+    }
+    // not reached: the table holds at most cap < mask + 1 pixels
+    if (mine != kSlotNone) spix[mine] = kPixNone;
+    return kSlotNone;
+}
+
+template <int KPL, bool TILED>
 __global__ void __launch_bounds__(kThreadsMax)
 sample_vt_bwd(const BwdParams p)
 {
@@ -507,6 +614,11 @@ sample_vt_bwd(const BwdParams p)
     float4 *s_w = reinterpret_cast<float4 *>(smem + p.lds_w);
     uint32_t *s_off = reinterpret_cast<uint32_t *>(smem + p.lds_off);
     float *s_g = reinterpret_cast<float *>(smem + p.lds_gtile);
+    uint2 *s_slot = reinterpret_cast<uint2 *>(smem + p.lds_slot);
+    uint32_t *s_tbl = reinterpret_cast<uint32_t *>(smem + p.lds_tbl);
+    uint32_t *s_spix = reinterpret_cast<uint32_t *>(smem + p.lds_spix);
+    float *s_acc = reinterpret_cast<float *>(smem + p.lds_acc);
+    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(smem + p.lds_cnt);
 
     const int cpw = p.cpw;
     const int tid = threadIdx.x;
@@ -515,6 +627,7 @@ sample_vt_bwd(const BwdParams p)
     const int lane = tid % kWave;
     const int N = p.N;
     const int C = p.C;
+    const int T = p.tile_cells;
 
     // same XCD-aware tile order as the forward
     const int g = blockIdx.x;
@@ -525,24 +638,49 @@ sample_vt_bwd(const BwdParams p)
         tile = (k / kStripe) * (kXcds * kStripe) + xcd * kStripe + k % kStripe;
     }
     const int b = tile / p.tiles_per_b;
-    const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
+    const int tl = tile - b * p.tiles_per_b;
+    // tile origin: a run of T cells (direct) or a tx x ty block (tiled)
+    int q_tile = 0, i0 = 0, j0 = 0;
+    if constexpr (TILED) {
+        const int ti = tl / p.tiles_y;
+        i0 = ti * p.tx;
+        j0 = (tl - ti * p.tiles_y) * p.ty;
+    } else {
+        q_tile = tl * T;
+    }
+    // cell t of the tile -> grid cell index (or -1 outside the grid)
+    auto cell_of = [&](int t) -> int {
+        if constexpr (TILED) {
+            const int a = div_small(t, p.ty, p.rcp_ty);
+            const int ci = i0 + a, cj = j0 + (t - a * p.ty);
+            return (ci < p.X && cj < p.Y) ? ci * p.Y + cj : -1;
+        } else {
+            return q_tile + t < p.XY ? q_tile + t : -1;
+        }
+    };
 
-    // stage camera matrices, heights and the tile's output gradient
-    // (consecutive threads read consecutive cells of one channel plane)
+    // stage camera matrices, heights and the tile's output gradient; in
+    // the tiled mode also clear the pixel table, row accumulators and
+    // row counter
     for (int t = tid; t < N * 12; t += nthreads) {
         const int n = t / 12, r = t - n * 12;
         s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
     }
     for (int t = tid; t < p.Z; t += nthreads) s_z[t] = p.z[t];
     {
-        const int rem = p.XY - q_tile;
-        const int nq = rem < p.tile_cells ? rem : p.tile_cells;
-        const float *gb = p.gout + (size_t)b * C * p.XY + q_tile;
-        const int rows = nthreads / nq;  // >= 1: a tile has at most nthreads cells
-        const int c0 = div_small(tid, nq, 1.0f / (float)nq);
-        const int k = tid - c0 * nq;
-        if (c0 < rows)
-            for (int c = c0; c < C; c += rows) s_g[c * p.gtile_ld + k] = gb[(size_t)c * p.XY + k];
+        const float *gb = p.gout + (size_t)b * C * p.XY;
+        const int rows = nthreads / T;  // >= 1: a tile has at most nthreads cells
+        const int c0 = div_small(tid, T, 1.0f / (float)T);
+        const int t = tid - c0 * T;
+        const int q = cell_of(t);
+        if (c0 < rows && q >= 0)
+            for (int c = c0; c < C; c += rows) s_g[c * p.gtile_ld + t] = gb[(size_t)c * p.XY + q];
+    }
+    if constexpr (TILED) {
+        for (uint32_t t = tid; t <= p.tbl_mask; t += nthreads) s_tbl[t] = 0u;
+        const int nacc = p.cap * C;
+        for (int t = tid; t < nacc; t += nthreads) s_acc[t] = 0.0f;
+        if (tid == 0) s_cnt[0] = 0u;
     }
     __syncthreads();
 
@@ -565,28 +703,34 @@ sample_vt_bwd(const BwdParams p)
 
     float4 *wl = s_w + (size_t)wave * cpw * kRecStride;
     uint32_t *ol = s_off + (size_t)wave * cpw * kRecStride;
+    uint2 *sl = s_slot + (size_t)wave * cpw * kRecStride;
     const int wcells = p.rounds * cpw;
-    const int q_wave = q_tile + wave * wcells;
     const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
+    const uint32_t pix0 = cam0 * (uint32_t)p.H * (uint32_t)p.W;
 
+    // voxel centres and validity of the wavefront's cells, one per lane
     float xs = 0.0f, ys = 0.0f;
-    if (lane < wcells && q_wave + lane < p.XY) {
-        const int q = q_wave + lane;
-        const int i = q / p.Y;
-        const int j = q - i * p.Y;
-        xs = p.x_min + ((float)i + 0.5f) * p.dx;
-        ys = p.y_min + ((float)j + 0.5f) * p.dy;
+    int cv = 0;
+    if (lane < wcells) {
+        const int q = cell_of(wave * wcells + lane);
+        if (q >= 0) {
+            const int i = q / p.Y;
+            const int j = q - i * p.Y;
+            cv = 1;
+            xs = p.x_min + ((float)i + 0.5f) * p.dx;
+            ys = p.y_min + ((float)j + 0.5f) * p.dy;
+        }
     }
+    const uint64_t cvmask = __ballot(cv != 0);
 
     for (int r = 0; r < p.rounds; ++r) {
-        const int q_grp = q_wave + r * cpw;
-        const int ncell = (p.XY - q_grp) < cpw ? (p.XY - q_grp) : cpw;
-        const bool g_active = m_g < ncell;
+        const int kg = r * cpw + m_lds;
+        const bool g_active = in_group && ((cvmask >> kg) & 1ull);
 
         // this lane's share of the cell's output gradient
         float gv[KPL];
         {
-            const int col = wave * wcells + r * cpw + m_lds;
+            const int col = wave * wcells + kg;
 #pragma unroll
             for (int kk = 0; kk < KPL; ++kk) {
                 const int c = slot + L * kk;
@@ -600,41 +744,27 @@ sample_vt_bwd(const BwdParams p)
             const bool l_ok = p_role && zi < p.Z;
             const float zv = l_ok ? s_z[zi] : 0.0f;
             const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
-            int total = 0, maxcnt = 0;
+            int total = 0;
             int cnt_lane = 0, pre_lane = 0;
-            for (int m = 0; m < ncell; ++m) {
-                const float x = bcast(xs, r * cpw + m);
-                const float y = bcast(ys, r * cpw + m);
-                const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
-                const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
-                const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
-                const float u = up / d;
-                const float v = vp / d;
-                const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
-                                (v >= 0.0f) && (v < p.img_h);
-                const uint64_t mask = __ballot(ok);
-                if (ok) {
-                    const int den = __popcll((mask >> zshift) & nmask);
-                    const int pos = __builtin_amdgcn_mbcnt_hi(
-                        (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    wl[m * kRecStride + pos] =
-                        make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
-                }
-                const int cnt = __popcll(mask);
+            for (int m = 0; m < cpw; ++m) {
+                int cnt = 0;
+                if ((cvmask >> (r * cpw + m)) & 1ull)
+                    cnt = bwd_project_cell(p, mr, t2u, t2v, t2d, bcast(xs, r * cpw + m),
+                                           bcast(ys, r * cpw + m), l_ok, zshift, nmask, n_p,
+                                           wl + m * kRecStride);
                 cnt_lane = lane == m ? cnt : cnt_lane;
                 pre_lane = lane == m ? total : pre_lane;
                 total += cnt;
-                maxcnt = cnt > maxcnt ? cnt : maxcnt;
             }
             wave_lds_sync();
 
             // ---- bilinear set-up, dense over the group's valid samples:
-            // tap weights with 1 / max(1, den_z) folded in, element index
-            // of the first tap in the gradient tensor
+            // weights, element index of the first tap in the gradient and,
+            // in the tiled mode, the LDS rows of the four taps
             for (int base = 0; base < total; base += kWave) {
                 const int idx = base + lane;
                 int m = 0, pm = 0;
-                for (int mm = 1; mm < ncell; ++mm) {
+                for (int mm = 1; mm < cpw; ++mm) {
                     const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
                     const bool ge = idx >= pf;
                     m = ge ? mm : m;
@@ -644,33 +774,19 @@ sample_vt_bwd(const BwdParams p)
                     const int slotk = m * kRecStride + (idx - pm);
                     const float4 pr = wl[slotk];
                     const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
-                    const int den = __builtin_bit_cast(int, pr.w);
-                    const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
-                    const float xf = pr.x * p.sx - 0.5f;
-                    const float yf = pr.y * p.sy - 0.5f;
-                    const float x0f = floorf(xf), y0f = floorf(yf);
-                    const float ax = xf - x0f, ay = yf - y0f;
-                    int xa = (int)x0f, ya = (int)y0f;
-                    float wxa = 1.0f - ax, wxb = ax;
-                    float wya = 1.0f - ay, wyb = ay;
-                    if (xa < 0) {
-                        xa = 0; wxa = ax; wxb = 0.0f;
-                    } else if (xa >= p.W - 1) {
-                        if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
-                        else { xa = 0; wxb = 0.0f; }
+                    int xa, ya;
+                    wl[slotk] = bwd_setup(p, pr.x, pr.y, __builtin_bit_cast(int, pr.w), xa, ya);
+                    const uint32_t q = (n * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W + (uint32_t)xa;
+                    ol[slotk] = (pix0 + q) * (uint32_t)C;
+                    if constexpr (TILED) {
+                        const uint32_t dxp = p.step_x ? 1u : 0u;
+                        const uint32_t dyp = p.step_y ? (uint32_t)p.W : 0u;
+                        const uint32_t r0 = tile_row(q, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
+                        const uint32_t r1 = tile_row(q + dxp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
+                        const uint32_t r2 = tile_row(q + dyp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
+                        const uint32_t r3 = tile_row(q + dxp + dyp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
+                        sl[slotk] = make_uint2(r0 | (r1 << 16), r2 | (r3 << 16));
                     }
-                    if (ya < 0) {
-                        ya = 0; wya = ay; wyb = 0.0f;
-                    } else if (ya >= p.H - 1) {
-                        if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
-                        else { ya = 0; wyb = 0.0f; }
-                    }
-                    wya *= inv;
-                    wyb *= inv;
-                    const uint32_t pix = ((cam0 + n) * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W +
-                                         (uint32_t)xa;
-                    wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
-                    ol[slotk] = pix * (uint32_t)C;
                 }
             }
             wave_lds_sync();
@@ -681,22 +797,49 @@ sample_vt_bwd(const BwdParams p)
             if (g_active) {
                 const float4 *wv = wl + m_lds * kRecStride;
                 const uint32_t *ov = ol + m_lds * kRecStride;
+                const uint2 *sv = sl + m_lds * kRecStride;
                 for (int k = 0; k < mycnt; ++k) {
                     const float4 w = wv[k];
+                    const float wt[4] = {w.x, w.y, w.z, w.w};
+                    const uint32_t toff[4] = {0u, p.step_x, p.step_y, p.step_x + p.step_y};
                     float *d = p.gfeat + ov[k] + slot;
+                    uint32_t rw[4] = {kSlotNone, kSlotNone, kSlotNone, kSlotNone};
+                    if constexpr (TILED) {
+                        const uint2 sr = sv[k];
+                        rw[0] = sr.x & 0xFFFFu; rw[1] = sr.x >> 16;
+                        rw[2] = sr.y & 0xFFFFu; rw[3] = sr.y >> 16;
+                    }
 #pragma unroll
-                    for (int kk = 0; kk < KPL; ++kk) {
-                        if (slot + L * kk < C) {
-                            float *dk = d + L * kk;
-                            unsafeAtomicAdd(dk, w.x * gv[kk]);
-                            unsafeAtomicAdd(dk + p.step_x, w.y * gv[kk]);
-                            unsafeAtomicAdd(dk + p.step_y, w.z * gv[kk]);
-                            unsafeAtomicAdd(dk + p.step_x + p.step_y, w.w * gv[kk]);
+                    for (int t = 0; t < 4; ++t) {
+                        if (TILED && rw[t] != kSlotNone) {
+                            float *a = s_acc + rw[t] * (uint32_t)C + slot;
+#pragma unroll
+                            for (int kk = 0; kk < KPL; ++kk)
+                                if (slot + L * kk < C) atomicAdd(a + L * kk, wt[t] * gv[kk]);
+                        } else {
+#pragma unroll
+                            for (int kk = 0; kk < KPL; ++kk)
+                                if (slot + L * kk < C)
+                                    unsafeAtomicAdd(d + toff[t] + L * kk, wt[t] * gv[kk]);
                         }
                     }
                 }
             }
             wave_lds_sync();
+        }
+    }
+
+    if constexpr (TILED) {
+        // ---- one global add per channel of each distinct pixel's row
+        __syncthreads();
+        const uint32_t used = s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap;
+        const int n_el = (int)used * C;
+        for (int t = tid; t < n_el; t += nthreads) {
+            const int row = div_small(t, C, p.rcp_c);
+            const uint32_t q = s_spix[row];
+            const float v = s_acc[t];
+            if (q != kPixNone && v != 0.0f)
+                unsafeAtomicAdd(p.gfeat + (size_t)(pix0 + q) * C + (t - row * C), v);
         }
     }
 }
@@ -899,19 +1042,26 @@ struct BwdPlan {
     int threads;
     size_t lds;
     int kpl;
+    bool tiled;
     uint64_t gfeat_elems;
 };
 
 using BwdKernelFn = void (*)(const BwdParams);
 
-BwdKernelFn pick_bwd(int kpl)
+template <bool TILED>
+BwdKernelFn pick_bwd_kpl(int kpl)
 {
     switch (kpl) {
-    case 4: return sample_vt_bwd<4>;
-    case 8: return sample_vt_bwd<8>;
-    case 16: return sample_vt_bwd<16>;
-    default: return sample_vt_bwd<32>;
+    case 4: return sample_vt_bwd<4, TILED>;
+    case 8: return sample_vt_bwd<8, TILED>;
+    case 16: return sample_vt_bwd<16, TILED>;
+    default: return sample_vt_bwd<32, TILED>;
     }
+}
+
+BwdKernelFn pick_bwd(int kpl, bool tiled)
+{
+    return tiled ? pick_bwd_kpl<true>(kpl) : pick_bwd_kpl<false>(kpl);
 }
 
 int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_grid_spec *s,
@@ -972,7 +1122,49 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     }
     if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
     if (rounds * cpw > kWave) return FLASHBEV_ERR_UNSUPPORTED;
-    const int tile_cells = waves * rounds * cpw;
+    int tile_cells = waves * rounds * cpw;
+
+    // tiled mode: 4 wavefronts of one group each on a 2-D tile with four
+    // cells per tile row, and the rest of the LDS budget as per-pixel rows
+    const uint64_t npix = (uint64_t)f->N * f->H * f->W;
+    bool tiled = false;
+    int t_waves = 0, t_tx = 0, t_ty = 0, t_cap = 0;
+    uint32_t t_mask = 0, l_slot = 0, l_tbl = 0, l_spix = 0, l_acc = 0, l_cnt = 0, l_total = 0;
+    int t_pitch = 0;
+    if (npix + 1 < (1u << kKeyBits) && cpw >= 2) {
+        t_waves = kWavesMax;
+        const int T = t_waves * cpw;
+        t_ty = (T % 4 == 0) ? 4 : T;
+        t_tx = T / t_ty;
+        t_pitch = T | 1;
+        const LdsLayout base = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
+        uint32_t o = base.total;
+        l_slot = o; o = align16(o + (uint32_t)t_waves * cpw * kRecStride * 8u);
+        l_cnt = o; o = align16(o + 4u);
+        // per row: C floats, one pixel id and two table entries
+        const uint32_t per_row = (uint32_t)f->C * 4u + 4u + 8u;
+        int cap = o < kLdsBudget ? (int)((kLdsBudget - o) / per_row) : 0;
+        if (cap > kSlotMax - 1) cap = kSlotMax - 1;
+        uint32_t entries = 1;
+        while (entries < 2u * (uint32_t)cap) entries <<= 1;
+        // the table is a power of two: shrink the rows until everything fits
+        while (cap >= 16 && o + align16(entries * 4u) + align16((uint32_t)cap * 4u) +
+                                    align16((uint32_t)cap * f->C * 4u) > kLdsBudget) {
+            --cap;
+            entries = 1;
+            while (entries < 2u * (uint32_t)cap) entries <<= 1;
+        }
+        if (cap >= 16) {
+            l_tbl = o; o = align16(o + entries * 4u);
+            l_spix = o; o = align16(o + (uint32_t)cap * 4u);
+            l_acc = o; o = align16(o + (uint32_t)cap * f->C * 4u);
+            l_total = o;
+            t_cap = cap;
+            t_mask = entries - 1u;
+            tiled = true;
+        }
+    }
+    if (tiled) tile_cells = t_waves * cpw;
 
     BwdParams &p = pl->prm;
     memset(&p, 0, sizeof(p));
@@ -983,8 +1175,23 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     p.X = s->X; p.Y = s->Y; p.Z = zb->Z;
     p.XY = (int32_t)XY;
     p.tile_cells = tile_cells;
-    p.rounds = rounds;
+    p.rounds = tiled ? 1 : rounds;
     p.tiles_per_b = (int32_t)((XY + tile_cells - 1) / tile_cells);
+    if (tiled) {
+        p.tx = t_tx;
+        p.ty = t_ty;
+        p.tiles_y = (s->Y + t_ty - 1) / t_ty;
+        p.tiles_per_b = ((s->X + t_tx - 1) / t_tx) * p.tiles_y;
+        p.rcp_ty = 1.0f / (float)t_ty;
+        p.rcp_c = 1.0f / (float)f->C;
+        p.cap = t_cap;
+        p.tbl_mask = t_mask;
+        p.lds_slot = l_slot;
+        p.lds_tbl = l_tbl;
+        p.lds_spix = l_spix;
+        p.lds_acc = l_acc;
+        p.lds_cnt = l_cnt;
+    }
     p.img_w = (float)f->img_w;
     p.img_h = (float)f->img_h;
     p.sx = (float)f->W / (float)f->img_w;
@@ -1001,7 +1208,8 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
     p.zc = zc < 1 ? 1 : zc;
-    p.gtile_ld = pitch(rounds);
+    p.gtile_ld = tiled ? t_pitch : pitch(rounds);
+    if (tiled) lay = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
     p.lds_z = lay.z;
     p.lds_w = lay.w;
     p.lds_off = lay.off;
@@ -1010,9 +1218,10 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
 
     pl->workgroups = scatter ? (int64_t)f->B * p.tiles_per_b : 0;
     if (pl->workgroups > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
-    pl->threads = waves * kWave;
-    pl->lds = lay.total;
+    pl->threads = (tiled ? t_waves : waves) * kWave;
+    pl->lds = tiled ? l_total : lay.total;
     pl->kpl = kpl;
+    pl->tiled = tiled;
     pl->gfeat_elems = gelems;
     return FLASHBEV_OK;
 }
@@ -1093,7 +1302,7 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
     if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
     if (pl.workgroups == 0) return FLASHBEV_OK;
     void *args[] = {&pl.prm};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(pick_bwd(pl.kpl)),
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled)),
                                          dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
                                          pl.lds, st);
     return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
