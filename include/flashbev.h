@@ -165,6 +165,20 @@ int flashbev_sample_vt_backward(const flashbev_features *features, const float *
                                 const flashbev_z_bins *z_bins, const float *grad_out,
                                 float *grad_features, void *stream);
 
+/*
+ * Launch geometry of flashbev_sample_vt_backward for these arguments: the
+ * scatter kernel's workgroup count (0 when only the fill runs), threads per
+ * workgroup, dynamic LDS bytes per workgroup, the LDS rows (distinct feature
+ * pixels) a tile can accumulate (0 when the kernel adds every term with a
+ * global atomic) and the lanes per BEV cell.  Same shape checks as the
+ * backward; no device pointer is needed and no HIP call is made.
+ */
+int flashbev_backward_launch_info(const flashbev_features *features,
+                                  const flashbev_bev_grid_spec *spec,
+                                  const flashbev_z_bins *z_bins, int64_t *workgroups,
+                                  int32_t *threads_per_workgroup, int32_t *lds_bytes,
+                                  int32_t *rows_per_tile, int32_t *lanes_per_cell);
+
 /* Static, human-readable text for a status code (never NULL). */
 const char *flashbev_status_string(int status);
 

@@ -14,7 +14,7 @@ import os
 from typing import Optional, Sequence, Tuple
 
 __all__ = [
-    "BevGrid", "sample_vt", "sample_vt_backward", "launch_info", "status_string", "abi_version", "library_path",
+    "BevGrid", "sample_vt", "sample_vt_backward", "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
 ]
 
@@ -98,6 +98,11 @@ def _lib():
                                                   P(ZBins), ctypes.c_void_p, ctypes.c_void_p,
                                                   ctypes.c_void_p]
         L.flashbev_sample_vt_backward.restype = ctypes.c_int
+        L.flashbev_backward_launch_info.argtypes = [P(Features), P(GridSpec), P(ZBins),
+                                                    P(ctypes.c_int64), P(ctypes.c_int32),
+                                                    P(ctypes.c_int32), P(ctypes.c_int32),
+                                                    P(ctypes.c_int32)]
+        L.flashbev_backward_launch_info.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -287,3 +292,23 @@ def launch_info(shape, dtype: str, z_bins, grid: BevGrid, img_hw, reduce: str = 
 def grid_of(wl) -> BevGrid:
     """BevGrid of a workload description with x_min/dx/X/y_min/dy/Y fields."""
     return BevGrid(wl.x_min, wl.dx, wl.X, wl.y_min, wl.dy, wl.Y, wl.depth_eps)
+
+
+def backward_launch_info(shape, dtype: str, z_bins, grid: BevGrid, img_hw,
+                         reduce: str = "mean") -> dict:
+    """Launch geometry of the backward for these arguments (no HIP call)."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], 0, img_hw, grid, z, reduce)
+    wg = ctypes.c_int64()
+    thr = ctypes.c_int32()
+    lds = ctypes.c_int32()
+    rows = ctypes.c_int32()
+    lpc = ctypes.c_int32()
+    rc = _lib().flashbev_backward_launch_info(ctypes.byref(f), ctypes.byref(g), ctypes.byref(zb),
+                                              ctypes.byref(wg), ctypes.byref(thr),
+                                              ctypes.byref(lds), ctypes.byref(rows),
+                                              ctypes.byref(lpc))
+    if rc != 0:
+        raise FlashBevError(rc, "flashbev_backward_launch_info")
+    return {"workgroups": wg.value, "threads": thr.value, "lds_bytes": lds.value,
+            "rows_per_tile": rows.value, "lanes_per_cell": lpc.value}

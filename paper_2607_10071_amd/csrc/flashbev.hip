@@ -62,6 +62,7 @@ constexpr int kStripe = 16;               // consecutive tiles per XCD stripe
 constexpr uint32_t kNoTap = 0x80000000u;
 constexpr uint64_t kFeatBytesMax = 0x7FFFFFFFull;
 constexpr uint32_t kLdsBudget = 64u * 1024u;   // dynamic LDS per workgroup
+constexpr uint32_t kLdsBudgetBwd = 80u * 1024u;  // tiled backward: two workgroups per CU
 
 struct Params {
     const void *feat;
@@ -474,14 +475,17 @@ sample_vt_fwd(const Params p)
 // channels slot, slot + L, slot + 2L, ..., so each add covers a contiguous
 // run of a pixel row.
 //
-// Global float atomics are the cost: MI355X retires about 2e11 of them per
-// second, whatever the address spread.  In the tiled mode a workgroup owns a
-// 2-D tile of cells, whose samples share most of their taps, and first adds
-// into one LDS row per distinct pixel of the tile; a lock-free LDS hash table
-// maps pixels to rows.  At the end it adds each row to the gradient with one
-// global atomic per channel.  Taps that find the table full go straight to
-// global atomics.  The direct mode (no table) serves shapes whose rows or
-// pixel ids do not fit.
+// Float atomics are the cost: MI355X retires about 2e11 float atomic adds
+// per second, in LDS as in global memory, whatever the address spread, while
+// integer LDS atomics run some 28 times faster.  In the tiled mode a
+// workgroup owns a 2-D tile of cells, whose samples share most of their taps,
+// and gives each distinct pixel of the tile an LDS row (a lock-free LDS hash
+// table with integer atomics maps pixels to rows).  After each height pass it
+// sorts the pass's (sample, tap) terms by row (integer counts, a prefix sum,
+// a fill), and one wavefront per row sums its terms into the row with plain
+// FMAs.  At the end each row goes to the gradient with one global atomic per
+// channel.  Taps that find the table full go straight to global atomics.  The
+// direct mode (no table) serves shapes whose rows or pixel ids do not fit.
 constexpr uint32_t kSlotNone = 0xFFFFu;   // tap not in the tile's table
 constexpr uint32_t kPixNone = 0xFFFFFFFFu; // LDS row claimed but not used
 constexpr int kKeyBits = 20;              // pixel ids (plus one) per batch element < 2^20
@@ -516,6 +520,7 @@ struct BwdParams {
     int32_t cap;             // LDS rows (distinct pixels) per tile
     uint32_t tbl_mask;       // hash table entries - 1 (power of two >= 2 cap)
     uint32_t lds_slot, lds_tbl, lds_spix, lds_acc, lds_cnt;
+    uint32_t lds_rcnt, lds_rbase, lds_rfill, lds_list;
     float z[FLASHBEV_ZMAX];
 };
 
@@ -567,41 +572,37 @@ __device__ __forceinline__ float4 bwd_setup(const BwdParams &p, float u, float v
     return make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
 }
 
-// LDS row of pixel q of the tile (q < 2^20 - 1): find it in the open-
-// addressing table, or claim a row and insert it.  Entries pack
-// (q + 1) | row << 20; 0 is empty.  A row claimed by a lane that then loses
-// the insert race to the same pixel is marked unused.  Returns kSlotNone
-// once the tile has used all its rows (the caller adds to global memory).
-__device__ __forceinline__ uint32_t tile_row(uint32_t q, uint32_t *tbl, uint32_t *spix,
-                                             uint32_t *counter, uint32_t mask, int cap)
+// Table entry of pixel q of the tile (q < 2^20 - 1): find it in the open-
+// addressing table or insert it.  Entries pack (q + 1) | row << 20, with row
+// kRowUnset until the pass's row assignment gives the pixel an LDS row; 0
+// is empty.  Returns the entry's index, or kSlotNone when the table is full
+// (the caller then adds the tap to global memory).
+constexpr uint32_t kRowUnset = (1u << (32 - kKeyBits)) - 1u;
+
+__device__ __forceinline__ uint32_t tile_insert(uint32_t q, uint32_t *tbl, uint32_t mask)
 {
     const uint32_t key = q + 1u;
     uint32_t h = (key * 0x9E3779B1u) >> 8;
-    uint32_t mine = kSlotNone;
     for (uint32_t probe = 0; probe <= mask; ++probe) {
         h &= mask;
         uint32_t e = tbl[h];
         if (e == 0u) {
-            if (mine == kSlotNone) {
-                const uint32_t r = atomicAdd(counter, 1u);
-                if (r >= (uint32_t)cap) return kSlotNone;  // full: nothing is inserted
-                mine = r;
-            }
-            e = atomicCAS(&tbl[h], 0u, key | (mine << kKeyBits));
-            if (e == 0u) {
-                spix[mine] = q;
-                return mine;
-            }
+            e = atomicCAS(&tbl[h], 0u, key | (kRowUnset << kKeyBits));
+            if (e == 0u) return h;
         }
-        if ((e & kKeyMask) == key) {
-            if (mine != kSlotNone) spix[mine] = kPixNone;
-            return e >> kKeyBits;
-        }
+        if ((e & kKeyMask) == key) return h;
         ++h;
     }
-    // not reached: the table holds at most cap < mask + 1 pixels
-    if (mine != kSlotNone) spix[mine] = kPixNone;
     return kSlotNone;
+}
+
+// LDS row of table entry h (kSlotNone when h is kSlotNone or the pixel got
+// no row because the tile's rows ran out).
+__device__ __forceinline__ uint32_t tile_row_of(const uint32_t *tbl, uint32_t h)
+{
+    if (h == kSlotNone) return kSlotNone;
+    const uint32_t r = tbl[h] >> kKeyBits;
+    return r == kRowUnset ? kSlotNone : r;
 }
 
 template <int KPL, bool TILED>
@@ -618,7 +619,11 @@ sample_vt_bwd(const BwdParams p)
     uint32_t *s_tbl = reinterpret_cast<uint32_t *>(smem + p.lds_tbl);
     uint32_t *s_spix = reinterpret_cast<uint32_t *>(smem + p.lds_spix);
     float *s_acc = reinterpret_cast<float *>(smem + p.lds_acc);
-    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(smem + p.lds_cnt);
+    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(smem + p.lds_cnt);  // [0] rows, [1] overflow
+    uint32_t *s_rcnt = reinterpret_cast<uint32_t *>(smem + p.lds_rcnt);
+    uint32_t *s_rbase = reinterpret_cast<uint32_t *>(smem + p.lds_rbase);
+    uint32_t *s_rfill = reinterpret_cast<uint32_t *>(smem + p.lds_rfill);
+    uint32_t *s_list = reinterpret_cast<uint32_t *>(smem + p.lds_list);
 
     const int cpw = p.cpw;
     const int tid = threadIdx.x;
@@ -680,7 +685,8 @@ sample_vt_bwd(const BwdParams p)
         for (uint32_t t = tid; t <= p.tbl_mask; t += nthreads) s_tbl[t] = 0u;
         const int nacc = p.cap * C;
         for (int t = tid; t < nacc; t += nthreads) s_acc[t] = 0.0f;
-        if (tid == 0) s_cnt[0] = 0u;
+        for (int t = tid; t < p.cap; t += nthreads) s_rcnt[t] = 0u;
+        if (tid == 0) { s_cnt[0] = 0u; s_cnt[1] = 0u; }
     }
     __syncthreads();
 
@@ -779,22 +785,116 @@ sample_vt_bwd(const BwdParams p)
                     const uint32_t q = (n * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W + (uint32_t)xa;
                     ol[slotk] = (pix0 + q) * (uint32_t)C;
                     if constexpr (TILED) {
+                        // table entries of the four taps' pixels
                         const uint32_t dxp = p.step_x ? 1u : 0u;
                         const uint32_t dyp = p.step_y ? (uint32_t)p.W : 0u;
-                        const uint32_t r0 = tile_row(q, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
-                        const uint32_t r1 = tile_row(q + dxp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
-                        const uint32_t r2 = tile_row(q + dyp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
-                        const uint32_t r3 = tile_row(q + dxp + dyp, s_tbl, s_spix, s_cnt, p.tbl_mask, p.cap);
-                        sl[slotk] = make_uint2(r0 | (r1 << 16), r2 | (r3 << 16));
+                        const uint32_t h0 = tile_insert(q, s_tbl, p.tbl_mask);
+                        const uint32_t h1 = tile_insert(q + dxp, s_tbl, p.tbl_mask);
+                        const uint32_t h2 = tile_insert(q + dyp, s_tbl, p.tbl_mask);
+                        const uint32_t h3 = tile_insert(q + dxp + dyp, s_tbl, p.tbl_mask);
+                        sl[slotk] = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
                     }
                 }
             }
             wave_lds_sync();
 
+            if constexpr (TILED) {
+                // ---- rows for the pixels first seen in this pass: one claim
+                // per table entry, so every distinct pixel gets one row
+                __syncthreads();
+                for (uint32_t h = tid; h <= p.tbl_mask; h += nthreads) {
+                    const uint32_t e = s_tbl[h];
+                    if (e != 0u && (e >> kKeyBits) == kRowUnset) {
+                        const uint32_t r = atomicAdd(&s_cnt[0], 1u);
+                        if (r < (uint32_t)p.cap) {
+                            s_tbl[h] = (e & kKeyMask) | (r << kKeyBits);
+                            s_spix[r] = (e & kKeyMask) - 1u;
+                        } else {
+                            // no rows left: the pixel's taps go to global memory
+                            s_cnt[1] = 1u;
+                        }
+                    }
+                }
+                __syncthreads();
+                // ---- count the pass's terms per row (integer LDS atomics)
+                for (int base = 0; base < total; base += kWave) {
+                    const int idx = base + lane;
+                    int m = 0, pm = 0;
+                    for (int mm = 1; mm < cpw; ++mm) {
+                        const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
+                        const bool ge = idx >= pf;
+                        m = ge ? mm : m;
+                        pm = ge ? pf : pm;
+                    }
+                    if (idx < total) {
+                        const uint2 sh = sl[m * kRecStride + (idx - pm)];
+                        const uint32_t hh[4] = {sh.x & 0xFFFFu, sh.x >> 16, sh.y & 0xFFFFu, sh.y >> 16};
+                        bool none = false;
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const uint32_t r = tile_row_of(s_tbl, hh[t]);
+                            if (r != kSlotNone) atomicAdd(&s_rcnt[r], 1u);
+                            else none = true;
+                        }
+                        if (none) s_cnt[1] = 1u;
+                    }
+                }
+                // ---- sort the pass's terms by row: prefix of the counts (one
+                // wavefront), then each term claims a place in its row's run
+                __syncthreads();
+                const int nr = (int)(s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap);
+                if (wave == 0) {
+                    const int per = (nr + kWave - 1) / kWave;
+                    const int r0 = lane * per < nr ? lane * per : nr;
+                    const int r1 = r0 + per < nr ? r0 + per : nr;
+                    uint32_t sum = 0;
+                    for (int q = r0; q < r1; ++q) sum += s_rcnt[q];
+                    uint32_t incl = sum;
+#pragma unroll
+                    for (int d = 1; d < kWave; d <<= 1) {
+                        const uint32_t t = __shfl_up(incl, d);
+                        if (lane >= d) incl += t;
+                    }
+                    uint32_t run = incl - sum;
+                    for (int q = r0; q < r1; ++q) {
+                        s_rbase[q] = run;
+                        s_rfill[q] = run;
+                        run += s_rcnt[q];
+                        s_rcnt[q] = 0u;
+                    }
+                    if (lane == kWave - 1) s_rbase[nr] = incl;
+                }
+                __syncthreads();
+                for (int base = 0; base < total; base += kWave) {
+                    const int idx = base + lane;
+                    int m = 0, pm = 0;
+                    for (int mm = 1; mm < cpw; ++mm) {
+                        const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
+                        const bool ge = idx >= pf;
+                        m = ge ? mm : m;
+                        pm = ge ? pf : pm;
+                    }
+                    if (idx < total) {
+                        const int slotk = m * kRecStride + (idx - pm);
+                        const uint2 sh = sl[slotk];
+                        const uint32_t rr[4] = {tile_row_of(s_tbl, sh.x & 0xFFFFu), tile_row_of(s_tbl, sh.x >> 16),
+                                                tile_row_of(s_tbl, sh.y & 0xFFFFu), tile_row_of(s_tbl, sh.y >> 16)};
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            if (rr[t] != kSlotNone) {
+                                const uint32_t pos = atomicAdd(&s_rfill[rr[t]], 1u);
+                                s_list[pos] = ((uint32_t)wave << 14) | ((uint32_t)slotk << 2) | (uint32_t)t;
+                            }
+                        }
+                    }
+                }
+            }
+
             // ---- scatter: each lane adds its channels' terms to the four
-            // taps; lanes of cells with fewer samples sit out
+            // taps; lanes of cells with fewer samples sit out.  In the tiled
+            // mode only taps without an LDS row (table full) come here.
             const int mycnt = __shfl(cnt_lane, m_lds);
-            if (g_active) {
+            if (g_active && (!TILED || s_cnt[1] != 0u)) {
                 const float4 *wv = wl + m_lds * kRecStride;
                 const uint32_t *ov = ol + m_lds * kRecStride;
                 const uint2 *sv = sl + m_lds * kRecStride;
@@ -805,18 +905,15 @@ sample_vt_bwd(const BwdParams p)
                     float *d = p.gfeat + ov[k] + slot;
                     uint32_t rw[4] = {kSlotNone, kSlotNone, kSlotNone, kSlotNone};
                     if constexpr (TILED) {
-                        const uint2 sr = sv[k];
-                        rw[0] = sr.x & 0xFFFFu; rw[1] = sr.x >> 16;
-                        rw[2] = sr.y & 0xFFFFu; rw[3] = sr.y >> 16;
+                        const uint2 sh = sv[k];
+                        rw[0] = tile_row_of(s_tbl, sh.x & 0xFFFFu);
+                        rw[1] = tile_row_of(s_tbl, sh.x >> 16);
+                        rw[2] = tile_row_of(s_tbl, sh.y & 0xFFFFu);
+                        rw[3] = tile_row_of(s_tbl, sh.y >> 16);
                     }
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        if (TILED && rw[t] != kSlotNone) {
-                            float *a = s_acc + rw[t] * (uint32_t)C + slot;
-#pragma unroll
-                            for (int kk = 0; kk < KPL; ++kk)
-                                if (slot + L * kk < C) atomicAdd(a + L * kk, wt[t] * gv[kk]);
-                        } else {
+                        if (!TILED || rw[t] == kSlotNone) {
 #pragma unroll
                             for (int kk = 0; kk < KPL; ++kk)
                                 if (slot + L * kk < C)
@@ -825,7 +922,47 @@ sample_vt_bwd(const BwdParams p)
                     }
                 }
             }
-            wave_lds_sync();
+
+            if constexpr (TILED) {
+                // ---- one wavefront per row: sum the row's terms into it
+                // (lanes over channels, the term's weight and cell uniform)
+                __syncthreads();
+                const int nr = (int)(s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap);
+                const float *s_wf = reinterpret_cast<const float *>(s_w);
+                const int wstride = cpw * kRecStride;
+                const int nwaves = nthreads / kWave;
+                for (int row = wave; row < nr; row += nwaves) {
+                    const uint32_t e0 = s_rbase[row], n = s_rbase[row + 1] - e0;
+                    for (uint32_t k0 = 0; k0 < n; k0 += kWave) {
+                        const uint32_t kn = n - k0 < (uint32_t)kWave ? n - k0 : (uint32_t)kWave;
+                        // lane i decodes term k0 + i: its weight and its cell's column
+                        float wi = 0.0f;
+                        uint32_t coli = 0;
+                        if ((uint32_t)lane < kn) {
+                            const uint32_t ent = s_list[e0 + k0 + lane];
+                            const uint32_t we = ent >> 14, sk = (ent >> 2) & 0xFFFu, t = ent & 3u;
+                            wi = s_wf[((we * wstride) + sk) * 4u + t];
+                            coli = we * wcells + r * cpw + sk / kRecStride;
+                        }
+                        for (int c0 = 0; c0 < C; c0 += kWave) {
+                            const int c = c0 + lane;
+                            const float *gc = s_g + (c < C ? c : C - 1) * p.gtile_ld;
+                            float sum = 0.0f;
+#pragma unroll 4
+                            for (uint32_t k = 0; k < kn; ++k) {
+                                const float w = __builtin_bit_cast(
+                                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
+                                const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
+                                sum = fmaf(w, gc[col], sum);
+                            }
+                            if (c < C) s_acc[row * C + c] += sum;
+                        }
+                    }
+                }
+                __syncthreads();
+            } else {
+                wave_lds_sync();
+            }
         }
     }
 
@@ -1064,8 +1201,10 @@ BwdKernelFn pick_bwd(int kpl, bool tiled)
     return tiled ? pick_bwd_kpl<true>(kpl) : pick_bwd_kpl<false>(kpl);
 }
 
+// All argument checks; `need_data` requires the device pointers.
 int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_grid_spec *s,
-                  const flashbev_z_bins *zb, const float *gout, const float *gfeat, BwdPlan *pl)
+                  const flashbev_z_bins *zb, const float *gout, const float *gfeat, bool need_data,
+                  BwdPlan *pl)
 {
     if (!f || !s || !zb) return FLASHBEV_ERR_NULLPTR;
     if (f->dtype != FLASHBEV_F32 && f->dtype != FLASHBEV_F16 && f->dtype != FLASHBEV_BF16)
@@ -1087,12 +1226,12 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     if (XY > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
     const uint64_t out_elems = (uint64_t)f->B * f->C * XY;
     if (zb->Z > 0 && !zb->z) return FLASHBEV_ERR_NULLPTR;
-    if (gelems > 0) {
+    if (need_data && gelems > 0) {
         if (!gfeat) return FLASHBEV_ERR_NULLPTR;
         if ((uintptr_t)gfeat % 4) return FLASHBEV_ERR_ALIGN;
     }
     const bool scatter = gelems > 0 && out_elems > 0 && zb->Z > 0;
-    if (scatter) {
+    if (need_data && scatter) {
         if (!gout || !l2i) return FLASHBEV_ERR_NULLPTR;
         if (((uintptr_t)gout % 4) || ((uintptr_t)l2i % 4)) return FLASHBEV_ERR_ALIGN;
         const size_t gb = gelems * 4;
@@ -1125,43 +1264,69 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     int tile_cells = waves * rounds * cpw;
 
     // tiled mode: 4 wavefronts of one group each on a 2-D tile with four
-    // cells per tile row, and the rest of the LDS budget as per-pixel rows
+    // cells per tile row; LDS holds the per-wave records, the row table, the
+    // pass's sorted term list (sized for the pass's largest possible number
+    // of terms) and as many per-pixel rows as the budget leaves
     const uint64_t npix = (uint64_t)f->N * f->H * f->W;
     bool tiled = false;
-    int t_waves = 0, t_tx = 0, t_ty = 0, t_cap = 0;
+    int t_waves = 0, t_tx = 0, t_ty = 0, t_cap = 0, t_zc = 0;
     uint32_t t_mask = 0, l_slot = 0, l_tbl = 0, l_spix = 0, l_acc = 0, l_cnt = 0, l_total = 0;
+    uint32_t l_rcnt = 0, l_rbase = 0, l_rfill = 0, l_list = 0;
     int t_pitch = 0;
-    if (npix + 1 < (1u << kKeyBits) && cpw >= 2) {
+    if (npix + 1 < (1u << kKeyBits) && cpw >= 2 && f->N > 0) {
         t_waves = kWavesMax;
         const int T = t_waves * cpw;
         t_ty = (T % 4 == 0) ? 4 : T;
         t_tx = T / t_ty;
         t_pitch = T | 1;
-        const LdsLayout base = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
-        uint32_t o = base.total;
-        l_slot = o; o = align16(o + (uint32_t)t_waves * cpw * kRecStride * 8u);
-        l_cnt = o; o = align16(o + 4u);
-        // per row: C floats, one pixel id and two table entries
-        const uint32_t per_row = (uint32_t)f->C * 4u + 4u + 8u;
-        int cap = o < kLdsBudget ? (int)((kLdsBudget - o) / per_row) : 0;
-        if (cap > kSlotMax - 1) cap = kSlotMax - 1;
-        uint32_t entries = 1;
-        while (entries < 2u * (uint32_t)cap) entries <<= 1;
-        // the table is a power of two: shrink the rows until everything fits
-        while (cap >= 16 && o + align16(entries * 4u) + align16((uint32_t)cap * 4u) +
-                                    align16((uint32_t)cap * f->C * 4u) > kLdsBudget) {
-            --cap;
-            entries = 1;
+        int zc_max = kWave / f->N;
+        if (zc_max > zb->Z && zb->Z > 0) zc_max = zb->Z;
+        if (zc_max < 1) zc_max = 1;
+        for (int zc_try = zc_max; zc_try >= 1 && !tiled; zc_try = zc_try > 1 ? zc_try / 2 : 0) {
+            const LdsLayout base = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
+            uint32_t o = base.total;
+            const uint32_t lslot = o; o = align16(o + (uint32_t)t_waves * cpw * kRecStride * 8u);
+            const uint32_t lcnt = o; o = align16(o + 16u);
+            const uint32_t entries_max = 4u * (uint32_t)t_waves * cpw * (uint32_t)(zc_try * f->N);
+            const uint32_t llist = o; o = align16(o + entries_max * 4u);
+            // per row: C floats, a pixel id, two table entries and the
+            // count, base and fill words
+            const uint32_t per_row = (uint32_t)f->C * 4u + 4u + 8u + 12u;
+            int cap = o < kLdsBudgetBwd ? (int)((kLdsBudgetBwd - o) / per_row) : 0;
+            if (cap > kSlotMax - 1) cap = kSlotMax - 1;
+            auto total_for = [&](int c, uint32_t ent) {
+                uint32_t t = o;
+                t = align16(t + ent * 4u);
+                t = align16(t + (uint32_t)c * 4u);          // spix
+                t = align16(t + (uint32_t)c * 4u);          // rcnt
+                t = align16(t + ((uint32_t)c + 1u) * 4u);   // rbase
+                t = align16(t + (uint32_t)c * 4u);          // rfill
+                t = align16(t + (uint32_t)c * f->C * 4u);   // rows
+                return t;
+            };
+            uint32_t entries = 1;
             while (entries < 2u * (uint32_t)cap) entries <<= 1;
-        }
-        if (cap >= 16) {
-            l_tbl = o; o = align16(o + entries * 4u);
-            l_spix = o; o = align16(o + (uint32_t)cap * 4u);
-            l_acc = o; o = align16(o + (uint32_t)cap * f->C * 4u);
-            l_total = o;
-            t_cap = cap;
-            t_mask = entries - 1u;
-            tiled = true;
+            while (cap >= 16 && total_for(cap, entries) > kLdsBudgetBwd) {
+                --cap;
+                entries = 1;
+                while (entries < 2u * (uint32_t)cap) entries <<= 1;
+            }
+            if (cap >= 16) {
+                l_slot = lslot;
+                l_cnt = lcnt;
+                l_list = llist;
+                l_tbl = o; o = align16(o + entries * 4u);
+                l_spix = o; o = align16(o + (uint32_t)cap * 4u);
+                l_rcnt = o; o = align16(o + (uint32_t)cap * 4u);
+                l_rbase = o; o = align16(o + ((uint32_t)cap + 1u) * 4u);
+                l_rfill = o; o = align16(o + (uint32_t)cap * 4u);
+                l_acc = o; o = align16(o + (uint32_t)cap * f->C * 4u);
+                l_total = o;
+                t_cap = cap;
+                t_mask = entries - 1u;
+                t_zc = zc_try;
+                tiled = true;
+            }
         }
     }
     if (tiled) tile_cells = t_waves * cpw;
@@ -1191,6 +1356,10 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
         p.lds_spix = l_spix;
         p.lds_acc = l_acc;
         p.lds_cnt = l_cnt;
+        p.lds_rcnt = l_rcnt;
+        p.lds_rbase = l_rbase;
+        p.lds_rfill = l_rfill;
+        p.lds_list = l_list;
     }
     p.img_w = (float)f->img_w;
     p.img_h = (float)f->img_h;
@@ -1207,7 +1376,7 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     p.rcp_lpc = 1.0f / (float)lpc;
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
-    p.zc = zc < 1 ? 1 : zc;
+    p.zc = tiled ? t_zc : (zc < 1 ? 1 : zc);
     p.gtile_ld = tiled ? t_pitch : pitch(rounds);
     if (tiled) lay = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
     p.lds_z = lay.z;
@@ -1283,6 +1452,23 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
 
 }  // extern "C"
 
+extern "C" int flashbev_backward_launch_info(const flashbev_features *features,
+                                            const flashbev_bev_grid_spec *spec,
+                                            const flashbev_z_bins *z_bins, int64_t *workgroups,
+                                            int32_t *threads_per_workgroup, int32_t *lds_bytes,
+                                            int32_t *rows_per_tile, int32_t *lanes_per_cell)
+{
+    BwdPlan pl;
+    const int rc = make_bwd_plan(features, nullptr, spec, z_bins, nullptr, nullptr, false, &pl);
+    if (rc) return rc;
+    if (workgroups) *workgroups = pl.workgroups;
+    if (threads_per_workgroup) *threads_per_workgroup = pl.threads;
+    if (lds_bytes) *lds_bytes = (int32_t)pl.lds;
+    if (rows_per_tile) *rows_per_tile = pl.tiled ? pl.prm.cap : 0;
+    if (lanes_per_cell) *lanes_per_cell = pl.prm.lpc;
+    return FLASHBEV_OK;
+}
+
 extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
                                            const float *lidar2img,
                                            const flashbev_bev_grid_spec *spec,
@@ -1290,7 +1476,8 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
                                            float *grad_features, void *stream)
 {
     BwdPlan pl;
-    const int rc = make_bwd_plan(features, lidar2img, spec, z_bins, grad_out, grad_features, &pl);
+    const int rc = make_bwd_plan(features, lidar2img, spec, z_bins, grad_out, grad_features, true,
+                                 &pl);
     if (rc) return rc;
     if (pl.gfeat_elems == 0) return FLASHBEV_OK;
     const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
@@ -1302,7 +1489,11 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
     if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
     if (pl.workgroups == 0) return FLASHBEV_OK;
     void *args[] = {&pl.prm};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled)),
+    const void *fn = reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled));
+    if (pl.lds > 65536 &&
+        hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds) != hipSuccess)
+        return FLASHBEV_ERR_HIP;
+    const hipError_t e = hipLaunchKernel(fn,
                                          dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
                                          pl.lds, st);
     return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
