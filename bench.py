@@ -116,8 +116,9 @@ def time_gpu(fn, steps: int, warmup: int, stream):
 
 def ceilings(row_bytes: int, device) -> dict:
     """Measured memory ceilings of this GPU: the gather access shape on an
-    L2-resident (2 MiB) and an L1-resident (16 KiB) buffer, and a 1 GiB
-    coalesced HBM read stream (GB/s, best of 5)."""
+    L2-resident (2 MiB) and an L1-resident (16 KiB) buffer, a 1 GiB
+    coalesced HBM read stream (GB/s, best of 5), and float atomic adds to
+    pseudo-random rows (Gops/s)."""
     import torch
 
     from paper_2607_10071_amd import membench
@@ -155,6 +156,21 @@ def ceilings(row_bytes: int, device) -> dict:
         best = min(best, a.elapsed_time(b) * 1e-3)
     out["hbm_read"] = nbytes / best / 1e9
     del buf, sink
+    # float atomic adds (Gops/s) on a 16 MiB buffer: the backward's global adds
+    abuf = torch.zeros(4 << 20, dtype=torch.float32, device=device)
+    wgs, iters = 256 * 16, 32
+    membench.atomic_add(abuf, iters, wgs, stream.cuda_stream)
+    best = float("inf")
+    for _ in range(3):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        membench.atomic_add(abuf, iters, wgs, stream.cuda_stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b) * 1e-3)
+    out["float_atomic_Gops"] = membench.atomic_ops(wgs, iters) / best / 1e9
+    del abuf
     torch.cuda.empty_cache()
     return {k: round(v, 1) for k, v in out.items()}
 
@@ -220,10 +236,11 @@ def measure_backward(wl, inst, device, steps, warmup, taps=None) -> dict:
            "hbm_bytes_per_call": backward_bytes(wl),
            "hbm_frac": round(backward_bytes(wl) / sec / 1e9 / HBM_PEAK_GBS, 5)}
     if taps is not None:
-        # every in-range tap adds C float32 terms atomically
-        ab = taps * wl.C * 4
-        rec["atomic_bytes_per_call"] = ab
-        rec["atomic_GBs"] = round(ab / sec / 1e9, 1)
+        # every in-range tap contributes C float32 terms; a plain scatter adds
+        # each with a float atomic, so terms/s over the measured atomic ceiling
+        # says how far the tiled reduction goes beyond that design
+        rec["terms_per_call"] = taps * wl.C
+        rec["terms_G_per_s"] = round(taps * wl.C / sec / 1e9, 1)
     del fn, keep
     return rec
 
@@ -403,6 +420,10 @@ def main(argv=None) -> int:
                                             max(20, args.steps // 2), args.warmup)
         bwd["paper_context"] = {"flashbev_a6000_backward_ms": 3.27,
                                 "tensorized_a6000_backward_ms": 17.90}
+        ceil = rec.get("ceilings_GBs", {}).get("float_atomic_Gops")
+        if ceil and "terms_G_per_s" in bwd[wl.name]:
+            bwd[wl.name]["float_atomic_ceiling_Gops"] = ceil
+            bwd[wl.name]["terms_over_atomic_ceiling"] = round(bwd[wl.name]["terms_G_per_s"] / ceil, 3)
         rec["backward"] = bwd
 
     print(json.dumps(rec), flush=True)

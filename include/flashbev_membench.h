@@ -12,7 +12,8 @@
  *     of the bilinear gather-reduce (FlashBEV paper, Sec. 3.3, Alg. 2);
  *     with a buffer of a few MiB it stays in L2, with a few KiB in L1;
  *   - the HBM read ceiling: a coalesced stream of 16-byte loads over a
- *     buffer much larger than every cache.
+ *     buffer much larger than every cache;
+ *   - the float atomic-add ceiling that bounds the backward's global adds.
  *
  * Both write one float per thread to `sink` (so no load is optimized away)
  * and return 0, or a negative value on bad arguments (checked before any
@@ -48,6 +49,16 @@ int flashbev_membench_gather(const void *buf, uint64_t buf_bytes, int32_t row_by
  * with 16-byte loads spread over `workgroups` workgroups of 256 threads.
  */
 int flashbev_membench_stream(const void *buf, uint64_t bytes, int32_t workgroups, float *sink,
+                             void *stream);
+
+/*
+ * Float atomic-add ceiling: every lane adds 1.0 with a float atomic add
+ * (no return value) to `iters` pseudo-random 256-byte rows of buf (buf_floats
+ * floats, at least 64, 4-byte aligned; the values change).  Operations:
+ * workgroups * 256 * iters.  The backward's per-tile flush and its overflow
+ * taps are bound by this rate.
+ */
+int flashbev_membench_atomic(float *buf, uint64_t buf_floats, int32_t iters, int32_t workgroups,
                              void *stream);
 
 #ifdef __cplusplus

@@ -84,6 +84,17 @@ stream_kernel(const uint4 *buf, uint64_t n16, float *sink)
     sink[blockIdx.x * kThreads + threadIdx.x] = __builtin_bit_cast(float, (a ^ b ^ c ^ d) & 0x007fffffu);
 }
 
+__global__ void __launch_bounds__(kThreads)
+atomic_kernel(float *buf, uint32_t nrows, int32_t iters)
+{
+    const int lane = threadIdx.x % 64;
+    const uint32_t wave = (blockIdx.x * kThreads + threadIdx.x) / 64;
+    for (int it = 0; it < iters; ++it) {
+        const uint32_t row = mix(wave * 0x9e3779b9u + (uint32_t)it * 0x85ebca6bu) % nrows;
+        unsafeAtomicAdd(buf + (size_t)row * 64u + lane, 1.0f);
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -120,3 +131,14 @@ int flashbev_membench_stream(const void *buf, uint64_t bytes, int32_t workgroups
 }
 
 }  // extern "C"
+
+extern "C" int flashbev_membench_atomic(float *buf, uint64_t buf_floats, int32_t iters,
+                                        int32_t workgroups, void *stream)
+{
+    if (!buf) return -1;
+    if (buf_floats < 64 || iters < 1 || workgroups < 1 || ((uintptr_t)buf % 4)) return -2;
+    if (buf_floats / 64 > 0xFFFFFFFFull) return -3;
+    hipLaunchKernelGGL(atomic_kernel, dim3(workgroups), dim3(kThreads), 0, (hipStream_t)stream, buf,
+                       (uint32_t)(buf_floats / 64), iters);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}

@@ -1,7 +1,8 @@
 """Binding of the memory-ceiling micro-benchmarks (include/flashbev_membench.h).
 
 Measurement tools for bench.py: the gather ceiling (the access shape of the
-fused gather on an L2- or L1-resident buffer) and the HBM read ceiling.
+fused gather on an L2- or L1-resident buffer), the HBM read ceiling and the
+float atomic-add ceiling.
 """
 from __future__ import annotations
 
@@ -26,6 +27,9 @@ def _lib():
         L.flashbev_membench_stream.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
                                                ctypes.c_void_p, ctypes.c_void_p]
         L.flashbev_membench_stream.restype = ctypes.c_int
+        L.flashbev_membench_atomic.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_void_p]
+        L.flashbev_membench_atomic.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -52,3 +56,14 @@ def stream_read(buf, workgroups: int, sink, stream: int) -> None:
                                          ctypes.c_void_p(stream))
     if rc:
         raise RuntimeError(f"flashbev_membench_stream failed: {rc}")
+
+
+def atomic_ops(workgroups: int, iters: int) -> int:
+    return workgroups * 256 * iters
+
+
+def atomic_add(buf, iters: int, workgroups: int, stream: int) -> None:
+    rc = _lib().flashbev_membench_atomic(ctypes.c_void_p(buf.data_ptr()), buf.numel(), iters,
+                                         workgroups, ctypes.c_void_p(stream))
+    if rc:
+        raise RuntimeError(f"flashbev_membench_atomic failed: {rc}")
