@@ -22,6 +22,7 @@ paper's reference setting; --backward-only times just the backward.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -95,21 +96,29 @@ def settle(fn, seconds: float = 0.3) -> None:
 
 def time_gpu(fn, steps: int, warmup: int, stream):
     """W untimed calls, then exactly K back-to-back calls between two HIP
-    events recorded on the launch stream (synchronized on both sides)."""
+    events recorded on the launch stream (synchronized on both sides).
+    Python's garbage collector is held off meanwhile: a collection pause of
+    tens of milliseconds would drain the launch queue and be timed as GPU
+    time."""
     import torch
 
-    for _ in range(warmup):
-        fn()
-    torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
-    t0.record(stream)
-    for _ in range(steps):
-        fn()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    gc.collect()
+    gc.disable()
+    try:
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        wall0 = time.perf_counter()
+        t0.record(stream)
+        for _ in range(steps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+    finally:
+        gc.enable()
     total_ms = t0.elapsed_time(t1)
     return {"total_ms": total_ms, "ms_per_step": total_ms / steps, "wall_s": wall}
 
@@ -187,11 +196,8 @@ def make_call(wl, inst, device):
     grid = fb.grid_of(wl)
     img = (wl.img_h, wl.img_w)
     stream = torch.cuda.current_stream(device)
-    z = inst.z
-
-    def fn():
-        fb.sample_vt(feats, l2i, z, grid, img, out=out, stream=stream)
-
+    # arguments marshalled once: each step is one C call, no Python allocation
+    fn = fb.prepare_sample_vt(feats, l2i, inst.z, grid, img, out, stream=stream)
     return fn, feats, l2i, out, stream
 
 
@@ -210,12 +216,8 @@ def make_backward_call(wl, inst, device):
     grid = fb.grid_of(wl)
     img = (wl.img_h, wl.img_w)
     stream = torch.cuda.current_stream(device)
-    shape = inst.features.shape
-
-    def fn():
-        fb.sample_vt_backward(gout, l2i, inst.z, grid, img, shape, wl.dtype, grad_features=gfeat,
-                              stream=stream)
-
+    fn = fb.prepare_sample_vt_backward(gout, l2i, inst.z, grid, img, inst.features.shape,
+                                       wl.dtype, gfeat, stream=stream)
     return fn, (gout, l2i, gfeat), stream
 
 

@@ -14,7 +14,8 @@ import os
 from typing import Optional, Sequence, Tuple
 
 __all__ = [
-    "BevGrid", "sample_vt", "sample_vt_backward", "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
+    "BevGrid", "sample_vt", "sample_vt_backward", "prepare_sample_vt", "prepare_sample_vt_backward",
+    "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
 ]
 
@@ -312,3 +313,68 @@ def backward_launch_info(shape, dtype: str, z_bins, grid: BevGrid, img_hw,
         raise FlashBevError(rc, "flashbev_backward_launch_info")
     return {"workgroups": wg.value, "threads": thr.value, "lds_bytes": lds.value,
             "rows_per_tile": rows.value, "lanes_per_cell": lpc.value}
+
+
+class _Prepared:
+    """A C entry point with its arguments marshalled once: calling it makes
+    the call again with no Python-side allocation.  It keeps the tensors and
+    structures it refers to alive."""
+
+    def __init__(self, fn, args, keep, what):
+        self._fn = fn
+        self._args = args
+        self._keep = keep
+        self._what = what
+
+    def __call__(self) -> None:
+        rc = self._fn(*self._args)
+        if rc != 0:
+            raise FlashBevError(rc, self._what)
+
+
+def prepare_sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw, out,
+                      reduce: str = "mean", stream=None) -> _Prepared:
+    """``sample_vt`` with every argument fixed: returns a callable that
+    enqueues the same forward call again (same tensors, same stream)."""
+    import torch
+
+    B, N, H, W, C = features.shape
+    if not (features.is_cuda and lidar2img.is_cuda and out.is_cuda):
+        raise ValueError("features, lidar2img and out must be device tensors")
+    if out.dtype != torch.float32 or not out.is_contiguous() or \
+            tuple(out.shape) != (B, C, grid.X, grid.Y):
+        raise ValueError(f"out must be a contiguous float32 tensor [{B}, {C}, {grid.X}, {grid.Y}]")
+    z = _z_array(z_bins)
+    f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
+                        grid, z, reduce)
+    s = _stream_handle(stream, features.device)
+    args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
+    return _Prepared(_lib().flashbev_sample_vt, args,
+                     (features, lidar2img, out, z, f, g, zb), "flashbev_sample_vt")
+
+
+def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw,
+                               features_shape, features_dtype, grad_features,
+                               reduce: str = "mean", stream=None) -> _Prepared:
+    """``sample_vt_backward`` with every argument fixed (see prepare_sample_vt)."""
+    import torch
+
+    B, N, H, W, C = (int(v) for v in features_shape)
+    if not (grad_out.is_cuda and lidar2img.is_cuda and grad_features.is_cuda):
+        raise ValueError("grad_out, lidar2img and grad_features must be device tensors")
+    if grad_features.dtype != torch.float32 or not grad_features.is_contiguous() or \
+            tuple(grad_features.shape) != (B, N, H, W, C):
+        raise ValueError(f"grad_features must be a contiguous float32 tensor [{B}, {N}, {H}, {W}, {C}]")
+    if not isinstance(features_dtype, str):
+        features_dtype = {torch.float32: "f32", torch.float16: "f16",
+                          torch.bfloat16: "bf16"}[features_dtype]
+    z = _z_array(z_bins)
+    f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
+    s = _stream_handle(stream, grad_out.device)
+    args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
+            ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(s))
+    return _Prepared(_lib().flashbev_sample_vt_backward, args,
+                     (grad_out, lidar2img, grad_features, z, f, g, zb),
+                     "flashbev_sample_vt_backward")

@@ -575,15 +575,17 @@ __device__ __forceinline__ float4 bwd_setup(const BwdParams &p, float u, float v
 // Table entry of pixel q of the tile (q < 2^20 - 1): find it in the open-
 // addressing table or insert it.  Entries pack (q + 1) | row << 20, with row
 // kRowUnset until the pass's row assignment gives the pixel an LDS row; 0
-// is empty.  Returns the entry's index, or kSlotNone when the table is full
-// (the caller then adds the tap to global memory).
+// is empty.  The probe sequence is cut after kProbeMax entries, so a crowded
+// table costs little: the call then returns kSlotNone and the caller reads
+// or adds that tap in global memory instead.
 constexpr uint32_t kRowUnset = (1u << (32 - kKeyBits)) - 1u;
+constexpr uint32_t kProbeMax = 32;
 
 __device__ __forceinline__ uint32_t tile_insert(uint32_t q, uint32_t *tbl, uint32_t mask)
 {
     const uint32_t key = q + 1u;
     uint32_t h = (key * 0x9E3779B1u) >> 8;
-    for (uint32_t probe = 0; probe <= mask; ++probe) {
+    for (uint32_t probe = 0; probe < kProbeMax; ++probe) {
         h &= mask;
         uint32_t e = tbl[h];
         if (e == 0u) {
@@ -948,7 +950,6 @@ sample_vt_bwd(const BwdParams p)
                             const int c = c0 + lane;
                             const float *gc = s_g + (c < C ? c : C - 1) * p.gtile_ld;
                             float sum = 0.0f;
-#pragma unroll 4
                             for (uint32_t k = 0; k < kn; ++k) {
                                 const float w = __builtin_bit_cast(
                                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));

@@ -186,3 +186,13 @@ def test_binding_rejects_host_tensors():
     m = torch.zeros(1, 1, 4, 4)
     with pytest.raises(ValueError):
         fb.sample_vt(f, m, [0.0], fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8))
+    with pytest.raises(ValueError):
+        fb.prepare_sample_vt(f, m, [0.0], fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8),
+                             torch.zeros(1, 4, 2, 2))
+    with pytest.raises(ValueError):
+        fb.sample_vt_backward(torch.zeros(1, 4, 2, 2), m, [0.0], fb.BevGrid(-1, 1, 2, -1, 1, 2),
+                              (8, 8), (1, 1, 2, 2, 4))
+    with pytest.raises(ValueError):
+        fb.prepare_sample_vt_backward(torch.zeros(1, 4, 2, 2), m, [0.0],
+                                      fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8), (1, 1, 2, 2, 4),
+                                      "f32", f)

@@ -196,3 +196,20 @@ def test_backward_allocates_nothing_beyond_its_output(fb, device):
                           inst.features.shape, grad_features=gf)
     torch.cuda.synchronize()
     assert torch.cuda.max_memory_allocated(device) == base
+
+
+def test_prepared_backward_matches_plain_call(fb, device):
+    import torch
+    inst = synth.make_workload(synth.config("tiny"))
+    wl = inst.wl
+    g = _grad_out(wl)
+    l2i = torch.from_numpy(np.ascontiguousarray(inst.lidar2img)).to(device)
+    gt = torch.from_numpy(g).to(device)
+    gf = torch.full(inst.features.shape, float("nan"), dtype=torch.float32, device=device)
+    call = fb.prepare_sample_vt_backward(gt, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w),
+                                         inst.features.shape, wl.dtype, gf)
+    call()
+    call()
+    torch.cuda.synchronize()
+    ref, scale, terms = oracle.backward_instance(inst, g)
+    assert_bwd_parity(gf.cpu().numpy(), ref, scale, terms, "prepared")

@@ -231,3 +231,19 @@ def test_peak_operator_memory_is_the_output(fb, device, Z):
     peak = torch.cuda.max_memory_allocated() - base
     out_bytes = out.numel() * 4
     assert out_bytes <= peak <= out_bytes + 2 * 1024 * 1024, (peak, out_bytes)
+
+
+def test_prepared_call_matches_plain_call(fb, device):
+    """The binding's prepared call (arguments marshalled once) enqueues the
+    same C call as sample_vt."""
+    import torch
+    wl = synth.config("tiny")
+    inst = synth.make_workload(wl)
+    ft, l2i = to_dev(inst, device)
+    ref = fb.sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w))
+    out = torch.full_like(ref, float("nan"))
+    call = fb.prepare_sample_vt(ft, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w), out)
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
