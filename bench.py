@@ -17,7 +17,8 @@ with HIP events on the launch stream), peak operator memory and the CPU
 oracle timed on the host as a reported baseline.  Unless --no-extra is
 given it also reports two more workloads, the measured memory ceilings and
 the backward (gradient w.r.t. the features) on this workload and on the
-paper's reference setting; --backward-only times just the backward.
+paper's reference setting; --backward-only times just the backward, and
+--sweep the scaling along height bins, grid size and channels.
 """
 from __future__ import annotations
 
@@ -265,6 +266,67 @@ def peak_operator_memory(wl, inst, device) -> int:
     return int(peak)
 
 
+PAPER_TENSORIZED_MS = 9.18      # Table 4: tensorized forward at the reference setting
+PAPER_TENSORIZED_MB = 1971.94   # Table 4: its peak memory
+
+
+def sweep(device, steps: int, warmup: int) -> dict:
+    """Scaling along the paper's axes (Sec. 4, Figs. 4-6, Table 5) at its
+    reference setting (paper_ref): height bins, BEV grid size and channels.
+    Each point: latency, Gsamples/s, peak operator memory and the analytic
+    tensorized footprint.  The grid sweep keeps the +-50 m extent and refines
+    the cell size."""
+    import torch
+
+    import synth
+
+    base = synth.config("paper_ref")
+
+    def point(wl):
+        inst = synth.make_workload(wl)
+        fn, feats, l2i, out, stream = make_call(wl, inst, device)
+        settle(fn, 0.05)
+        t = time_gpu(fn, steps, warmup, stream)
+        del fn, out
+        peak = peak_operator_memory(wl, inst, device)
+        del feats, l2i
+        torch.cuda.empty_cache()
+        return {"ms": round(t["ms_per_step"], 5),
+                "gsamples_per_s": round(wl.samples / (t["ms_per_step"] * 1e-3) / 1e9, 3),
+                "peak_op_memory_bytes": peak, "output_bytes": wl.B * wl.C * wl.X * wl.Y * 4,
+                "tensorized_features3d_bytes": tensorized_footprint(wl)["features3d_bytes"]}
+
+    out = {"workload": "paper_ref: B=1 N=6 images 448x800, maps 56x100, C=128 f32, "
+                       "BEV 200x200 over +-50 m, Z=8 over [-5, 5] m",
+           "height_bins": {}, "grid": {}, "channels": {}}
+    for Z in (4, 8, 16, 32, 64, 128, 256):
+        out["height_bins"][Z] = point(base.with_(Z=Z))
+    for n in (100, 200, 400, 800, 1600, 3200):
+        out["grid"][n] = point(base.with_(X=n, Y=n, dx=100.0 / n, dy=100.0 / n))
+    for C in (32, 64, 128, 256, 512, 1024):
+        out["channels"][C] = point(base.with_(C=C))
+    # deployment capacity under the tensorized baseline's reference budgets
+    # (Table 5): latency 9.18 ms, memory 1971.94 MB
+    zs = [z for z, r in out["height_bins"].items() if r["ms"] <= PAPER_TENSORIZED_MS]
+    gs = [n for n, r in out["grid"].items() if r["ms"] <= PAPER_TENSORIZED_MS]
+    g_top = max(gs) if gs else None
+    t_top = out["grid"][g_top]["ms"] if g_top else None
+    out["capacity"] = {
+        "latency_budget_ms": PAPER_TENSORIZED_MS,
+        "max_Z_measured": max(zs) if zs else None,
+        "max_Z_note": "every measured Z up to the ABI limit of 256 fits the budget"
+                      if len(zs) == len(out["height_bins"]) else "",
+        "max_grid_measured": g_top,
+        # time grows with X*Y: the largest X=Y the budget allows, from the
+        # largest measured grid within it
+        "max_grid_extrapolated": int(g_top * (PAPER_TENSORIZED_MS / t_top) ** 0.5) if g_top else None,
+        "memory_budget_MB": PAPER_TENSORIZED_MB,
+        # peak operator memory is the output B*C*X*Y*4 bytes (checked above)
+        "max_grid_within_memory": int((PAPER_TENSORIZED_MB * 1e6 / (base.B * base.C * 4)) ** 0.5),
+    }
+    return out
+
+
 def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
     """The CPU oracle (float64, OpenMP) on the same workload, repeated until
     about `min_seconds` of work has been timed."""
@@ -296,6 +358,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the secondary workloads reported for context")
+    ap.add_argument("--sweep", action="store_true",
+                    help="scaling sweeps along height bins, grid size and channels at the "
+                         "paper's reference setting (one JSON line)")
     ap.add_argument("--backward-only", action="store_true",
                     help="time only the backward (gradient w.r.t. the features) on the workload")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -325,6 +390,9 @@ def main(argv=None) -> int:
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.sweep:
+        print(json.dumps({"sweep": sweep(device, max(5, min(args.steps, 20)), 3)}), flush=True)
+        return 0
     wl = synth.config(args.workload)
     inst = synth.make_workload(wl)
     if args.backward_only:
