@@ -1099,6 +1099,12 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     const int nvec = (int)(row / lw);
     int vpl = 1;
     while (vpl < 4 && (nvec + vpl - 1) / vpl > kWave) vpl <<= 1;
+    // wide rows: give a lane several vectors so that a wavefront covers at
+    // least two cells (four from 1 KiB rows on), which shares the set-up
+    // pass among more cells (measured on MI355X: C=256 float32 124 -> 81 us,
+    // C=512 278 -> 200 us at the paper's reference setting)
+    const int min_cpw = row >= 1024 ? 4 : 2;
+    while (vpl < 4 && kWave / ((nvec + vpl - 1) / vpl) < min_cpw && nvec >= 2 * vpl) vpl <<= 1;
     const int lpc = (nvec + vpl - 1) / vpl;
     if (lpc > kWave) return FLASHBEV_ERR_UNSUPPORTED;
     int cpw = kWave / lpc;

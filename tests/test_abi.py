@@ -161,7 +161,7 @@ def test_empty_outputs_enqueue_nothing():
 def test_launch_info_geometry():
     for dtype, C, cpw, lpc in (("f32", 80, 3, 20), ("bf16", 128, 4, 16), ("f16", 64, 8, 8),
                                ("bf16", 64, 8, 8), ("f32", 32, 8, 8), ("f32", 4, 8, 1),
-                               ("f32", 136, 1, 34), ("f32", 1024, 1, 64), ("bf16", 5, 8, 5)):
+                               ("f32", 136, 3, 17), ("f32", 1024, 1, 64), ("bf16", 5, 8, 5)):
         info = fb.launch_info((1, 6, 32, 88, C), dtype, np.zeros(8), fb.BevGrid(-50, .5, 200, -50, .5, 200),
                               (256, 704))
         assert info["cells_per_wave"] == cpw and info["lanes_per_cell"] == lpc, (dtype, C, info)
