@@ -95,17 +95,19 @@ def settle(fn, seconds: float = 0.3) -> None:
         torch.cuda.synchronize()
 
 
-def time_gpu(fn, steps: int, warmup: int, stream):
-    """W untimed calls, then exactly K back-to-back calls between two HIP
-    events recorded on the launch stream (synchronized on both sides).
-    Python's garbage collector is held off meanwhile: a collection pause of
-    tens of milliseconds would drain the launch queue and be timed as GPU
-    time."""
+def time_gpu(fn, steps: int, warmup: int, stream, settle_s: float = 0.3):
+    """A settle period and W untimed calls, then exactly K back-to-back calls
+    between two HIP events recorded on the launch stream (synchronized on
+    both sides).  Python's garbage collector runs once before the settle
+    period and is held off from then on: a collection pause of tens of
+    milliseconds would drain the launch queue and be timed as GPU time, and
+    an idle GPU lowers its clocks, which the settle period brings back up."""
     import torch
 
     gc.collect()
     gc.disable()
     try:
+        settle(fn, settle_s)
         for _ in range(warmup):
             fn()
         torch.cuda.synchronize()
@@ -231,8 +233,7 @@ def backward_bytes(wl) -> int:
 
 def measure_backward(wl, inst, device, steps, warmup, taps=None) -> dict:
     fn, keep, stream = make_backward_call(wl, inst, device)
-    settle(fn, 0.1)
-    t = time_gpu(fn, steps, warmup, stream)
+    t = time_gpu(fn, steps, warmup, stream, 0.1)
     sec = t["ms_per_step"] * 1e-3
     rec = {"ms": round(t["ms_per_step"], 5),
            "gsamples_per_s": round(wl.samples / sec / 1e9, 3),
@@ -285,8 +286,7 @@ def sweep(device, steps: int, warmup: int) -> dict:
     def point(wl):
         inst = synth.make_workload(wl)
         fn, feats, l2i, out, stream = make_call(wl, inst, device)
-        settle(fn, 0.05)
-        t = time_gpu(fn, steps, warmup, stream)
+        t = time_gpu(fn, steps, warmup, stream, 0.05)
         del fn, out
         peak = peak_operator_memory(wl, inst, device)
         del feats, l2i
@@ -401,7 +401,6 @@ def main(argv=None) -> int:
         print(json.dumps(rec), flush=True)
         return 0
     fn, feats, l2i, out, stream = make_call(wl, inst, device)
-    settle(fn)
     t = time_gpu(fn, args.steps, args.warmup, stream)
     launch_s = t["ms_per_step"] * 1e-3  # average launch duration over the timed region
     samples = wl.samples
@@ -449,8 +448,7 @@ def main(argv=None) -> int:
             w2 = synth.config(name)
             i2 = synth.make_workload(w2)
             f2, a, b_, c_, s2 = make_call(w2, i2, device)
-            settle(f2, 0.1)
-            t2 = time_gpu(f2, max(20, args.steps // 2), args.warmup, s2)
+            t2 = time_gpu(f2, max(20, args.steps // 2), args.warmup, s2, 0.1)
             extra[name] = {"ms": round(t2["ms_per_step"], 5),
                            "gsamples_per_s": round(w2.samples / (t2["ms_per_step"] * 1e-3) / 1e9, 3),
                            "hbm_frac": round(algorithmic_bytes(w2) / (t2["ms_per_step"] * 1e-3) / 1e9
