@@ -1115,8 +1115,13 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     // 2-wavefront workgroups give twice the tiles and a shorter tail.
     const int waves = cpw >= kCpwMax ? kWavesMax : 2;
     // tile: at least kCellsPerWave cells per wavefront, fewer if the output
-    // tile would not fit the LDS budget (very wide rows)
+    // tile would not fit the LDS budget (very wide rows).  Where a wavefront
+    // holds at most two cells or a lane several vectors, one round per tile
+    // is faster (measured on MI355X: the paper's reference setting, C=128
+    // float32, 41.8 -> 35.2 us; C=256 78 -> 63 us): the heavier cells then
+    // spread over more, smaller workgroups.
     int rounds = (kCellsPerWave + cpw - 1) / cpw;
+    if (cpw <= 2 || vpl >= 2) rounds = 1;
     auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
     LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
     while (lay.total > kLdsBudget && rounds > 1) {

@@ -168,12 +168,17 @@ def test_launch_info_geometry():
         # 4 wavefronts per workgroup with full 8-cell groups, else 2
         waves = 4 if cpw == 8 else 2
         assert info["threads"] == 64 * waves
-        # a tile is `waves` wavefronts x `rounds` groups of cpw cells, at
-        # least 6 cells per wavefront unless the LDS budget forces fewer
+        # a tile is `waves` wavefronts x `rounds` groups of cpw cells: at
+        # least 6 cells per wavefront, except one round where a wavefront
+        # holds at most two cells or a lane several 16-byte vectors
         tiles = {math.ceil(40000 / (waves * r * cpw)): r for r in range(1, 9)}
         assert info["workgroups"] in tiles
         r = tiles[info["workgroups"]]
-        assert r * cpw >= 6 or info["lds_bytes"] > 40 * 1024 or C >= 1024
+        vpl = math.ceil(C * (4 if dtype == "f32" else 2) / 16 / lpc)
+        if cpw <= 2 or vpl >= 2:
+            assert r == 1, (dtype, C, info)
+        else:
+            assert r * cpw >= 6, (dtype, C, info)
         assert info["lds_bytes"] <= 64 * 1024
     with pytest.raises(fb.FlashBevError):
         fb.launch_info((1, 6, 32, 88, 80), "f32", np.zeros(300), fb.BevGrid(-50, .5, 200, -50, .5, 200),
