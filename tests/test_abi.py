@@ -201,3 +201,34 @@ def test_binding_rejects_host_tensors():
         fb.prepare_sample_vt_backward(torch.zeros(1, 4, 2, 2), m, [0.0],
                                       fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8), (1, 1, 2, 2, 4),
                                       "f32", f)
+
+
+def test_backward_launch_info_geometry():
+    """Tiled mode where pixel ids fit 20 bits and a wavefront holds at least
+    two cells; LDS within the tiled budget; direct mode otherwise."""
+    grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
+    for dtype, C, tiled in (("f32", 80, True), ("bf16", 128, True), ("f16", 64, True),
+                            ("f32", 32, True), ("f32", 1, True), ("f32", 1024, False),
+                            ("bf16", 2048, False)):
+        info = fb.backward_launch_info((1, 6, 32, 88, C), dtype, np.zeros(8), grid, (256, 704))
+        lpc = min(64, (C + 3) // 4)
+        assert info["lanes_per_cell"] == lpc, (C, info)
+        assert (info["rows_per_tile"] > 0) == tiled, (C, info)
+        if tiled:
+            assert info["rows_per_tile"] >= 16 and info["threads"] == 256
+            assert info["lds_bytes"] <= 80 * 1024
+            cpw = min(8, 64 // lpc)
+            T = 4 * cpw
+            ty = 4 if T % 4 == 0 else T
+            assert info["workgroups"] == math.ceil(200 / (T // ty)) * math.ceil(200 / ty)
+        else:
+            assert info["lds_bytes"] <= 64 * 1024
+    # more than 2^20 - 1 pixels per batch element: direct mode
+    info = fb.backward_launch_info((1, 64, 128, 128, 16), "f32", np.zeros(4), grid, (512, 512))
+    assert info["rows_per_tile"] == 0
+    # nothing to scatter when the grid is empty; the fill still runs in the call
+    info = fb.backward_launch_info((1, 6, 32, 88, 80), "f32", np.zeros(8),
+                                   fb.BevGrid(-50, .5, 0, -50, .5, 200), (256, 704))
+    assert info["workgroups"] == 0
+    with pytest.raises(fb.FlashBevError):
+        fb.backward_launch_info((1, 6, 32, 88, 80), "f32", np.zeros(300), grid, (256, 704))
