@@ -62,6 +62,7 @@ constexpr int kStripe = 16;               // consecutive tiles per XCD stripe
 constexpr uint32_t kNoTap = 0x80000000u;
 constexpr uint64_t kFeatBytesMax = 0x7FFFFFFFull;
 constexpr uint32_t kLdsBudget = 64u * 1024u;   // dynamic LDS per workgroup
+constexpr uint64_t kOneRoundTilesMax = 262144;  // grids up to this many one-round tiles
 constexpr uint32_t kLdsBudgetBwd = 80u * 1024u;  // tiled backward: two workgroups per CU
 
 struct Params {
@@ -1117,11 +1118,14 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     // tile: at least kCellsPerWave cells per wavefront, fewer if the output
     // tile would not fit the LDS budget (very wide rows).  Where a wavefront
     // holds at most two cells or a lane several vectors, one round per tile
-    // is faster (measured on MI355X: the paper's reference setting, C=128
-    // float32, 41.8 -> 35.2 us; C=256 78 -> 63 us): the heavier cells then
-    // spread over more, smaller workgroups.
+    // is faster as long as the grid does not get too many workgroups
+    // (measured on MI355X at the paper's reference setting, C=128 float32:
+    // 200x200 41.8 -> 35.2 us, 800x800 432 -> 401 us; but 1600x1600
+    // 1.44 -> 1.99 ms, where per-workgroup set-up dominates)
     int rounds = (kCellsPerWave + cpw - 1) / cpw;
-    if (cpw <= 2 || vpl >= 2) rounds = 1;
+    if ((cpw <= 2 || vpl >= 2) &&
+        (uint64_t)f->B * (uint64_t)s->X * (uint64_t)s->Y <= (uint64_t)waves * cpw * kOneRoundTilesMax)
+        rounds = 1;
     auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
     LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
     while (lay.total > kLdsBudget && rounds > 1) {

@@ -175,11 +175,15 @@ def test_launch_info_geometry():
         assert info["workgroups"] in tiles
         r = tiles[info["workgroups"]]
         vpl = math.ceil(C * (4 if dtype == "f32" else 2) / 16 / lpc)
-        if cpw <= 2 or vpl >= 2:
+        if (cpw <= 2 or vpl >= 2) and 40000 <= waves * cpw * 262144:
             assert r == 1, (dtype, C, info)
         else:
             assert r * cpw >= 6, (dtype, C, info)
         assert info["lds_bytes"] <= 64 * 1024
+    # a very large grid keeps several rounds per tile (fewer workgroups)
+    info = fb.launch_info((1, 6, 56, 100, 128), "f32", np.zeros(8),
+                          fb.BevGrid(-50, 0.0625, 1600, -50, 0.0625, 1600), (448, 800))
+    assert info["workgroups"] == math.ceil(1600 * 1600 / (2 * 3 * info["cells_per_wave"]))
     with pytest.raises(fb.FlashBevError):
         fb.launch_info((1, 6, 32, 88, 80), "f32", np.zeros(300), fb.BevGrid(-50, .5, 200, -50, .5, 200),
                        (256, 704))
