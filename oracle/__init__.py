@@ -201,3 +201,114 @@ def backward_instance(inst, grad_out, reduce: str = "mean", nthreads: int = 0):
     return sample_vt_backward(grad_out, inst.lidar2img, inst.z, inst.features.shape,
                               (wl.img_h, wl.img_w), wl.x_min, wl.dx, wl.y_min, wl.dy,
                               wl.depth_eps, reduce, nthreads)
+
+
+# ---------------------------------------------------------------------------
+# FlashSCA (BEVFormer spatial cross-attention), flashsca_oracle.c
+# ---------------------------------------------------------------------------
+
+SCA_LMAX = 8
+
+
+class ScaProblem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("N", ctypes.c_int32), ("C", ctypes.c_int32),
+        ("heads", ctypes.c_int32), ("L", ctypes.c_int32), ("P", ctypes.c_int32),
+        ("Z", ctypes.c_int32),
+        ("level_h", ctypes.c_int32 * SCA_LMAX), ("level_w", ctypes.c_int32 * SCA_LMAX),
+        ("img_h", ctypes.c_int32), ("img_w", ctypes.c_int32),
+        ("X", ctypes.c_int32), ("Y", ctypes.c_int32),
+        ("x_min", ctypes.c_float), ("dx", ctypes.c_float),
+        ("y_min", ctypes.c_float), ("dy", ctypes.c_float),
+        ("depth_eps", ctypes.c_float), ("reduce", ctypes.c_int32),
+    ]
+
+
+class ScaCounters(ctypes.Structure):
+    _fields_ = [("hits", ctypes.c_int64), ("taps", ctypes.c_int64)]
+
+
+def _sca_lib(path: Optional[str] = None):
+    """The oracle library (or, for the mutant tests, another build of it)."""
+    L = lib() if path is None else ctypes.CDLL(path)
+    P = ctypes.POINTER
+    L.sca_oracle_forward.argtypes = [P(ScaProblem)] + [ctypes.c_void_p] * 8 + [
+        P(ScaCounters), ctypes.c_int]
+    L.sca_oracle_forward.restype = ctypes.c_int
+    L.sca_oracle_reference_points.argtypes = [P(ScaProblem)] + [ctypes.c_void_p] * 6
+    L.sca_oracle_reference_points.restype = ctypes.c_int
+    return L
+
+
+def sca_problem(B, N, C, heads, levels, P, Z, img_hw, X, Y, x_min, dx, y_min, dy,
+                depth_eps=1e-5, reduce="mean") -> ScaProblem:
+    L = len(levels)
+    assert 1 <= L <= SCA_LMAX
+    lh = (ctypes.c_int32 * SCA_LMAX)(*[int(h) for h, _ in levels], *([0] * (SCA_LMAX - L)))
+    lw = (ctypes.c_int32 * SCA_LMAX)(*[int(w) for _, w in levels], *([0] * (SCA_LMAX - L)))
+    return ScaProblem(B, N, C, heads, L, P, Z, lh, lw, int(img_hw[0]), int(img_hw[1]), X, Y,
+                      float(x_min), float(dx), float(y_min), float(dy), float(depth_eps),
+                      REDUCE[reduce])
+
+
+def sca_forward(value, lidar2img, z, offsets, logits, levels, heads, img_hw, X, Y, x_min, dx,
+                y_min, dy, depth_eps=1e-5, reduce="mean", nthreads=0, libpath=None):
+    """FlashSCA forward on the CPU.
+
+    ``value`` [B, N, S, C], ``offsets`` [B, X*Y, heads, L, P, 2], ``logits``
+    [B, X*Y, heads, L, P] (all float32).  Returns ``(out, scale, terms,
+    counters)``: ``out`` and ``scale`` float64 [B, X*Y, C], ``terms`` int32
+    [B, X*Y, heads] (in-range taps per query and head), ``counters`` a dict
+    with the (query, camera) hits and in-range taps.
+    """
+    v = np.ascontiguousarray(value, dtype=np.float32)
+    m = np.ascontiguousarray(lidar2img, dtype=np.float32)
+    zz = np.ascontiguousarray(z, dtype=np.float32)
+    off = np.ascontiguousarray(offsets, dtype=np.float32)
+    lg = np.ascontiguousarray(logits, dtype=np.float32)
+    B, N, S, C = v.shape
+    L = len(levels)
+    P = lg.shape[-1]
+    assert S == sum(h * w for h, w in levels)
+    assert m.shape == (B, N, 4, 4)
+    assert lg.shape == (B, X * Y, heads, L, P) and off.shape == lg.shape + (2,)
+    p = sca_problem(B, N, C, heads, levels, P, len(zz), img_hw, X, Y, x_min, dx, y_min, dy,
+                    depth_eps, reduce)
+    out = np.empty((B, X * Y, C), dtype=np.float64)
+    scale = np.empty_like(out)
+    terms = np.empty((B, X * Y, heads), dtype=np.int32)
+    cnt = ScaCounters()
+    rc = _sca_lib(libpath).sca_oracle_forward(
+        ctypes.byref(p), _ptr(v), _ptr(m), _ptr(zz), _ptr(off), _ptr(lg), _ptr(out),
+        _ptr(scale), _ptr(terms), ctypes.byref(cnt), int(nthreads))
+    if rc:
+        raise ValueError(f"sca_oracle_forward failed: {rc}")
+    return out, scale, terms, {"hits": int(cnt.hits), "taps": int(cnt.taps)}
+
+
+def sca_reference_points(lidar2img, z, B, N, img_hw, X, Y, x_min, dx, y_min, dy,
+                         depth_eps=1e-5, libpath=None):
+    """Anchor reference points: ``(un, vn, valid, hit)``; the first three are
+    [B, X*Y, N, Z], ``hit`` is [B, X*Y, N]."""
+    m = np.ascontiguousarray(lidar2img, dtype=np.float32)
+    zz = np.ascontiguousarray(z, dtype=np.float32)
+    Z = len(zz)
+    p = sca_problem(B, N, 1, 1, [(1, 1)], Z, Z, img_hw, X, Y, x_min, dx, y_min, dy, depth_eps)
+    shape = (B, X * Y, N, Z)
+    un = np.empty(shape, dtype=np.float32)
+    vn = np.empty(shape, dtype=np.float32)
+    valid = np.empty(shape, dtype=np.uint8)
+    hit = np.empty(shape[:3], dtype=np.uint8)
+    rc = _sca_lib(libpath).sca_oracle_reference_points(ctypes.byref(p), _ptr(m), _ptr(zz),
+                                                       _ptr(un), _ptr(vn), _ptr(valid), _ptr(hit))
+    if rc:
+        raise ValueError(f"sca_oracle_reference_points failed: {rc}")
+    return un, vn, valid.astype(bool), hit.astype(bool)
+
+
+def sca_instance(inst, reduce="mean", nthreads=0, libpath=None):
+    """FlashSCA oracle on a ``synth.ScaInstance``."""
+    wl = inst.wl
+    return sca_forward(inst.value, inst.lidar2img, inst.z, inst.offsets, inst.logits, wl.levels,
+                       wl.heads, (wl.img_h, wl.img_w), wl.X, wl.Y, wl.x_min, wl.dx, wl.y_min,
+                       wl.dy, wl.depth_eps, reduce, nthreads, libpath)

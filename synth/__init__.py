@@ -28,7 +28,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Dict, List, Optional, Sequence
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -41,6 +41,11 @@ __all__ = [
     "make_features",
     "make_workload",
     "DTYPES",
+    "ScaWorkload",
+    "SCA_CONFIGS",
+    "sca_config",
+    "pillar_anchors",
+    "make_sca_workload",
 ]
 
 # Feature element types understood by the operator.
@@ -162,10 +167,11 @@ def camera_matrix(yaw: float, position: Sequence[float], fx: float, fy: float,
     return m
 
 
-def make_rig(wl: Workload, seed: Optional[Sequence[int]] = None) -> np.ndarray:
+def make_rig(wl, seed: Optional[Sequence[int]] = None) -> np.ndarray:
     """Seeded ``lidar2img`` [B, N, 4, 4] float32 for a ring rig.
 
     Every batch element draws its own jitter (independent rigs per sample).
+    ``wl`` is a :class:`Workload` or a :class:`ScaWorkload`.
     """
     rng = np.random.default_rng(list(seed) if seed is not None else [wl.cfg_id, 0])
     fx = fy = 0.75 * wl.img_w
@@ -244,3 +250,146 @@ def all_parity_workloads() -> List[Workload]:
     out = [CONFIGS["tiny"], CONFIGS["rep"], CONFIGS["half_batch"], CONFIGS["long_range"]]
     out += [CONFIGS["z_sweep"].with_(Z=z) for z in Z_SWEEP]
     return out
+
+
+# ---------------------------------------------------------------------------
+# FlashSCA (BEVFormer spatial cross-attention) inputs.
+#
+# The paper measures FlashSCA at BEVFormer-base defaults (Sec. 4.5, Table 7):
+# N=6 cameras, C=256, 8 heads, L=4 levels, BEV 200x200, Z=4 anchors and
+# P in {8, 16, 32} points.  BEVFormer-base takes 900x1600 images padded to
+# 928x1600 and a feature pyramid of strides 8, 16, 32, 64 (116x200, 58x100,
+# 29x50, 15x25); its BEV spans +-51.2 m (0.512 m cells) and its pillars
+# [-5, 3] m.  No trained weights or nuScenes data are used: the value maps
+# are standard normal (the output of a value projection), the attention
+# logits standard normal, and the sampling offsets follow the initial
+# pattern of BEVFormer's offset predictor (head m points along angle
+# 2 pi m / heads, point k at distance k + 1 pixels, on the square of the
+# direction's largest component) plus N(0, 1) pixel noise per component.
+# ---------------------------------------------------------------------------
+
+
+@dataclasses.dataclass(frozen=True)
+class ScaWorkload:
+    """One synthetic FlashSCA problem description."""
+
+    name: str
+    cfg_id: int
+    B: int
+    N: int
+    img_h: int
+    img_w: int
+    levels: Tuple[Tuple[int, int], ...]  # (H_l, W_l) per level
+    C: int
+    heads: int
+    P: int  # sampling points per (head, level)
+    Z: int  # pillar anchors
+    dtype: str
+    X: int
+    Y: int
+    x_min: float
+    dx: float
+    y_min: float
+    dy: float
+    z_lo: float = -5.0
+    z_hi: float = 3.0
+    offset_noise: float = 1.0
+    ring_radius: float = 1.0
+    mount_height: float = 1.5
+    jitter_deg: float = 2.0
+    jitter_m: float = 0.05
+    depth_eps: float = 1e-5
+
+    @property
+    def L(self) -> int:
+        return len(self.levels)
+
+    @property
+    def Q(self) -> int:
+        return self.X * self.Y
+
+    @property
+    def S(self) -> int:
+        """Value pixels per camera over all levels."""
+        return sum(h * w for h, w in self.levels)
+
+    def with_(self, **kw) -> "ScaWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+def pillar_anchors(z_lo: float, z_hi: float, Z: int) -> np.ndarray:
+    """Z anchor heights spread evenly from 0.5 m above the bottom of the
+    pillar [z_lo, z_hi] to 0.5 m below its top (float32), as BEVFormer
+    places its pillar points."""
+    if Z == 1:
+        return np.array([0.5 * (z_lo + z_hi)], dtype=np.float32)
+    k = np.arange(Z, dtype=np.float64)
+    return (z_lo + 0.5 + k * ((z_hi - z_lo) - 1.0) / (Z - 1)).astype(np.float32)
+
+
+_BEVFORMER_LEVELS = ((116, 200), (58, 100), (29, 50), (15, 25))
+
+
+def _sca(name, cfg_id, B, N, img_hw, levels, C, heads, P, Z, dtype, XY, half_range, **kw):
+    d = 2.0 * half_range / XY
+    return ScaWorkload(name=name, cfg_id=cfg_id, B=B, N=N, img_h=img_hw[0], img_w=img_hw[1],
+                       levels=tuple(levels), C=C, heads=heads, P=P, Z=Z, dtype=dtype, X=XY,
+                       Y=XY, x_min=-half_range, dx=d, y_min=-half_range, dy=d, **kw)
+
+
+SCA_CONFIGS: Dict[str, ScaWorkload] = {
+    # several tiles and a ragged tail, small enough for pure-Python checks
+    "sca_tiny": _sca("sca_tiny", 101, 1, 6, (256, 704), ((16, 44), (8, 22)), 32, 4, 4, 2,
+                     "f32", 23, 25.0),
+    # BEVFormer-base defaults (Table 7), P = 8
+    "sca_base": _sca("sca_base", 102, 1, 6, (900, 1600), _BEVFORMER_LEVELS, 256, 8, 8, 4,
+                     "f32", 200, 51.2),
+    # the same at half precision storage, two batch elements
+    "sca_base_bf16": _sca("sca_base_bf16", 103, 2, 6, (900, 1600), _BEVFORMER_LEVELS, 256, 8,
+                          8, 4, "bf16", 200, 51.2),
+}
+SCA_P_SWEEP = (8, 16, 32)
+
+
+def sca_config(name: str, **overrides) -> ScaWorkload:
+    wl = SCA_CONFIGS[name]
+    return wl.with_(**overrides) if overrides else wl
+
+
+@dataclasses.dataclass
+class ScaInstance:
+    """Concrete FlashSCA inputs."""
+
+    wl: ScaWorkload
+    value: np.ndarray  # [B, N, S, C] float32 (exact values of the storage dtype)
+    lidar2img: np.ndarray  # [B, N, 4, 4] float32
+    z: np.ndarray  # [Z] float32 anchor heights
+    offsets: np.ndarray  # [B, Q, heads, L, P, 2] float32, level pixels (x, y)
+    logits: np.ndarray  # [B, Q, heads, L, P] float32
+
+
+def sca_offsets(wl: ScaWorkload, rng) -> np.ndarray:
+    """Offsets in the initial pattern of BEVFormer's offset predictor, plus noise."""
+    H, L, P = wl.heads, wl.L, wl.P
+    theta = 2.0 * math.pi * np.arange(H) / H
+    g = np.stack([np.cos(theta), np.sin(theta)], axis=-1)  # [H, 2]
+    g = g / np.abs(g).max(axis=-1, keepdims=True)
+    base = g[:, None, None, :] * (np.arange(P) + 1.0)[None, None, :, None]  # [H, 1, P, 2]
+    base = np.broadcast_to(base, (H, L, P, 2))
+    noise = rng.standard_normal((wl.B, wl.Q, H, L, P, 2)) * wl.offset_noise
+    return (base[None, None] + noise).astype(np.float32)
+
+
+def make_sca_workload(wl: ScaWorkload, seed: Optional[Sequence[int]] = None) -> ScaInstance:
+    """Rig, value maps, anchors, offsets and logits for ``wl``."""
+    base = list(seed) if seed is not None else [wl.cfg_id]
+    rng = np.random.default_rng(base + [1])
+    v = rng.standard_normal((wl.B, wl.N, wl.S, wl.C), dtype=np.float32)
+    if wl.dtype != "f32":
+        v = round_to(v, wl.dtype)
+    rng2 = np.random.default_rng(base + [2])
+    offsets = sca_offsets(wl, rng2)
+    logits = rng2.standard_normal((wl.B, wl.Q, wl.heads, wl.L, wl.P), dtype=np.float32)
+    return ScaInstance(wl=wl, value=v, lidar2img=make_rig(wl, base + [0]),
+                       z=pillar_anchors(wl.z_lo, wl.z_hi, wl.Z), offsets=offsets,
+                       logits=logits)
