@@ -1,7 +1,7 @@
-"""Fused Sampling-VT forward (FlashBEV) for AMD MI355X.
+"""Fused Sampling-VT (FlashBEV) and FlashSCA for AMD MI355X.
 
-A thin Python binding over the C ABI of ``include/flashbev.h``
-(``libflashbev.so``).  It only marshals arguments: every step of the
+A thin Python binding over the C ABI of ``include/flashbev.h`` and
+``include/flashsca.h`` (``libflashbev.so``).  It only marshals arguments: every step of the
 operator runs in the library's HIP kernel.  PyTorch supplies device memory
 and the current stream.  If the built library is missing the calls raise;
 there is no fallback implementation.
@@ -15,6 +15,7 @@ from typing import Optional, Sequence, Tuple
 
 __all__ = [
     "BevGrid", "sample_vt", "sample_vt_backward", "prepare_sample_vt", "prepare_sample_vt_backward",
+    "sca_forward", "sca_forward_raw", "sca_launch_info", "prepare_sca_forward",
     "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
 ]
@@ -52,6 +53,21 @@ class GridSpec(ctypes.Structure):
     _fields_ = [("x_min", ctypes.c_float), ("dx", ctypes.c_float), ("X", ctypes.c_int32),
                 ("y_min", ctypes.c_float), ("dy", ctypes.c_float), ("Y", ctypes.c_int32),
                 ("depth_eps", ctypes.c_float), ("reduce", ctypes.c_int32)]
+
+
+SCA_LMAX = 8
+SCA_NMAX = 32
+SCA_ZMAX = 32
+SCA_LPMAX = 512
+SCA_HEAD_BYTES_MAX = 1024
+
+
+class ScaValue(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32),
+                ("B", ctypes.c_int32), ("N", ctypes.c_int32), ("C", ctypes.c_int32),
+                ("heads", ctypes.c_int32), ("L", ctypes.c_int32),
+                ("level_h", ctypes.c_int32 * SCA_LMAX), ("level_w", ctypes.c_int32 * SCA_LMAX),
+                ("img_h", ctypes.c_int32), ("img_w", ctypes.c_int32)]
 
 
 class ZBins(ctypes.Structure):
@@ -104,6 +120,15 @@ def _lib():
                                                     P(ctypes.c_int32), P(ctypes.c_int32),
                                                     P(ctypes.c_int32)]
         L.flashbev_backward_launch_info.restype = ctypes.c_int
+        L.flashsca_forward.argtypes = [P(ScaValue), ctypes.c_void_p, P(GridSpec), P(ZBins),
+                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p]
+        L.flashsca_forward.restype = ctypes.c_int
+        L.flashsca_launch_info.argtypes = [P(ScaValue), P(GridSpec), P(ZBins), ctypes.c_int32,
+                                           P(ctypes.c_int64), P(ctypes.c_int32),
+                                           P(ctypes.c_int32), P(ctypes.c_int32),
+                                           P(ctypes.c_int32)]
+        L.flashsca_launch_info.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -378,3 +403,146 @@ def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_h
     return _Prepared(_lib().flashbev_sample_vt_backward, args,
                      (grad_out, lidar2img, grad_features, z, f, g, zb),
                      "flashbev_sample_vt_backward")
+
+
+# ---------------------------------------------------------------------------
+# FlashSCA (include/flashsca.h)
+# ---------------------------------------------------------------------------
+
+
+def _sca_structs(shape, dtype_code, data_ptr, heads, levels, img_hw, grid: BevGrid, z, reduce):
+    B, N, S, C = (int(v) for v in shape)
+    L = len(levels)
+    if not 1 <= L <= SCA_LMAX:
+        raise ValueError(f"between 1 and {SCA_LMAX} levels are supported")
+    lh = (ctypes.c_int32 * SCA_LMAX)(*[int(h) for h, _ in levels], *([0] * (SCA_LMAX - L)))
+    lw = (ctypes.c_int32 * SCA_LMAX)(*[int(w) for _, w in levels], *([0] * (SCA_LMAX - L)))
+    v = ScaValue(data_ptr, dtype_code, B, N, C, int(heads), L, lh, lw, int(img_hw[0]),
+                 int(img_hw[1]))
+    g = GridSpec(grid.x_min, grid.dx, grid.X, grid.y_min, grid.dy, grid.Y, grid.depth_eps,
+                 REDUCE_CODES[reduce])
+    zb = ZBins(z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(z))
+    return v, g, zb
+
+
+def _sca_check(value, lidar2img, offsets, logits, levels, heads, grid):
+    import torch
+
+    if value.dim() != 4:
+        raise ValueError("value must be [B, N, S, C]")
+    for name, t in (("value", value), ("lidar2img", lidar2img), ("offsets", offsets),
+                    ("logits", logits)):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    for name, t in (("lidar2img", lidar2img), ("offsets", offsets), ("logits", logits)):
+        if t.dtype != torch.float32:
+            raise ValueError(f"{name} must be float32")
+    B, N, S, C = value.shape
+    if S != sum(int(h) * int(w) for h, w in levels):
+        raise ValueError("value's S must equal the sum of the levels' H * W")
+    if tuple(lidar2img.shape) != (B, N, 4, 4):
+        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
+    Q = grid.X * grid.Y
+    if logits.dim() != 5 or tuple(logits.shape[:4]) != (B, Q, heads, len(levels)):
+        raise ValueError(f"logits must be [{B}, {Q}, {heads}, {len(levels)}, P]")
+    P = int(logits.shape[4])
+    if tuple(offsets.shape) != (B, Q, heads, len(levels), P, 2):
+        raise ValueError(f"offsets must be [{B}, {Q}, {heads}, {len(levels)}, {P}, 2]")
+    return B, N, S, C, Q, P
+
+
+def sca_forward(value, lidar2img, anchors, grid: BevGrid, img_hw: Tuple[int, int], levels,
+                heads: int, offsets, logits, out=None, reduce: str = "mean", stream=None):
+    """FlashSCA forward (BEVFormer spatial cross-attention, Sec. 4.5) on the GPU.
+
+    value      CUDA tensor [B, N, S, C] (float32, float16 or bfloat16): the
+               value maps of all levels, concatenated, channel-last.
+    lidar2img  CUDA float32 tensor [B, N, 4, 4].
+    anchors    pillar heights in metres (host sequence, numpy array or tensor).
+    grid       BevGrid of the queries (query q = i * Y + j).
+    img_hw     (img_h, img_w) of the image lidar2img projects into.
+    levels     sequence of (H_l, W_l).
+    heads      number of attention heads (C % heads == 0).
+    offsets    CUDA float32 tensor [B, X*Y, heads, L, P, 2], level pixels.
+    logits     CUDA float32 tensor [B, X*Y, heads, L, P].
+    out        optional CUDA float32 tensor [B, X*Y, C].
+    reduce     "mean" over hit cameras (BEVFormer) or "sum".
+
+    Returns ``out``.  Asynchronous on ``stream`` (default: the current one).
+    """
+    import torch
+
+    B, N, S, C, Q, P = _sca_check(value, lidar2img, offsets, logits, levels, heads, grid)
+    if out is None:
+        out = torch.empty((B, Q, C), dtype=torch.float32, device=value.device)
+    elif out.dtype != torch.float32 or not out.is_contiguous() or tuple(out.shape) != (B, Q, C):
+        raise ValueError(f"out must be a contiguous float32 tensor [{B}, {Q}, {C}]")
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
+                            img_hw, grid, z, reduce)
+    s = _stream_handle(stream, value.device)
+    rc = _lib().flashsca_forward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
+                                 ctypes.byref(g), ctypes.byref(zb), P,
+                                 ctypes.c_void_p(offsets.data_ptr()),
+                                 ctypes.c_void_p(logits.data_ptr()),
+                                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
+    if rc != 0:
+        raise FlashBevError(rc, "flashsca_forward")
+    return out
+
+
+def sca_forward_raw(value_ptr: int, dtype: str, shape, heads: int, levels, lidar2img_ptr: int,
+                    anchors, grid: BevGrid, img_hw, P: int, offsets_ptr: int, logits_ptr: int,
+                    out_ptr: int, reduce: str = "mean", stream: int = 0) -> int:
+    """The FlashSCA C entry point with raw device addresses; returns the status."""
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(shape, DTYPE_CODES[dtype], value_ptr, heads, levels, img_hw, grid,
+                            z, reduce)
+    return int(_lib().flashsca_forward(ctypes.byref(v), ctypes.c_void_p(lidar2img_ptr),
+                                       ctypes.byref(g), ctypes.byref(zb), int(P),
+                                       ctypes.c_void_p(offsets_ptr), ctypes.c_void_p(logits_ptr),
+                                       ctypes.c_void_p(out_ptr), ctypes.c_void_p(stream)))
+
+
+def sca_launch_info(shape, dtype: str, heads: int, levels, anchors, grid: BevGrid, img_hw,
+                    P: int, reduce: str = "mean", data_ptr: int = 0) -> dict:
+    """Launch geometry of the FlashSCA forward for these arguments (no HIP call)."""
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(shape, DTYPE_CODES[dtype], data_ptr, heads, levels, img_hw, grid, z,
+                            reduce)
+    wg = ctypes.c_int64()
+    thr = ctypes.c_int32()
+    lds = ctypes.c_int32()
+    lph = ctypes.c_int32()
+    lw = ctypes.c_int32()
+    rc = _lib().flashsca_launch_info(ctypes.byref(v), ctypes.byref(g), ctypes.byref(zb), int(P),
+                                     ctypes.byref(wg), ctypes.byref(thr), ctypes.byref(lds),
+                                     ctypes.byref(lph), ctypes.byref(lw))
+    if rc != 0:
+        raise FlashBevError(rc, "flashsca_launch_info")
+    return {"workgroups": wg.value, "threads": thr.value, "lds_bytes": lds.value,
+            "lanes_per_head": lph.value, "lane_bytes": lw.value}
+
+
+def prepare_sca_forward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels, heads: int,
+                        offsets, logits, out, reduce: str = "mean", stream=None) -> _Prepared:
+    """``sca_forward`` with every argument fixed: a callable that enqueues the
+    same call again (same tensors, same stream)."""
+    import torch
+
+    B, N, S, C, Q, P = _sca_check(value, lidar2img, offsets, logits, levels, heads, grid)
+    if out.dtype != torch.float32 or not out.is_contiguous() or tuple(out.shape) != (B, Q, C) \
+            or not out.is_cuda:
+        raise ValueError(f"out must be a contiguous float32 device tensor [{B}, {Q}, {C}]")
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
+                            img_hw, grid, z, reduce)
+    s = _stream_handle(stream, value.device)
+    args = (ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_int32(P), ctypes.c_void_p(offsets.data_ptr()),
+            ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+            ctypes.c_void_p(s))
+    return _Prepared(_lib().flashsca_forward, args,
+                     (value, lidar2img, offsets, logits, out, z, v, g, zb), "flashsca_forward")

@@ -3,7 +3,8 @@
     python -m paper_2607_10071_amd.build
 
 Produces ``paper_2607_10071_amd/libflashbev.so`` (the fused Sampling-VT
-forward behind the C ABI of ``include/flashbev.h``) and
+forward and backward behind the C ABI of ``include/flashbev.h``, and FlashSCA
+behind ``include/flashsca.h``) and
 ``libflashbev_membench.so`` (the memory-ceiling micro-benchmarks of
 ``include/flashbev_membench.h`` that bench.py uses).
 """
@@ -17,6 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 INCLUDE = os.path.join(ROOT, "include")
 SRC = os.path.join(HERE, "csrc", "flashbev.hip")
+SCA_SRC = os.path.join(HERE, "csrc", "flashsca.hip")
 LIB = os.path.join(HERE, "libflashbev.so")
 # memory-ceiling micro-benchmarks used by bench.py (not part of the operator)
 MEMBENCH_SRC = os.path.join(HERE, "csrc", "membench.hip")
@@ -43,9 +45,9 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def _compile(src: str, lib: str, verbose: bool) -> str:
+def _compile(srcs, lib: str, verbose: bool) -> str:
     tmp = lib + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", src, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -58,8 +60,8 @@ def _compile(src: str, lib: str, verbose: bool) -> str:
 
 def build(verbose: bool = False) -> str:
     """Compile the operator library and the micro-benchmark library."""
-    _compile(MEMBENCH_SRC, MEMBENCH_LIB, verbose)
-    return _compile(SRC, LIB, verbose)
+    _compile([MEMBENCH_SRC], MEMBENCH_LIB, verbose)
+    return _compile([SRC, SCA_SRC], LIB, verbose)
 
 
 if __name__ == "__main__":

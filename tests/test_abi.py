@@ -24,13 +24,13 @@ HEADER = os.path.join(ROOT, "include", "flashbev.h")
 def declared_functions(header=HEADER):
     src = open(header).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(flashbev_\w+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(flash(?:bev|sca)_\w+)\s*\(", src)))
 
 
 def exported(lib_path):
     out = subprocess.run(["nm", "-D", "--defined-only", lib_path],
                          capture_output=True, text=True, check=True).stdout
-    return set(re.findall(r" T (flashbev_\w+)", out))
+    return set(re.findall(r" T (flash(?:bev|sca)_\w+)", out))
 
 
 def test_library_exports_every_declared_symbol():
@@ -40,20 +40,25 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(fb.library_path())
     for n in names:
         assert hasattr(lib, n), n
-    # everything declared is exported, and nothing else with the prefix leaks
-    assert exported(fb.library_path()) == set(names)
+    # everything declared is exported, and nothing else with the prefixes leaks
+    sca = declared_functions(os.path.join(ROOT, "include", "flashsca.h"))
+    assert exported(fb.library_path()) == set(names) | set(sca)
 
 
 def test_every_header_maps_to_a_library_that_exports_it():
     from paper_2607_10071_amd import membench
-    libs = {"flashbev.h": fb.library_path(), "flashbev_membench.h": membench._LIB_PATH}
+    libs = {"flashbev.h": fb.library_path(), "flashsca.h": fb.library_path(),
+            "flashbev_membench.h": membench._LIB_PATH}
     headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
     assert headers == sorted(libs)
+    per_lib = {}
     for h in headers:
         names = declared_functions(os.path.join(ROOT, "include", h))
         assert names, h
-        ctypes.CDLL(libs[h])
-        assert exported(libs[h]) == set(names), h
+        per_lib.setdefault(libs[h], set()).update(names)
+    for lib, names in per_lib.items():
+        ctypes.CDLL(lib)
+        assert exported(lib) == names, lib
 
 
 def test_abi_version_and_status_strings():

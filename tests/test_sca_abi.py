@@ -1,0 +1,159 @@
+"""FlashSCA C ABI: argument checks and launch geometry (CPU only).
+
+Every check of flashsca_forward runs before any HIP call, so the error paths
+run here without a GPU.  Device pointers are fake addresses that the library
+never dereferences because validation rejects the call first.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_10071_amd as fb
+from paper_2607_10071_amd import GridSpec, ScaValue, ZBins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+S = fb.STATUS
+VAL = 0x7F0000000000   # fake, 256-byte aligned device addresses
+L2I = 0x7F1000000000
+OFF = 0x7F2000000000
+LOG = 0x7F3000000000
+OUT = 0x7F4000000000
+LEVELS = ((116, 200), (58, 100), (29, 50), (15, 25))
+
+
+def call(B=1, N=6, C=256, heads=8, levels=LEVELS, dtype="f32", img=(900, 1600), X=200, Y=200,
+         z=(-4.5, -2.1666667, 0.16666667, 2.5), P=8, reduce="mean", val=VAL, l2i=L2I, off=OFF,
+         log=LOG, out=OUT, L=None, grid=None, zptr_null=False, Z=None, level_override=None):
+    z = np.asarray(z, np.float32)
+    nl = len(levels)
+    lh = (ctypes.c_int32 * 8)(*[h for h, _ in levels], *([0] * (8 - nl)))
+    lw = (ctypes.c_int32 * 8)(*[w for _, w in levels], *([0] * (8 - nl)))
+    if level_override:
+        i, h, w = level_override
+        lh[i], lw[i] = h, w
+    v = ScaValue(val, fb.DTYPE_CODES.get(dtype, dtype) if isinstance(dtype, str) else dtype,
+                 B, N, C, heads, nl if L is None else L, lh, lw, img[0], img[1])
+    g = grid or GridSpec(-51.2, 0.512, X, -51.2, 0.512, Y, 1e-5,
+                         fb.REDUCE_CODES.get(reduce, reduce) if isinstance(reduce, str) else reduce)
+    zb = ZBins(None if zptr_null else z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+               len(z) if Z is None else Z)
+    return fb._lib().flashsca_forward(ctypes.byref(v), ctypes.c_void_p(l2i), ctypes.byref(g),
+                                      ctypes.byref(zb), P, ctypes.c_void_p(off),
+                                      ctypes.c_void_p(log), ctypes.c_void_p(out),
+                                      ctypes.c_void_p(0))
+
+
+def test_header_constants_match_binding():
+    src = open(os.path.join(ROOT, "include", "flashsca.h")).read()
+    for k, v in (("FLASHSCA_LMAX", fb.SCA_LMAX), ("FLASHSCA_NMAX", fb.SCA_NMAX),
+                 ("FLASHSCA_ZMAX", fb.SCA_ZMAX), ("FLASHSCA_LPMAX", fb.SCA_LPMAX),
+                 ("FLASHSCA_HEAD_BYTES_MAX", fb.SCA_HEAD_BYTES_MAX)):
+        assert re.search(rf"#define {k} {v}\b", src), k
+
+
+def test_null_structs():
+    lib = fb._lib()
+    assert lib.flashsca_forward(None, None, None, None, 8, None, None, None, None) == S["ERR_NULLPTR"]
+    assert lib.flashsca_launch_info(None, None, None, 8, None, None, None, None, None) == \
+        S["ERR_NULLPTR"]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), "ERR_DTYPE"),
+    (dict(B=-1), "ERR_SHAPE"),
+    (dict(N=-1), "ERR_SHAPE"),
+    (dict(C=0), "ERR_SHAPE"),
+    (dict(heads=0), "ERR_SHAPE"),
+    (dict(C=255), "ERR_SHAPE"),                      # C % heads != 0
+    (dict(L=0), "ERR_SHAPE"),
+    (dict(L=9), "ERR_UNSUPPORTED"),
+    (dict(level_override=(2, 0, 50)), "ERR_SHAPE"),
+    (dict(img=(0, 1600)), "ERR_SHAPE"),
+    (dict(X=-1), "ERR_SHAPE"),
+    (dict(P=0), "ERR_SHAPE"),
+    (dict(P=6), "ERR_SHAPE"),                        # P % Z != 0
+    (dict(z=()), "ERR_SHAPE"),                       # no anchors
+    (dict(z=np.zeros(33)), "ERR_UNSUPPORTED"),       # Z > ZMAX (P stays a multiple)
+    (dict(N=33), "ERR_UNSUPPORTED"),
+    (dict(P=132), "ERR_UNSUPPORTED"),                # L * P > 512
+    (dict(C=2048, heads=4), "ERR_UNSUPPORTED"),      # 2 KiB head rows
+    (dict(levels=((30000, 30000),)), "ERR_UNSUPPORTED"),  # one camera over 2 GiB
+    (dict(zptr_null=True), "ERR_NULLPTR"),
+    (dict(reduce=3), "ERR_VALUE"),
+    (dict(grid=GridSpec(float("nan"), 0.5, 10, 0.0, 0.5, 10, 1e-5, 0)), "ERR_VALUE"),
+    (dict(out=0), "ERR_NULLPTR"),
+    (dict(off=0), "ERR_NULLPTR"),
+    (dict(log=0), "ERR_NULLPTR"),
+    (dict(val=0), "ERR_NULLPTR"),
+    (dict(l2i=0), "ERR_NULLPTR"),
+    (dict(val=VAL + 2), "ERR_ALIGN"),
+    (dict(val=VAL + 2, dtype="bf16"), "ERR_ALIAS"),   # 2-byte aligned bf16 is fine; see below
+    (dict(out=OUT + 2), "ERR_ALIGN"),
+    (dict(off=OFF + 4), "ERR_ALIGN"),                # offsets travel as float2
+    (dict(log=LOG + 1), "ERR_ALIGN"),
+    (dict(l2i=L2I + 2), "ERR_ALIGN"),
+    (dict(out=VAL + 4096), "ERR_ALIAS"),
+    (dict(out=OFF), "ERR_ALIAS"),
+    (dict(out=LOG + 64), "ERR_ALIAS"),
+])
+def test_argument_errors_before_any_hip_call(kw, status):
+    if kw.get("dtype") == "bf16" and kw.get("val") == VAL + 2:
+        # a bf16 value at a 2-byte aligned address passes alignment; make the
+        # output overlap it so the call still fails before any HIP call
+        kw = dict(kw, out=VAL + 64)
+    if "z" in kw and len(kw["z"]) == 33:
+        kw = dict(kw, P=33)
+    assert call(**kw) == S[status], kw
+
+
+def test_empty_outputs_enqueue_nothing():
+    # B = 0 or an empty grid: OK without touching the (null) device pointers
+    assert call(B=0, val=0, l2i=0, off=0, log=0, out=0) == S["OK"]
+    assert call(X=0, val=0, l2i=0, off=0, log=0, out=0) == S["OK"]
+
+
+def info(**kw):
+    d = dict(shape=(1, 6, sum(h * w for h, w in LEVELS), 256), dtype="f32", heads=8,
+             levels=LEVELS, anchors=[-4.5, -2.2, 0.2, 2.5],
+             grid=fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), img_hw=(900, 1600), P=8)
+    d.update(kw)
+    return fb.sca_launch_info(**d)
+
+
+def test_launch_geometry():
+    # BEVFormer-base: 8 lanes of 16 bytes per head, 8 heads per wavefront,
+    # 4 wavefronts (4 queries) per workgroup
+    g = info()
+    assert (g["lanes_per_head"], g["lane_bytes"], g["threads"]) == (8, 16, 256)
+    assert g["workgroups"] == 200 * 200 // 4
+    # bfloat16: 8-byte lanes, still 8 per head
+    g = info(dtype="bf16")
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (8, 8)
+    # D = 64 float32: 16 lanes per head, 4 heads per wavefront
+    g = info(shape=(1, 6, 30825, 512))
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (16, 16)
+    assert g["workgroups"] == 200 * 200 * 8 // 16
+    # D = 3 float32: three 4-byte lanes padded to four
+    g = info(shape=(1, 6, 30825, 12), heads=4)
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (4, 4)
+    # a value base that is only 4-byte aligned narrows the lanes
+    g = fb.sca_launch_info((1, 6, 30825, 256), "f32", 8, LEVELS, [0.0],
+                           fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), (900, 1600), 1,
+                           data_ptr=VAL + 4)
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (32, 4)
+    # LDS grows with L * P; past the budget the workgroup shrinks
+    lds = [info(P=p)["lds_bytes"] for p in (8, 16, 32)]
+    assert lds[0] < lds[1] < lds[2] <= 64 * 1024
+    g = info(P=128, levels=LEVELS, anchors=[0.0, 1.0, 2.0, 3.0])
+    assert g["threads"] < 256 and g["lds_bytes"] <= 64 * 1024
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        fb.sca_forward(torch.zeros(1, 6, 16, 8), torch.zeros(1, 6, 4, 4), [0.0],
+                       fb.BevGrid(0, 1, 2, 0, 1, 2), (32, 32), ((4, 4),), 2,
+                       torch.zeros(1, 4, 2, 1, 1, 2), torch.zeros(1, 4, 2, 1, 1))
