@@ -17,8 +17,10 @@ with HIP events on the launch stream), peak operator memory and the CPU
 oracle timed on the host as a reported baseline.  Unless --no-extra is
 given it also reports two more workloads, the measured memory ceilings and
 the backward (gradient w.r.t. the features) on this workload and on the
-paper's reference setting; --backward-only times just the backward, and
---sweep the scaling along height bins, grid size and channels.
+paper's reference setting, and FlashSCA (BEVFormer spatial cross-attention,
+Sec. 4.5) at BEVFormer-base defaults for P = 8, 16, 32; --backward-only
+times just the backward, --sca-only just FlashSCA, and --sweep the scaling
+along height bins, grid size and channels.
 """
 from __future__ import annotations
 
@@ -327,6 +329,138 @@ def sweep(device, steps: int, warmup: int) -> dict:
     return out
 
 
+def sca_algorithmic_bytes(wl) -> int:
+    """Compulsory HBM bytes of one FlashSCA call: every value element, offset,
+    logit and matrix read once, the output written once."""
+    value = wl.B * wl.N * wl.S * wl.C * elem_size(wl.dtype)
+    pts = wl.B * wl.Q * wl.heads * wl.L * wl.P
+    return value + pts * 2 * 4 + pts * 4 + wl.B * wl.N * 64 + wl.B * wl.Q * wl.C * 4
+
+
+def make_sca_call(wl, inst, device):
+    import torch
+
+    import paper_2607_10071_amd as fb
+
+    v = synth_to_storage(inst.value, wl.dtype).to(device)
+    l2i = torch.from_numpy(inst.lidar2img).to(device)
+    off = torch.from_numpy(inst.offsets).to(device)
+    lg = torch.from_numpy(inst.logits).to(device)
+    out = torch.empty((wl.B, wl.Q, wl.C), dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream(device)
+    call = fb.prepare_sca_forward(v, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w),
+                                  wl.levels, wl.heads, off, lg, out, stream=stream)
+    return call, (v, l2i, off, lg, out), stream
+
+
+def synth_to_storage(a, dtype):
+    import synth
+
+    return synth.to_storage(a, dtype)
+
+
+def sca_peak_memory(wl, inst, device) -> int:
+    """Allocator peak of one FlashSCA call that allocates its output, with the
+    inputs already resident."""
+    import torch
+
+    import paper_2607_10071_amd as fb
+
+    v = synth_to_storage(inst.value, wl.dtype).to(device)
+    l2i = torch.from_numpy(inst.lidar2img).to(device)
+    off = torch.from_numpy(inst.offsets).to(device)
+    lg = torch.from_numpy(inst.logits).to(device)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats(device)
+    base = torch.cuda.memory_allocated(device)
+    out = fb.sca_forward(v, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w), wl.levels,
+                         wl.heads, off, lg)
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated(device) - base
+    del out, v, l2i, off, lg
+    return int(peak)
+
+
+# Table 7 (RTX 4070 Ti SUPER, TensorRT, FP32, BEVFormer-base defaults)
+SCA_PAPER = {8: {"flashsca_ms": 5.27, "bevformersca_ms": 8.96, "flashsca_MB": 464,
+                 "bevformersca_MB": 1178},
+             16: {"flashsca_ms": 8.16, "bevformersca_ms": 15.81, "flashsca_MB": 698,
+                  "bevformersca_MB": 1990},
+             32: {"flashsca_ms": 13.90, "bevformersca_ms": 29.27, "flashsca_MB": 1168,
+                  "bevformersca_MB": 3708}}
+
+
+def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
+                points=(8, 16, 32), bf16: bool = True) -> dict:
+    """FlashSCA forward at BEVFormer-base defaults (Table 7's sweep over P)."""
+    import synth
+
+    base = synth.sca_config("sca_base")
+    rec = {"workload": f"sca_base: B={base.B} N={base.N} value levels "
+                       f"{'/'.join(f'{h}x{w}' for h, w in base.levels)} C={base.C} "
+                       f"heads={base.heads} {base.dtype} BEV {base.X}x{base.Y} Z={base.Z}",
+           "kernel": "sca_fwd", "points": {}}
+    for P in points:
+        wl = base.with_(P=P)
+        inst = synth.make_sca_workload(wl)
+        fn, keep, stream = make_sca_call(wl, inst, device)
+        t = time_gpu(fn, steps, warmup, stream, 0.1)
+        sec = t["ms_per_step"] * 1e-3
+        alg = sca_algorithmic_bytes(wl)
+        r = {"ms": round(t["ms_per_step"], 5),
+             "queries_per_s_M": round(wl.B * wl.Q / sec / 1e6, 2),
+             "algorithmic_bytes_per_launch": alg,
+             "hbm_GBs": round(alg / sec / 1e9, 1),
+             "hbm_frac": round(alg / sec / 1e9 / HBM_PEAK_GBS, 5),
+             "peak_op_memory_bytes": sca_peak_memory(wl, inst, device),
+             "paper_4070tis": SCA_PAPER.get(P)}
+        del fn, keep
+        if cpu:
+            cb = sca_cpu_baseline(inst, cpu_seconds)
+            counters = cb.pop("counters")
+            # gather roofline: in-range taps (counted by the oracle) times
+            # the head row, over the launch time
+            g = counters["taps"] * (wl.C // wl.heads) * elem_size(wl.dtype)
+            r["gather_bytes_per_launch"] = g
+            r["gather_GBs"] = round(g / sec / 1e9, 1)
+            r["taps"] = counters["taps"]
+            r["hits"] = counters["hits"]
+            r["cpu_baseline"] = cb
+        rec["points"][str(P)] = r
+    if bf16:
+        wl = synth.sca_config("sca_base_bf16")
+        inst = synth.make_sca_workload(wl)
+        fn, keep, stream = make_sca_call(wl, inst, device)
+        t = time_gpu(fn, steps, warmup, stream, 0.1)
+        sec = t["ms_per_step"] * 1e-3
+        alg = sca_algorithmic_bytes(wl)
+        rec["bf16_B2_P8"] = {"ms": round(t["ms_per_step"], 5),
+                             "queries_per_s_M": round(wl.B * wl.Q / sec / 1e6, 2),
+                             "hbm_frac": round(alg / sec / 1e9 / HBM_PEAK_GBS, 5)}
+        del fn, keep
+    return rec
+
+
+def sca_cpu_baseline(inst, min_seconds: float = 5.0) -> dict:
+    """The FlashSCA CPU oracle (float64, OpenMP) on the same workload."""
+    import oracle
+
+    threads = min(16, os.cpu_count() or 1)
+    _, _, _, counters = oracle.sca_instance(inst, nthreads=threads)  # warm-up
+    n, t0 = 0, time.perf_counter()
+    while True:
+        oracle.sca_instance(inst, nthreads=threads)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    per = el / n
+    wl = inst.wl
+    return {"value": round(wl.B * wl.Q / per / 1e6, 4), "unit": "Mqueries/s", "cores": threads,
+            "kind": "oracle", "ms_per_call": round(per * 1e3, 2), "calls": n,
+            "counters": counters}
+
+
 def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
     """The CPU oracle (float64, OpenMP) on the same workload, repeated until
     about `min_seconds` of work has been timed."""
@@ -363,6 +497,10 @@ def main(argv=None) -> int:
                          "paper's reference setting (one JSON line)")
     ap.add_argument("--backward-only", action="store_true",
                     help="time only the backward (gradient w.r.t. the features) on the workload")
+    ap.add_argument("--sca-only", action="store_true",
+                    help="time only the FlashSCA forward at BEVFormer-base defaults")
+    ap.add_argument("--sca-points", default="8,16,32",
+                    help="sampling points per (head, level) for --sca-only")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB three times "
                          "(a plain copy of known size that scales the HBM byte counters)")
@@ -392,6 +530,13 @@ def main(argv=None) -> int:
         del src, dst
     if args.sweep:
         print(json.dumps({"sweep": sweep(device, max(5, min(args.steps, 20)), 3)}), flush=True)
+        return 0
+    if args.sca_only:
+        pts = tuple(int(x) for x in args.sca_points.split(","))
+        rec = {"pass": "sca_forward", **measure_sca(device, args.steps, args.warmup,
+                                                    not args.no_cpu_baseline, 5.0, pts,
+                                                    bf16=False)}
+        print(json.dumps(rec), flush=True)
         return 0
     wl = synth.config(args.workload)
     inst = synth.make_workload(wl)
@@ -493,6 +638,9 @@ def main(argv=None) -> int:
             bwd[wl.name]["float_atomic_ceiling_Gops"] = ceil
             bwd[wl.name]["terms_over_atomic_ceiling"] = round(bwd[wl.name]["terms_G_per_s"] / ceil, 3)
         rec["backward"] = bwd
+        # FlashSCA (Sec. 4.5, Table 7) at BEVFormer-base defaults
+        rec["sca"] = measure_sca(device, max(20, args.steps // 4), args.warmup,
+                                 not args.no_cpu_baseline, 3.0)
 
     print(json.dumps(rec), flush=True)
     return 0

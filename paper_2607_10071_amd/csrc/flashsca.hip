@@ -45,7 +45,7 @@ constexpr int kScaWave = 64;
 constexpr int kScaWavesMax = 4;
 constexpr int kScaThreads = kScaWave * kScaWavesMax;
 constexpr int kScaXcds = 8;      // MI355X: workgroups are dispatched to 8 XCDs round-robin
-constexpr int kScaStripe = 16;   // consecutive tiles per XCD stripe
+constexpr int kScaBlock = 32;    // queries are visited in blocks of 32 x 32 BEV cells
 // Offset of a tap that is not loaded: one camera's value is smaller than
 // 2 GiB and a lane adds less than 1 KiB, so the load is past the buffer's end
 // and returns zero without touching memory.
@@ -73,6 +73,7 @@ struct ScaParams {
     int32_t spw;            // slots per wavefront
     int32_t tile_pairs;     // (query, head) pairs per workgroup
     int32_t tiles_per_b;
+    int32_t stripe;         // consecutive tiles an XCD takes in turn (about one block)
     int32_t nq_max;         // queries a tile can touch
     int32_t slot_stride;    // dwords per slot in the chunk-record area
     float img_w, img_h;
@@ -112,6 +113,25 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
     return s;
 }
 
+// Cell (i, j) of the query of rank r in the blocked visiting order: the grid
+// is cut into bands of kScaBlock rows; a band into blocks of kScaBlock
+// columns (the last band and block may be narrower); blocks follow each other
+// along the band, and a block's cells are row-major.  A bijection of
+// [0, X Y) onto the cells.
+__device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
+{
+    const int band_cells = kScaBlock * Y;
+    const int R = r / band_cells;
+    const int s = r - R * band_cells;
+    const int h = min(kScaBlock, X - R * kScaBlock);
+    const int c = s / (h * kScaBlock);
+    const int t = s - c * h * kScaBlock;
+    const int w = min(kScaBlock, Y - c * kScaBlock);
+    const int ti = t / w;
+    i = R * kScaBlock + ti;
+    j = c * kScaBlock + (t - ti * w);
+}
+
 template <int DT, int LW>
 __global__ void __launch_bounds__(kScaThreads)
 sca_fwd(const ScaParams p)
@@ -137,20 +157,32 @@ sca_fwd(const ScaParams p)
     const int lane = tid % kScaWave;
     const int N = p.N, Z = p.Z;
 
-    // XCD-aware tile order: the k-th workgroup on XCD x takes tile
-    // (k / S) * 8S + x * S + k % S, so each XCD works through stripes of S
-    // consecutive tiles (neighbouring queries sample neighbouring pixels,
-    // which then stay in that XCD's L2).
+    // XCD-aware tile order.  Queries are visited block by block (see
+    // query_of), so consecutive tiles cover a compact patch of the BEV whose
+    // samples land on overlapping pixels.  The k-th workgroup on XCD x takes
+    // tile (k / S) * 8S + x * S + k % S with S = p.stripe (about one block):
+    // an XCD works through whole blocks, its resident workgroups share their
+    // pixels in its L2, and the blocks of the 8 XCDs interleave over the
+    // grid (a like mix of heavy and light regions).  The tail that does not
+    // fill 8 stripes is split the same way with shorter stripes.
     const int g = blockIdx.x;
-    const int full = (int)(gridDim.x / (kScaXcds * kScaStripe)) * (kScaXcds * kScaStripe);
+    const int S8 = kScaXcds * p.stripe;
+    const int full = (int)(gridDim.x / S8) * S8;
     int tile = g;
     if (g < full) {
         const int xcd = g % kScaXcds, k = g / kScaXcds;
-        tile = (k / kScaStripe) * (kScaXcds * kScaStripe) + xcd * kScaStripe + k % kScaStripe;
+        tile = (k / p.stripe) * S8 + xcd * p.stripe + k % p.stripe;
+    } else {
+        const int rem = (int)gridDim.x - full;
+        const int s2 = rem / kScaXcds;
+        if (g - full < s2 * kScaXcds) {
+            const int xcd = (g - full) % kScaXcds, k = (g - full) / kScaXcds;
+            tile = full + xcd * s2 + k;
+        }
     }
     const int b = tile / p.tiles_per_b;
     const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
-    const int q_first = (int)(pair0 / p.heads);
+    const int r_first = (int)(pair0 / p.heads);   // first query rank of the tile
     const int64_t pairs_b = (int64_t)p.Q * p.heads;
 
     for (int t = tid; t < N * 12; t += nthreads) {
@@ -171,9 +203,10 @@ sca_fwd(const ScaParams p)
     // ---- phase 1: reference points of the tile's queries in every camera
     for (int t = tid; t < p.nq_max * N; t += nthreads) {
         const int qi = t / N, n = t - qi * N;
-        const int q = q_first + qi;
-        if (q >= p.Q) continue;
-        const int i = q / p.Y, j = q - i * p.Y;
+        const int rank = r_first + qi;
+        if (rank >= p.Q) continue;
+        int i, j;
+        query_of(rank, p.X, p.Y, i, j);
         const float x = p.x_min + ((float)i + 0.5f) * p.dx;
         const float y = p.y_min + ((float)j + 0.5f) * p.dy;
         const float *m = s_mat + n * 12;
@@ -201,9 +234,12 @@ sca_fwd(const ScaParams p)
     const int slot = lane >> p.lph_shift;
     const int64_t pair = pair0 + (int64_t)wave * p.spw + slot;
     const bool active = pair < pairs_b;
-    const int q = active ? (int)(pair / p.heads) : q_first;
-    const int mh = active ? (int)(pair - (int64_t)q * p.heads) : 0;
-    const int qi = q - q_first;
+    const int rank = active ? (int)(pair / p.heads) : r_first;
+    const int mh = active ? (int)(pair - (int64_t)rank * p.heads) : 0;
+    const int qi = rank - r_first;
+    int qx, qy;
+    query_of(rank, p.X, p.Y, qx, qy);
+    const int q = qx * p.Y + qy;             // the query's index in offsets, logits, out
     const uint32_t hits = active ? s_hit[qi] : 0u;
     const int count = __popc(hits);
     const float inv = (p.reduce == FLASHBEV_REDUCE_VALID_MEAN && count > 1) ? 1.0f / (float)count
@@ -467,6 +503,10 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
     p.tile_pairs = tile_pairs;
     const uint64_t pairs_b = Q * (uint64_t)v->heads;
     p.tiles_per_b = (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
+    {
+        const int64_t st = (int64_t)kScaBlock * kScaBlock * v->heads / tile_pairs;
+        p.stripe = (int32_t)(st < 1 ? 1 : (st > 4096 ? 4096 : st));
+    }
     p.nq_max = nq_max;
     p.slot_stride = slot_stride;
     p.img_w = (float)v->img_w;
