@@ -40,10 +40,11 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_10071_amd", "csrc", "flashbev.hip")
+SCA_KERNEL_SRC = os.path.join(ROOT, "paper_2607_10071_amd", "csrc", "flashsca.hip")
 
 
-def kernel_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
+def kernel_hash(path: str = KERNEL_SRC) -> str:
+    with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
@@ -71,7 +72,7 @@ def tensorized_footprint(wl) -> dict:
     return {"features3d_bytes": f3d, "alg1_all_writes_bytes": allw}
 
 
-def load_traffic(workload: str):
+def load_traffic(workload: str, src: str = KERNEL_SRC):
     """HBM traffic per launch from committed rocprofv3 counter passes, if
     they were taken on the current kernel source."""
     path = os.path.join(PROFILE_DIR, "traffic.json")
@@ -80,7 +81,7 @@ def load_traffic(workload: str):
     with open(path) as f:
         data = json.load(f)
     rec = data.get(workload)
-    if not rec or rec.get("kernel_sha") != kernel_hash():
+    if not rec or rec.get("kernel_sha") != kernel_hash(src):
         return None
     return rec.get("bytes_per_launch")
 
@@ -399,7 +400,7 @@ def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
     rec = {"workload": f"sca_base: B={base.B} N={base.N} value levels "
                        f"{'/'.join(f'{h}x{w}' for h, w in base.levels)} C={base.C} "
                        f"heads={base.heads} {base.dtype} BEV {base.X}x{base.Y} Z={base.Z}",
-           "kernel": "sca_fwd", "points": {}}
+           "kernel": "sca_fwd", "kernel_sha": kernel_hash(SCA_KERNEL_SRC), "points": {}}
     for P in points:
         wl = base.with_(P=P)
         inst = synth.make_sca_workload(wl)
@@ -413,6 +414,7 @@ def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
              "hbm_GBs": round(alg / sec / 1e9, 1),
              "hbm_frac": round(alg / sec / 1e9 / HBM_PEAK_GBS, 5),
              "peak_op_memory_bytes": sca_peak_memory(wl, inst, device),
+             "traffic": load_traffic(f"sca_base_p{P}", SCA_KERNEL_SRC),
              "paper_4070tis": SCA_PAPER.get(P)}
         del fn, keep
         if cpu:

@@ -129,9 +129,10 @@ def test_launch_geometry():
     g = info()
     assert (g["lanes_per_head"], g["lane_bytes"], g["threads"]) == (8, 16, 256)
     assert g["workgroups"] == 200 * 200 // 4
-    # bfloat16: 8-byte lanes, still 8 per head
+    # bfloat16: 16-byte lanes, 4 per head, two queries per wavefront
     g = info(dtype="bf16")
-    assert (g["lanes_per_head"], g["lane_bytes"]) == (8, 8)
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (4, 16)
+    assert g["workgroups"] == 200 * 200 // 8
     # D = 64 float32: 16 lanes per head, 4 heads per wavefront
     g = info(shape=(1, 6, 30825, 512))
     assert (g["lanes_per_head"], g["lane_bytes"]) == (16, 16)
@@ -139,6 +140,9 @@ def test_launch_geometry():
     # D = 3 float32: three 4-byte lanes padded to four
     g = info(shape=(1, 6, 30825, 12), heads=4)
     assert (g["lanes_per_head"], g["lane_bytes"]) == (4, 4)
+    # D = 8 float32 (32-byte head rows): four 8-byte lanes
+    g = info(shape=(1, 6, 30825, 32), heads=4)
+    assert (g["lanes_per_head"], g["lane_bytes"]) == (4, 8)
     # a value base that is only 4-byte aligned narrows the lanes
     g = fb.sca_launch_info((1, 6, 30825, 256), "f32", 8, LEVELS, [0.0],
                            fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), (900, 1600), 1,
