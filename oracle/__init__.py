@@ -237,6 +237,8 @@ def _sca_lib(path: Optional[str] = None):
     L.sca_oracle_forward.restype = ctypes.c_int
     L.sca_oracle_reference_points.argtypes = [P(ScaProblem)] + [ctypes.c_void_p] * 6
     L.sca_oracle_reference_points.restype = ctypes.c_int
+    L.sca_oracle_backward.argtypes = [P(ScaProblem)] + [ctypes.c_void_p] * 14 + [ctypes.c_int]
+    L.sca_oracle_backward.restype = ctypes.c_int
     return L
 
 
@@ -312,3 +314,52 @@ def sca_instance(inst, reduce="mean", nthreads=0, libpath=None):
     return sca_forward(inst.value, inst.lidar2img, inst.z, inst.offsets, inst.logits, wl.levels,
                        wl.heads, (wl.img_h, wl.img_w), wl.X, wl.Y, wl.x_min, wl.dx, wl.y_min,
                        wl.dy, wl.depth_eps, reduce, nthreads, libpath)
+
+
+def sca_backward(value, lidar2img, z, offsets, logits, grad_out, levels, heads, img_hw, X, Y,
+                 x_min, dx, y_min, dy, depth_eps=1e-5, reduce="mean", nthreads=0, libpath=None):
+    """Gradients of the FlashSCA forward with respect to the value maps, the
+    offsets and the logits, for output gradient ``grad_out`` [B, X*Y, C].
+
+    Returns a dict of float64 arrays: ``value`` [B, N, S, C] with
+    ``value_scale`` and int32 ``value_terms`` [B, N, S, heads]; ``offsets``
+    [B, X*Y, heads, L, P, 2] with ``offsets_scale``; ``logits``
+    [B, X*Y, heads, L, P] with ``logits_scale``; int32 ``point_terms``
+    [B, X*Y, heads, L, P] (in-range corners per point over hit cameras).
+    """
+    v = np.ascontiguousarray(value, dtype=np.float32)
+    m = np.ascontiguousarray(lidar2img, dtype=np.float32)
+    zz = np.ascontiguousarray(z, dtype=np.float32)
+    off = np.ascontiguousarray(offsets, dtype=np.float32)
+    lg = np.ascontiguousarray(logits, dtype=np.float32)
+    g = np.ascontiguousarray(grad_out, dtype=np.float32)
+    B, N, S, C = v.shape
+    L = len(levels)
+    P = lg.shape[-1]
+    Q = X * Y
+    assert g.shape == (B, Q, C) and lg.shape == (B, Q, heads, L, P) and off.shape == lg.shape + (2,)
+    p = sca_problem(B, N, C, heads, levels, P, len(zz), img_hw, X, Y, x_min, dx, y_min, dy,
+                    depth_eps, reduce)
+    r = {
+        "value": np.empty((B, N, S, C)), "value_scale": np.empty((B, N, S, C)),
+        "value_terms": np.empty((B, N, S, heads), dtype=np.int32),
+        "offsets": np.empty((B, Q, heads, L, P, 2)), "offsets_scale": np.empty((B, Q, heads, L, P, 2)),
+        "logits": np.empty((B, Q, heads, L, P)), "logits_scale": np.empty((B, Q, heads, L, P)),
+        "point_terms": np.empty((B, Q, heads, L, P), dtype=np.int32),
+    }
+    rc = _sca_lib(libpath).sca_oracle_backward(
+        ctypes.byref(p), _ptr(v), _ptr(m), _ptr(zz), _ptr(off), _ptr(lg), _ptr(g),
+        _ptr(r["value"]), _ptr(r["value_scale"]), _ptr(r["value_terms"]), _ptr(r["offsets"]),
+        _ptr(r["offsets_scale"]), _ptr(r["logits"]), _ptr(r["logits_scale"]),
+        _ptr(r["point_terms"]), int(nthreads))
+    if rc:
+        raise ValueError(f"sca_oracle_backward failed: {rc}")
+    return r
+
+
+def sca_backward_instance(inst, grad_out, reduce="mean", nthreads=0, libpath=None):
+    """FlashSCA backward oracle on a ``synth.ScaInstance``."""
+    wl = inst.wl
+    return sca_backward(inst.value, inst.lidar2img, inst.z, inst.offsets, inst.logits, grad_out,
+                        wl.levels, wl.heads, (wl.img_h, wl.img_w), wl.X, wl.Y, wl.x_min, wl.dx,
+                        wl.y_min, wl.dy, wl.depth_eps, reduce, nthreads, libpath)

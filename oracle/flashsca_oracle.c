@@ -121,20 +121,18 @@ static int reference_point(const sca_problem *p, const float *m, float x, float 
 }
 
 /*
- * One query: all C channels of out[b, q, :], their scales, and the tap count
- * per head.  acc and scale hold C values; terms holds `heads` values.
- * Scratch: un, vn [N*Z] floats, hit [N] ints, attn [heads*L*P] doubles.
+ * Steps 1 and 2 for query (b, i, j): reference points of every anchor in
+ * every camera (un, vn [N*Z]), hit cameras (hit [N]) and the attention
+ * weights, a softmax over the L*P logits of each head (attn [heads*L*P]).
+ * Returns the number of hit cameras.
  */
-static void one_query(const sca_problem *p, const float *value, const float *l2i,
-                      const float *zs, const float *offsets, const float *logits, int b, int i,
-                      int j, double *acc, double *scale, int32_t *terms, float *un, float *vn,
-                      int *hit, double *attn, sca_counters *cnt)
+static int prepare_query(const sca_problem *p, const float *l2i, const float *zs,
+                         const float *logits, int b, int i, int j, float *un, float *vn,
+                         int *hit, double *attn)
 {
-    const int N = p->N, Z = p->Z, C = p->C, H = p->heads, L = p->L, P = p->P;
-    const int D = C / H;
+    const int N = p->N, Z = p->Z, H = p->heads, L = p->L, P = p->P;
     const int64_t Q = (int64_t)p->X * p->Y;
     const int64_t q = (int64_t)i * p->Y + j;
-    const int64_t S = sca_pixels(p);
     float x, y;
     cell_centre(p, i, j, &x, &y);
 
@@ -161,6 +159,77 @@ static void one_query(const sca_problem *p, const float *value, const float *l2i
         }
         for (int t = 0; t < L * P; ++t) attn[h * L * P + t] /= sum;
     }
+    return count;
+}
+
+/* The anchor of point k: BEVFormer splits a level's P points into P / Z
+ * groups of Z consecutive points, one per anchor. */
+static int anchor_of_point(int k, int P, int Z)
+{
+    (void)P;
+    return k % Z;
+}
+
+/*
+ * Bilinear corners of point (h, l, k) of a query in one camera: the sampling
+ * location (x, y) in level-l pixels from the anchor's reference point
+ * (un, vn) and the offset o, then the four corners (x0 + tx, y0 + ty),
+ * tx, ty in {0, 1}, in the order 00, 01 (right), 10 (below), 11, with their
+ * weights and whether each lies inside the map (zero padding otherwise).
+ * Returns 0 when no corner lies inside the map (also for a location that is
+ * not finite); the fractions are written to *fx, *fy.
+ */
+typedef struct {
+    int64_t pix[4];          /* pixel index within the camera's value, all levels */
+    int in[4];               /* corner inside the level's map */
+    double w[4];             /* bilinear weight */
+} corners;
+
+static int point_corners(const sca_problem *p, int l, int64_t start, float un, float vn,
+                         const float *o, corners *cr, double *fx, double *fy)
+{
+    const int Hl = p->level_h[l], Wl = p->level_w[l];
+    float sx = un * (float)Wl;
+    float sy = vn * (float)Hl;
+    sx = sx + o[0];
+    sy = sy + o[1];
+    const float xim = sx - 0.5f;
+    const float yim = sy - 0.5f;
+    /* no corner inside the map (also non-finite locations) */
+    if (!(xim > -1.0f && xim < (float)Wl && yim > -1.0f && yim < (float)Hl))
+        return 0;
+    const float x0f = floorf(xim), y0f = floorf(yim);
+    const double ax = (double)(xim - x0f), ay = (double)(yim - y0f);
+    const int x0 = (int)x0f, y0 = (int)y0f;
+    for (int ty = 0; ty < 2; ++ty)
+        for (int tx = 0; tx < 2; ++tx) {
+            const int c = ty * 2 + tx;
+            const int xt = x0 + tx, yt = y0 + ty;
+            cr->in[c] = !(xt < 0 || xt >= Wl || yt < 0 || yt >= Hl);
+            cr->w[c] = (tx ? ax : 1.0 - ax) * (ty ? ay : 1.0 - ay);
+            cr->pix[c] = cr->in[c] ? start + (int64_t)yt * Wl + xt : 0;
+        }
+    *fx = ax;
+    *fy = ay;
+    return 1;
+}
+
+/*
+ * One query: all C channels of out[b, q, :], their scales, and the tap count
+ * per head.  acc and scale hold C values; terms holds `heads` values.
+ * Scratch: un, vn [N*Z] floats, hit [N] ints, attn [heads*L*P] doubles.
+ */
+static void one_query(const sca_problem *p, const float *value, const float *l2i,
+                      const float *zs, const float *offsets, const float *logits, int b, int i,
+                      int j, double *acc, double *scale, int32_t *terms, float *un, float *vn,
+                      int *hit, double *attn, sca_counters *cnt)
+{
+    const int N = p->N, Z = p->Z, C = p->C, H = p->heads, L = p->L, P = p->P;
+    const int D = C / H;
+    const int64_t Q = (int64_t)p->X * p->Y;
+    const int64_t q = (int64_t)i * p->Y + j;
+    const int64_t S = sca_pixels(p);
+    const int count = prepare_query(p, l2i, zs, logits, b, i, j, un, vn, hit, attn);
 
     /* 3. deformable sampling in every hit camera, summed over cameras */
     for (int c = 0; c < C; ++c) { acc[c] = 0.0; scale[c] = 0.0; }
@@ -173,40 +242,28 @@ static void one_query(const sca_problem *p, const float *value, const float *l2i
         for (int h = 0; h < H; ++h) {
             int64_t start = 0;
             for (int l = 0; l < L; ++l) {
-                const int Hl = p->level_h[l], Wl = p->level_w[l];
                 for (int k = 0; k < P; ++k) {
-                    const int z = k % Z;                 /* the point's anchor */
+                    const int z = anchor_of_point(k, P, Z);
                     const float *o = off + (((size_t)h * L + l) * P + k) * 2;
-                    float sx = un[n * Z + z] * (float)Wl;
-                    float sy = vn[n * Z + z] * (float)Hl;
-                    sx = sx + o[0];
-                    sy = sy + o[1];
-                    const float xim = sx - 0.5f;
-                    const float yim = sy - 0.5f;
-                    /* no corner inside the map (also non-finite locations) */
-                    if (!(xim > -1.0f && xim < (float)Wl && yim > -1.0f && yim < (float)Hl))
+                    corners cr;
+                    double fx, fy;
+                    if (!point_corners(p, l, start, un[n * Z + z], vn[n * Z + z], o, &cr, &fx,
+                                       &fy))
                         continue;
-                    const float x0f = floorf(xim), y0f = floorf(yim);
-                    const double ax = (double)(xim - x0f), ay = (double)(yim - y0f);
-                    const int x0 = (int)x0f, y0 = (int)y0f;
                     const double a = attn[(h * L + l) * P + k];
-                    for (int ty = 0; ty < 2; ++ty)
-                        for (int tx = 0; tx < 2; ++tx) {
-                            const int xt = x0 + tx, yt = y0 + ty;
-                            if (xt < 0 || xt >= Wl || yt < 0 || yt >= Hl) continue;
-                            const double w = (tx ? ax : 1.0 - ax) * (ty ? ay : 1.0 - ay);
-                            const float *row = vcam + (size_t)(start + (int64_t)yt * Wl + xt) * C
-                                               + (size_t)h * D;
-                            for (int e = 0; e < D; ++e) {
-                                const double t = a * w * (double)row[e];
-                                acc[h * D + e] += t;
-                                scale[h * D + e] += fabs(t);
-                            }
-                            terms[h] += 1;
-                            if (cnt) cnt->taps += 1;
+                    for (int t = 0; t < 4; ++t) {
+                        if (!cr.in[t]) continue;
+                        const float *row = vcam + (size_t)cr.pix[t] * C + (size_t)h * D;
+                        for (int e = 0; e < D; ++e) {
+                            const double v = a * cr.w[t] * (double)row[e];
+                            acc[h * D + e] += v;
+                            scale[h * D + e] += fabs(v);
                         }
+                        terms[h] += 1;
+                        if (cnt) cnt->taps += 1;
+                    }
                 }
-                start += (int64_t)Hl * Wl;
+                start += (int64_t)p->level_h[l] * p->level_w[l];
             }
         }
     }
@@ -310,5 +367,207 @@ int sca_oracle_reference_points(const sca_problem *p, const float *l2i, const fl
                     hit[q * N + n] = (uint8_t)any;
                 }
             }
+    return 0;
+}
+
+/*
+ * Backward of the FlashSCA forward with respect to its learned inputs: the
+ * value maps, the sampling offsets and the attention logits (the camera
+ * matrices and anchors get no gradient).  With G = dL/d out and
+ * alpha = 1 / max(1, hits) (1 in sum mode), every term of the forward,
+ * alpha a w V[tap, c] for a point (head h, level l, point k) in hit camera n,
+ * gives:
+ *
+ *   d value[b, n, tap, c]  += alpha a w G[b, q, c]                  (scatter)
+ *   d a                    += alpha w V[tap, c] G[b, q, c]
+ *   d x                    += alpha a (dw / dx) V[tap, c] G[b, q, c]
+ *
+ * where x, y is the sampling location in level pixels and w the bilinear
+ * weight of the tap, (1 - ax)(1 - ay), ax (1 - ay), (1 - ax) ay or ax ay with
+ * (ax, ay) the location's fractional part; a location moves one pixel per
+ * pixel of offset, so d offset = (d x, d y).  Taps outside the map have value
+ * zero (zero padding) and points with no corner inside the map contribute
+ * nothing.  The logits' gradient is the softmax backward over the head's
+ * L * P pairs: d s_j = a_j (d a_j - sum_j' a_j' d a_j').
+ *
+ * Outputs (float64), with magnitude scales that bound a float32
+ * implementation's rounding error:
+ *   grad_value [B, N, S, C], scale_value (sum of |terms|), terms_value
+ *     [B, N, S, heads] (terms reaching the pixel's head slice)
+ *   grad_offsets [B, Q, heads, L, P, 2], scale_offsets (sum over cameras
+ *     and channels of alpha a |G| ((1 - ay)(|V01| + |V00|) + ay (|V11| + |V10|))
+ *     for x, and likewise for y)
+ *   grad_logits [B, Q, heads, L, P], scale_logits (a_j (S_j + sum_j' a_j' S_j')
+ *     with S_j the sum of |terms| of d a_j)
+ *   terms_points [B, Q, heads, L, P] int32: in-range corners of the point
+ *     over the hit cameras
+ * Any of the scale and terms arrays may be NULL.
+ *
+ * Computed in two passes: per query (offsets and logits; reads only), then
+ * one camera (b, n) per task for the value scatter, which writes only that
+ * camera's slice.
+ */
+int sca_oracle_backward(const sca_problem *p, const float *value, const float *l2i,
+                        const float *zs, const float *offsets, const float *logits,
+                        const float *grad_out, double *grad_value, double *scale_value,
+                        int32_t *terms_value, double *grad_offsets, double *scale_offsets,
+                        double *grad_logits, double *scale_logits, int32_t *terms_points,
+                        int nthreads)
+{
+    int rc = check(p);
+    if (rc) return rc;
+    const int N = p->N, Z = p->Z, C = p->C, H = p->heads, L = p->L, P = p->P;
+    const int D = C / H;
+    const int LP = L * P;
+    const int64_t Q = (int64_t)p->X * p->Y;
+    const int64_t S = sca_pixels(p);
+    const int64_t rows = (int64_t)p->B * p->X;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    /* pass 1: per query, gradients of the offsets and logits */
+#pragma omp parallel
+    {
+        double *attn = (double *)malloc(sizeof(double) * (size_t)H * LP);
+        double *da = (double *)malloc(sizeof(double) * (size_t)LP * 6);
+        float *uv = (float *)malloc(sizeof(float) * 2 * (size_t)(N * Z + 1));
+        int *hit = (int *)malloc(sizeof(int) * (size_t)(N + 1));
+        int32_t *kt = (int32_t *)malloc(sizeof(int32_t) * (size_t)LP);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < rows; ++r) {
+            const int b = (int)(r / p->X), i = (int)(r % p->X);
+            for (int j = 0; j < p->Y; ++j) {
+                float *un = uv, *vn = uv + N * Z;
+                const int count = prepare_query(p, l2i, zs, logits, b, i, j, un, vn, hit, attn);
+                const double alpha = (p->reduce == 0 && count > 1) ? 1.0 / (double)count : 1.0;
+                const int64_t q = (int64_t)i * p->Y + j;
+                const float *off = offsets + ((size_t)b * Q + q) * (size_t)H * LP * 2;
+                const float *g = grad_out + ((size_t)b * Q + q) * C;
+                for (int h = 0; h < H; ++h) {
+                    /* da[t]: d a; da[LP + t], da[2LP + t]: d x, d y (before alpha a);
+                     * da[3LP..]: their scales */
+                    for (int t = 0; t < 6 * LP; ++t) da[t] = 0.0;
+                    for (int t = 0; t < LP; ++t) kt[t] = 0;
+                    for (int n = 0; n < N; ++n) {
+                        if (!hit[n]) continue;
+                        const float *vcam = value + ((size_t)b * N + n) * (size_t)S * C;
+                        int64_t start = 0;
+                        for (int l = 0; l < L; ++l) {
+                            for (int k = 0; k < P; ++k) {
+                                const int z = anchor_of_point(k, P, Z);
+                                const int t = l * P + k;
+                                corners cr;
+                                double ax, ay;
+                                if (!point_corners(p, l, start, un[n * Z + z], vn[n * Z + z],
+                                                   off + (((size_t)h * L + l) * P + k) * 2, &cr,
+                                                   &ax, &ay))
+                                    continue;
+                                for (int c4 = 0; c4 < 4; ++c4) kt[t] += cr.in[c4];
+                                for (int e = 0; e < D; ++e) {
+                                    double v[4];
+                                    for (int c4 = 0; c4 < 4; ++c4)
+                                        v[c4] = cr.in[c4]
+                                            ? (double)vcam[(size_t)cr.pix[c4] * C + (size_t)h * D + e]
+                                            : 0.0;
+                                    const double ge = (double)g[h * D + e];
+                                    double smp = 0.0, mag = 0.0;
+                                    for (int c4 = 0; c4 < 4; ++c4) {
+                                        smp += cr.w[c4] * v[c4];
+                                        mag += cr.w[c4] * fabs(v[c4]);
+                                    }
+                                    da[t] += ge * smp;
+                                    da[3 * LP + t] += fabs(ge) * mag;
+                                    /* corners: 0 = (x0, y0), 1 = (x0 + 1, y0), 2 = (x0, y0 + 1), 3 */
+                                    da[LP + t] += ge * ((1.0 - ay) * (v[1] - v[0]) + ay * (v[3] - v[2]));
+                                    da[4 * LP + t] += fabs(ge) * ((1.0 - ay) * (fabs(v[1]) + fabs(v[0]))
+                                                                  + ay * (fabs(v[3]) + fabs(v[2])));
+                                    da[2 * LP + t] += ge * ((1.0 - ax) * (v[2] - v[0]) + ax * (v[3] - v[1]));
+                                    da[5 * LP + t] += fabs(ge) * ((1.0 - ax) * (fabs(v[2]) + fabs(v[0]))
+                                                                  + ax * (fabs(v[3]) + fabs(v[1])));
+                                }
+                            }
+                            start += (int64_t)p->level_h[l] * p->level_w[l];
+                        }
+                    }
+                    /* softmax backward over the head's L*P pairs */
+                    const double *a = attn + (size_t)h * LP;
+                    double dot = 0.0, sdot = 0.0;
+                    for (int t = 0; t < LP; ++t) {
+                        dot += a[t] * alpha * da[t];
+                        sdot += a[t] * alpha * da[3 * LP + t];
+                    }
+                    const size_t o = (((size_t)b * Q + q) * H + h) * LP;
+                    for (int t = 0; t < LP; ++t) {
+                        grad_logits[o + t] = a[t] * (alpha * da[t] - dot);
+                        if (scale_logits) scale_logits[o + t] = a[t] * (alpha * da[3 * LP + t] + sdot);
+                        grad_offsets[(o + t) * 2 + 0] = alpha * a[t] * da[LP + t];
+                        grad_offsets[(o + t) * 2 + 1] = alpha * a[t] * da[2 * LP + t];
+                        if (scale_offsets) {
+                            scale_offsets[(o + t) * 2 + 0] = alpha * a[t] * da[4 * LP + t];
+                            scale_offsets[(o + t) * 2 + 1] = alpha * a[t] * da[5 * LP + t];
+                        }
+                        if (terms_points) terms_points[o + t] = kt[t];
+                    }
+                }
+            }
+        }
+        free(attn); free(da); free(uv); free(hit); free(kt);
+    }
+    /* pass 2: value scatter, one camera (b, n) per task */
+#pragma omp parallel
+    {
+        double *attn = (double *)malloc(sizeof(double) * (size_t)H * LP);
+        float *uv = (float *)malloc(sizeof(float) * 2 * (size_t)(N * Z + 1));
+        int *hit = (int *)malloc(sizeof(int) * (size_t)(N + 1));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t bn = 0; bn < (int64_t)p->B * N; ++bn) {
+            const int b = (int)(bn / N), n = (int)(bn % N);
+            double *gv = grad_value + (size_t)bn * S * C;
+            double *sv = scale_value ? scale_value + (size_t)bn * S * C : NULL;
+            int32_t *tv = terms_value ? terms_value + (size_t)bn * S * H : NULL;
+            memset(gv, 0, sizeof(double) * (size_t)S * C);
+            if (sv) memset(sv, 0, sizeof(double) * (size_t)S * C);
+            if (tv) memset(tv, 0, sizeof(int32_t) * (size_t)S * H);
+            for (int i = 0; i < p->X; ++i)
+                for (int j = 0; j < p->Y; ++j) {
+                    float *un = uv, *vn = uv + N * Z;
+                    const int count = prepare_query(p, l2i, zs, logits, b, i, j, un, vn, hit, attn);
+                    if (!hit[n]) continue;
+                    const double alpha = (p->reduce == 0 && count > 1) ? 1.0 / (double)count : 1.0;
+                    const int64_t q = (int64_t)i * p->Y + j;
+                    const float *off = offsets + ((size_t)b * Q + q) * (size_t)H * LP * 2;
+                    const float *g = grad_out + ((size_t)b * Q + q) * C;
+                    for (int h = 0; h < H; ++h) {
+                        int64_t start = 0;
+                        for (int l = 0; l < L; ++l) {
+                            for (int k = 0; k < P; ++k) {
+                                const int z = anchor_of_point(k, P, Z);
+                                corners cr;
+                                double ax, ay;
+                                if (!point_corners(p, l, start, un[n * Z + z], vn[n * Z + z],
+                                                   off + (((size_t)h * L + l) * P + k) * 2, &cr,
+                                                   &ax, &ay))
+                                    continue;
+                                const double wa = alpha * attn[(size_t)h * LP + l * P + k];
+                                for (int c4 = 0; c4 < 4; ++c4) {
+                                    if (!cr.in[c4]) continue;
+                                    double *dst = gv + (size_t)cr.pix[c4] * C + (size_t)h * D;
+                                    for (int e = 0; e < D; ++e) {
+                                        const double term = wa * cr.w[c4] * (double)g[h * D + e];
+                                        dst[e] += term;
+                                        if (sv) sv[(size_t)cr.pix[c4] * C + (size_t)h * D + e] += fabs(term);
+                                    }
+                                    if (tv) tv[(size_t)cr.pix[c4] * H + h] += 1;
+                                }
+                            }
+                            start += (int64_t)p->level_h[l] * p->level_w[l];
+                        }
+                    }
+                }
+        }
+        free(attn); free(uv); free(hit);
+    }
     return 0;
 }

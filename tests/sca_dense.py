@@ -92,3 +92,46 @@ def robust_queries(lidar2img, z, X, Y, x_min, dx, y_min, dy, img_hw, eps=1e-5, m
         r = ref[..., k]
         near |= (depth > eps) & ((r.abs() < margin) | ((r - 1.0).abs() < margin))
     return ~(near.any(dim=-1).any(dim=1)).numpy()                   # [B, Q]
+
+
+def dense_sca_grads(value, lidar2img, z, offsets, logits, grad_out, levels, heads, img_hw, X, Y,
+                    x_min, dx, y_min, dy, eps=1e-5, reduce="mean"):
+    """Gradients of the dense path (torch autograd through grid_sample and
+    softmax, float64) with respect to value, offsets and logits, for output
+    gradient ``grad_out``; also the float64 sampling locations in level
+    pixels [B, N, Q, heads, L, P, 2] and the hit mask [B, N, Q]."""
+    v = torch.from_numpy(np.asarray(value, dtype=np.float64)).requires_grad_(True)
+    off = torch.from_numpy(np.asarray(offsets, dtype=np.float64)).requires_grad_(True)
+    lg = torch.from_numpy(np.asarray(logits, dtype=np.float64)).requires_grad_(True)
+    g = torch.from_numpy(np.asarray(grad_out, dtype=np.float64))
+    B, N, S, C = v.shape
+    D = C // heads
+    L = len(levels)
+    P = lg.shape[-1]
+    Z = len(z)
+    Q = X * Y
+    ref, valid, _ = anchors_in_cameras(lidar2img, z, X, Y, x_min, dx, y_min, dy, img_hw, eps)
+    hit = valid.any(dim=-1)
+    count = hit.sum(dim=1).clamp(min=1).to(torch.float64)
+    norm = torch.tensor([[w, h] for h, w in levels], dtype=torch.float64)
+    off_n = off.view(B, 1, Q, heads, L, P // Z, Z, 2) / norm.view(1, 1, 1, 1, L, 1, 1, 2)
+    loc = (ref.view(B, N, Q, 1, 1, 1, Z, 2) + off_n).reshape(B, N, Q, heads, L, P, 2)
+    attn = torch.softmax(lg.view(B, Q, heads, L * P), dim=-1).view(B, Q, heads, L, P)
+    out = torch.zeros(B, Q, C, dtype=torch.float64)
+    start = 0
+    for l, (hl, wl) in enumerate(levels):
+        for n in range(N):
+            vl = v[:, n, start:start + hl * wl, :].reshape(B, hl, wl, heads, D)
+            vl = vl.permute(0, 3, 4, 1, 2).reshape(B * heads, D, hl, wl)
+            grid = (2.0 * loc[:, n, :, :, l] - 1.0).permute(0, 2, 1, 3, 4).reshape(B * heads, Q, P, 2)
+            samp = F.grid_sample(vl, grid, mode="bilinear", padding_mode="zeros",
+                                 align_corners=False)
+            w = attn[:, :, :, l, :].permute(0, 2, 1, 3).reshape(B * heads, 1, Q, P)
+            contrib = (samp * w).sum(dim=-1).view(B, heads, D, Q).permute(0, 3, 1, 2)
+            out = out + contrib.reshape(B, Q, C) * hit[:, n, :, None]
+        start += hl * wl
+    if reduce == "mean":
+        out = out / count[..., None]
+    (out * g).sum().backward()
+    pix = loc.detach() * norm.view(1, 1, 1, 1, L, 1, 2) - 0.5
+    return (v.grad.numpy(), off.grad.numpy(), lg.grad.numpy(), pix.numpy(), hit.numpy())
