@@ -2,7 +2,8 @@
  * flashsca.h -- C ABI of FlashSCA for AMD MI355X (gfx950): BEVFormer's
  * spatial cross-attention (SCA) with the per-camera sampling points formed on
  * the fly (FlashBEV paper, Sec. 4.5, "Cross-framework applicability",
- * Table 7).
+ * Table 7), forward and backward (the paper states that FlashSCA reproduces
+ * the dense path's output and gradient).
  *
  * The operation.  Every BEV query q (cell (i, j) of the grid, q = i Y + j)
  * owns a pillar of Z anchors (x_i, y_j, z_k).  Projected into camera n, an
@@ -88,7 +89,7 @@ typedef struct {
  *   P          sampling points per (head, level), a multiple of Z;
  *              L * P <= FLASHSCA_LPMAX.
  *   offsets    device, [B, X Y, heads, L, P, 2] float32 (x, y) in pixels of
- *              the point's level, 4-byte aligned.
+ *              the point's level, 8-byte aligned (read as pairs).
  *   logits     device, [B, X Y, heads, L, P] float32 attention logits,
  *              4-byte aligned.
  *   out        device, [B, X Y, C] float32, 4-byte aligned, must not overlap
@@ -106,6 +107,50 @@ int flashsca_forward(const flashsca_value *value, const float *lidar2img,
                      void *stream);
 
 /*
+ * FlashSCA backward: gradients of a loss with respect to the forward's
+ * learned inputs, given G = grad_out = dL/d out [B, X Y, C] float32.  With
+ * alpha = 1 / max(1, hits) (1 in sum mode), every forward term
+ * alpha a w value[b, n, tap, c] of a point (head m, level l, point k) in a
+ * hit camera n gives
+ *
+ *   grad_value[b, n, tap, c]   += alpha a w G[b, q, c]
+ *   d a                        += alpha w value[b, n, tap, c] G[b, q, c]
+ *   grad_offsets[b, q, m, l, k] += alpha a (dw/dx, dw/dy) value[..] G[..]
+ *
+ * summed over taps, channels of head m and hit cameras; w is the bilinear
+ * weight of the tap, whose derivative is taken on the cell the forward's
+ * float32 location falls in (a location moves one pixel per pixel of
+ * offset).  grad_logits is the softmax backward over the head's L * P pairs,
+ * a_j (d a_j - sum_j' a_j' d a_j').  The camera matrices and anchors get no
+ * gradient.  Projection, hits, taps and weights are the forward's, computed
+ * the same way.
+ *
+ *   value, lidar2img, spec, anchors, P, offsets, logits: as in
+ *                  flashsca_forward (the value maps are read).
+ *   grad_out       device, [B, X Y, C] float32, 4-byte aligned.
+ *   grad_value     device, [B, N, S, C] float32 (whatever the value dtype),
+ *                  4-byte aligned, or NULL to skip it.  Fully overwritten (a
+ *                  fill kernel zeroes it first, on the same stream); the sum
+ *                  over terms uses float32 atomic adds, so its rounding order
+ *                  (not its terms) varies from run to run.
+ *   grad_offsets   device, [B, X Y, heads, L, P, 2] float32, 8-byte aligned,
+ *                  or NULL.  Every element written once (zero for queries no
+ *                  camera sees).
+ *   grad_logits    device, [B, X Y, heads, L, P] float32, 4-byte aligned, or
+ *                  NULL.  Every element written once.
+ *   stream         hipStream_t; NULL means the default stream.
+ *
+ * At least one gradient must be requested; outputs must not overlap the
+ * inputs or each other.  Limits and status codes: those of
+ * flashsca_forward.  Returns FLASHBEV_OK once enqueued.
+ */
+int flashsca_backward(const flashsca_value *value, const float *lidar2img,
+                      const flashbev_bev_grid_spec *spec, const flashbev_z_bins *anchors,
+                      int32_t P, const float *offsets, const float *logits,
+                      const float *grad_out, float *grad_value, float *grad_offsets,
+                      float *grad_logits, void *stream);
+
+/*
  * Launch geometry of flashsca_forward for these arguments: workgroups,
  * threads per workgroup, dynamic LDS bytes per workgroup, lanes per
  * (query, head) and bytes each lane loads per tap.  Same checks as the
@@ -115,6 +160,15 @@ int flashsca_launch_info(const flashsca_value *value, const flashbev_bev_grid_sp
                          const flashbev_z_bins *anchors, int32_t P, int64_t *workgroups,
                          int32_t *threads_per_workgroup, int32_t *lds_bytes,
                          int32_t *lanes_per_head, int32_t *lane_bytes);
+
+/* Launch geometry of flashsca_backward (the scatter kernel; the fill kernel
+ * is not counted), with the same outputs and checks as flashsca_launch_info. */
+int flashsca_backward_launch_info(const flashsca_value *value,
+                                  const flashbev_bev_grid_spec *spec,
+                                  const flashbev_z_bins *anchors, int32_t P,
+                                  int64_t *workgroups, int32_t *threads_per_workgroup,
+                                  int32_t *lds_bytes, int32_t *lanes_per_head,
+                                  int32_t *lane_bytes);
 
 #ifdef __cplusplus
 }

@@ -16,6 +16,7 @@ from typing import Optional, Sequence, Tuple
 __all__ = [
     "BevGrid", "sample_vt", "sample_vt_backward", "prepare_sample_vt", "prepare_sample_vt_backward",
     "sca_forward", "sca_forward_raw", "sca_launch_info", "prepare_sca_forward",
+    "sca_backward", "sca_backward_launch_info", "prepare_sca_backward",
     "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
 ]
@@ -129,6 +130,11 @@ def _lib():
                                            P(ctypes.c_int32), P(ctypes.c_int32),
                                            P(ctypes.c_int32)]
         L.flashsca_launch_info.restype = ctypes.c_int
+        L.flashsca_backward.argtypes = [P(ScaValue), ctypes.c_void_p, P(GridSpec), P(ZBins),
+                                        ctypes.c_int32] + [ctypes.c_void_p] * 7
+        L.flashsca_backward.restype = ctypes.c_int
+        L.flashsca_backward_launch_info.argtypes = L.flashsca_launch_info.argtypes
+        L.flashsca_backward_launch_info.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -507,8 +513,10 @@ def sca_forward_raw(value_ptr: int, dtype: str, shape, heads: int, levels, lidar
 
 
 def sca_launch_info(shape, dtype: str, heads: int, levels, anchors, grid: BevGrid, img_hw,
-                    P: int, reduce: str = "mean", data_ptr: int = 0) -> dict:
-    """Launch geometry of the FlashSCA forward for these arguments (no HIP call)."""
+                    P: int, reduce: str = "mean", data_ptr: int = 0,
+                    backward: bool = False) -> dict:
+    """Launch geometry of the FlashSCA forward (or backward) for these
+    arguments (no HIP call)."""
     z = _z_array(anchors)
     v, g, zb = _sca_structs(shape, DTYPE_CODES[dtype], data_ptr, heads, levels, img_hw, grid, z,
                             reduce)
@@ -517,11 +525,12 @@ def sca_launch_info(shape, dtype: str, heads: int, levels, anchors, grid: BevGri
     lds = ctypes.c_int32()
     lph = ctypes.c_int32()
     lw = ctypes.c_int32()
-    rc = _lib().flashsca_launch_info(ctypes.byref(v), ctypes.byref(g), ctypes.byref(zb), int(P),
-                                     ctypes.byref(wg), ctypes.byref(thr), ctypes.byref(lds),
-                                     ctypes.byref(lph), ctypes.byref(lw))
+    fn = _lib().flashsca_backward_launch_info if backward else _lib().flashsca_launch_info
+    rc = fn(ctypes.byref(v), ctypes.byref(g), ctypes.byref(zb), int(P), ctypes.byref(wg),
+            ctypes.byref(thr), ctypes.byref(lds), ctypes.byref(lph), ctypes.byref(lw))
     if rc != 0:
-        raise FlashBevError(rc, "flashsca_launch_info")
+        raise FlashBevError(rc, "flashsca_backward_launch_info" if backward
+                            else "flashsca_launch_info")
     return {"workgroups": wg.value, "threads": thr.value, "lds_bytes": lds.value,
             "lanes_per_head": lph.value, "lane_bytes": lw.value}
 
@@ -546,3 +555,79 @@ def prepare_sca_forward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels
             ctypes.c_void_p(s))
     return _Prepared(_lib().flashsca_forward, args,
                      (value, lidar2img, offsets, logits, out, z, v, g, zb), "flashsca_forward")
+
+
+def _sca_bwd_outputs(value, Q, heads, L, P, grad_value, grad_offsets, grad_logits, want):
+    import torch
+
+    B, N, S, C = value.shape
+    dev = value.device
+    shapes = {"value": (B, N, S, C), "offsets": (B, Q, heads, L, P, 2),
+              "logits": (B, Q, heads, L, P)}
+    given = {"value": grad_value, "offsets": grad_offsets, "logits": grad_logits}
+    out = {}
+    for k in ("value", "offsets", "logits"):
+        t = given[k]
+        if t is None and k in want:
+            t = torch.empty(shapes[k], dtype=torch.float32, device=dev)
+        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous() or not t.is_cuda
+                              or tuple(t.shape) != shapes[k]):
+            raise ValueError(f"grad_{k} must be a contiguous float32 device tensor {shapes[k]}")
+        out[k] = t
+    return out
+
+
+def sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels, heads: int, offsets,
+                 logits, grad_out, grad_value=None, grad_offsets=None, grad_logits=None,
+                 want=("value", "offsets", "logits"), reduce: str = "mean", stream=None):
+    """FlashSCA backward on the GPU: gradients with respect to the value maps,
+    the offsets and the logits for ``grad_out`` [B, X*Y, C] float32.
+
+    Returns a dict with the float32 tensors ``value`` [B, N, S, C],
+    ``offsets`` [B, X*Y, heads, L, P, 2] and ``logits`` [B, X*Y, heads, L, P]
+    (None for gradients not in ``want`` and not passed in).  Asynchronous.
+    """
+    import torch
+
+    B, N, S, C, Q, P = _sca_check(value, lidar2img, offsets, logits, levels, heads, grid)
+    if not grad_out.is_cuda or grad_out.dtype != torch.float32 or not grad_out.is_contiguous() \
+            or tuple(grad_out.shape) != (B, Q, C):
+        raise ValueError(f"grad_out must be a contiguous float32 device tensor [{B}, {Q}, {C}]")
+    outs = _sca_bwd_outputs(value, Q, heads, len(levels), P, grad_value, grad_offsets,
+                            grad_logits, want)
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
+                            img_hw, grid, z, reduce)
+    s = _stream_handle(stream, value.device)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    rc = _lib().flashsca_backward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
+                                  ctypes.byref(g), ctypes.byref(zb), P,
+                                  ctypes.c_void_p(offsets.data_ptr()),
+                                  ctypes.c_void_p(logits.data_ptr()),
+                                  ctypes.c_void_p(grad_out.data_ptr()), ptr(outs["value"]),
+                                  ptr(outs["offsets"]), ptr(outs["logits"]), ctypes.c_void_p(s))
+    if rc != 0:
+        raise FlashBevError(rc, "flashsca_backward")
+    return outs
+
+
+def prepare_sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels, heads: int,
+                         offsets, logits, grad_out, grad_value, grad_offsets, grad_logits,
+                         reduce: str = "mean", stream=None) -> _Prepared:
+    """``sca_backward`` with every argument fixed (outputs given; any may be
+    None): a callable that enqueues the same call again."""
+    B, N, S, C, Q, P = _sca_check(value, lidar2img, offsets, logits, levels, heads, grid)
+    outs = _sca_bwd_outputs(value, Q, heads, len(levels), P, grad_value, grad_offsets,
+                            grad_logits, ())
+    z = _z_array(anchors)
+    v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
+                            img_hw, grid, z, reduce)
+    s = _stream_handle(stream, value.device)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    args = (ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_int32(P), ctypes.c_void_p(offsets.data_ptr()),
+            ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(grad_out.data_ptr()),
+            ptr(outs["value"]), ptr(outs["offsets"]), ptr(outs["logits"]), ctypes.c_void_p(s))
+    return _Prepared(_lib().flashsca_backward, args,
+                     (value, lidar2img, offsets, logits, grad_out, outs, z, v, g, zb),
+                     "flashsca_backward")

@@ -1,6 +1,7 @@
-// FlashSCA forward for gfx950: BEVFormer's spatial cross-attention with the
+// FlashSCA for gfx950: BEVFormer's spatial cross-attention with the
 // per-camera sampling points formed on the fly (FlashBEV paper, Sec. 4.5,
-// Table 7), behind the C ABI declared in include/flashsca.h.
+// Table 7), forward and backward, behind the C ABI declared in
+// include/flashsca.h.
 //
 // Execution design (MI355X-first):
 //   * Work items are (query, head) pairs, "slots".  A slot owns `lph` lanes
@@ -8,23 +9,29 @@
 //     head's D channels, so every bilinear tap of the head is one coalesced
 //     run of D * elem bytes across the slot's lanes.  A wavefront holds
 //     64 / lph slots; a workgroup a tile of consecutive pairs of one batch
-//     element.
+//     element, in a blocked visiting order of the queries (query_of).
 //   * Phase 1 (workgroup): every (query, camera) pair of the tile projects the
 //     query's Z anchors (float32 recipe, IEEE divisions), records the
 //     normalized reference points in LDS and sets the camera's bit in the
 //     query's hit mask (LDS atomic OR).
 //   * Phase 2 (slot): softmax over the head's L * P logits, read once per
-//     query (not once per camera); the attention weights, already multiplied
-//     by 1 / max(1, hits), go to the slot's LDS area.
+//     query (not once per camera), kept in the slot's LDS area.
 //   * Phase 3 (slot, per hit camera): in chunks of lph points, lane `sub`
 //     sets up point c + sub (anchor k mod Z, location (u W_l + dx) - 1/2,
-//     floor, four tap offsets and weights a * w) and publishes them in LDS;
-//     then all lanes of the slot gather the chunk's lph * 4 taps with raw
-//     buffer loads and accumulate their channels in float32.  A tap outside
-//     the map gets an offset past the end of the camera's buffer, so its load
-//     returns zero without a memory access.
-//   * Each output element is written once; no atomics on global memory, no
-//     workspace, one launch.
+//     floor, four tap offsets and bilinear weights) and publishes it in LDS;
+//     then all lanes of the slot load the chunk's lph * 4 taps with raw buffer
+//     loads.  A tap outside the map gets an offset past the end of the
+//     camera's buffer, so its load returns zero without a memory access.
+//       - forward: each lane accumulates its channels in float32;
+//       - backward: each lane forms its channels' share of the tap rows'
+//         dot products with the output gradient; a reduction across the slot
+//         gives the point's gradients of attention weight and location, kept
+//         by the lane that owns the point; the value gradient is scattered
+//         with float atomic adds.
+//   * Forward: each output element is written once, no atomics on global
+//     memory, no workspace, one launch.  Backward: a fill kernel zeroes the
+//     value gradient, then one launch; offset and logit gradients are
+//     written once each.
 // Coordinates follow the float32 recipe of the conventions in flashsca.h, so
 // mask and floor decisions match the CPU oracle bit for bit: the file is
 // compiled with -ffp-contract=off and uses IEEE division.
@@ -51,10 +58,14 @@ constexpr int kScaBlock = 32;    // queries are visited in blocks of 32 x 32 BEV
 // and returns zero without touching memory.
 constexpr uint32_t kScaNoTap = 0x80000000u;
 constexpr uint64_t kScaCamBytesMax = 0x7FFFFFFFull;
-constexpr uint32_t kScaLdsBudget = 64u * 1024u;
-// a chunk record: 4 tap offsets then 4 weights (8 dwords) per lane, and a
-// 4-dword pad per slot so that the slots' broadcast reads hit different banks
-constexpr int kTapDwords = 8;
+constexpr uint32_t kScaLdsBudget = 64u * 1024u;    // preferred dynamic LDS per workgroup
+constexpr uint32_t kScaLdsMax = 160u * 1024u;      // gfx950's LDS per workgroup
+// A chunk record per lane: 4 tap offsets and 4 weights (forward); the
+// backward adds the location's fractions and the point's attention weight
+// (12 dwords).  A 4-dword pad per slot puts the slots' broadcast reads in
+// different banks.
+constexpr int kRecFwd = 8;
+constexpr int kRecBwd = 12;
 constexpr int kSlotPad = 4;
 
 struct ScaParams {
@@ -62,43 +73,49 @@ struct ScaParams {
     const float *l2i;
     const float *offsets;
     const float *logits;
-    float *out;
-    uint64_t cam_bytes;     // bytes of one camera's value maps (S C elem)
-    uint32_t row_bytes;     // C * elem
-    uint32_t head_bytes;    // D * elem
+    float *out;              // forward output
+    const float *grad_out;   // backward: dL/d out
+    float *grad_value;       // backward outputs (each may be null)
+    float *grad_offsets;
+    float *grad_logits;
+    uint64_t cam_bytes;      // bytes of one camera's value maps (S C elem)
+    uint64_t cam_elems;      // S C
+    uint32_t row_bytes;      // C * elem
+    uint32_t head_bytes;     // D * elem
     int32_t B, N, C, heads, D, L, P, Z, LP;
     int32_t X, Y, Q;
-    int32_t lph;            // lanes per slot (power of two)
-    int32_t lph_shift;      // log2(lph)
-    int32_t spw;            // slots per wavefront
-    int32_t tile_pairs;     // (query, head) pairs per workgroup
+    int32_t lph;             // lanes per slot (power of two)
+    int32_t lph_shift;       // log2(lph)
+    int32_t spw;             // slots per wavefront
+    int32_t tile_pairs;      // (query, head) pairs per workgroup
     int32_t tiles_per_b;
-    int32_t stripe;         // consecutive tiles an XCD takes in turn (about one block)
-    int32_t nq_max;         // queries a tile can touch
-    int32_t slot_stride;    // dwords per slot in the chunk-record area
+    int32_t stripe;          // consecutive tiles an XCD takes in turn (about one block)
+    int32_t nq_max;          // queries a tile can touch
+    int32_t slot_stride;     // dwords per slot in the chunk-record area
     float img_w, img_h;
     float x_min, dx, y_min, dy, depth_eps;
     int32_t reduce;
-    float rcp_p, rcp_z;     // float32 1 / P and 1 / Z for div_small
+    float rcp_p, rcp_z;      // float32 1 / P and 1 / Z for div_small
     float level_wf[FLASHSCA_LMAX], level_hf[FLASHSCA_LMAX];
     int32_t level_w[FLASHSCA_LMAX], level_h[FLASHSCA_LMAX];
     uint32_t level_start[FLASHSCA_LMAX];   // first pixel of each level
     // LDS layout (byte offsets)
-    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_tap;
+    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_acc, lds_tap;
     float z[FLASHSCA_ZMAX];
 };
 
 // LDS: camera matrices [N][12]; level table [5][LMAX]; anchors [Z];
 // reference points [nq_max][N][Z] float2; hit masks [nq_max]; attention
-// weights [waves][spw][LP]; chunk records [waves][spw][slot_stride].
+// weights [waves][spw][LP]; backward only: point gradients
+// [waves][spw][3][LP]; chunk records [waves][spw][slot_stride].
 struct ScaLds {
-    uint32_t mat, lvl, z, ref, hit, att, tap, total;
+    uint32_t mat, lvl, z, ref, hit, att, acc, tap, total;
 };
 
 __host__ inline uint32_t sca_align16(uint32_t v) { return (v + 15u) & ~15u; }
 
 __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int LP,
-                               int slot_stride)
+                               int slot_stride, bool backward)
 {
     ScaLds s;
     uint32_t o = 0;
@@ -108,6 +125,7 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
     s.ref = o; o = sca_align16(o + (uint32_t)nq_max * N * Z * 8u);
     s.hit = o; o = sca_align16(o + (uint32_t)nq_max * 4u);
     s.att = o; o = sca_align16(o + (uint32_t)waves * spw * LP * 4u);
+    s.acc = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * LP * 12u : 0u));
     s.tap = o; o = sca_align16(o + (uint32_t)waves * spw * slot_stride * 4u);
     s.total = o;
     return s;
@@ -132,39 +150,42 @@ __device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
     j = c * kScaBlock + (t - ti * w);
 }
 
-template <int DT, int LW>
-__global__ void __launch_bounds__(kScaThreads)
-sca_fwd(const ScaParams p)
+// LDS views of one workgroup.
+struct ScaSmem {
+    float *mat, *lwf, *lhf, *z, *att, *acc;
+    int32_t *lw, *lh;
+    uint32_t *lst, *hit, *tap;
+    float2 *ref;
+};
+
+__device__ __forceinline__ ScaSmem sca_smem(const ScaParams &p, unsigned char *smem)
 {
-    constexpr int ES = ElemSize<DT>::value;
-    constexpr int EPV = LW / ES;   // elements per lane slice
-    extern __shared__ __align__(16) unsigned char smem[];
-    float *s_mat = reinterpret_cast<float *>(smem + p.lds_mat);
-    float *s_lwf = reinterpret_cast<float *>(smem + p.lds_lvl);
-    float *s_lhf = s_lwf + FLASHSCA_LMAX;
-    int32_t *s_lw = reinterpret_cast<int32_t *>(s_lhf + FLASHSCA_LMAX);
-    int32_t *s_lh = s_lw + FLASHSCA_LMAX;
-    uint32_t *s_lst = reinterpret_cast<uint32_t *>(s_lh + FLASHSCA_LMAX);
-    float *s_z = reinterpret_cast<float *>(smem + p.lds_z);
-    float2 *s_ref = reinterpret_cast<float2 *>(smem + p.lds_ref);
-    uint32_t *s_hit = reinterpret_cast<uint32_t *>(smem + p.lds_hit);
-    float *s_att = reinterpret_cast<float *>(smem + p.lds_att);
-    uint32_t *s_tap = reinterpret_cast<uint32_t *>(smem + p.lds_tap);
+    ScaSmem m;
+    m.mat = reinterpret_cast<float *>(smem + p.lds_mat);
+    m.lwf = reinterpret_cast<float *>(smem + p.lds_lvl);
+    m.lhf = m.lwf + FLASHSCA_LMAX;
+    m.lw = reinterpret_cast<int32_t *>(m.lhf + FLASHSCA_LMAX);
+    m.lh = m.lw + FLASHSCA_LMAX;
+    m.lst = reinterpret_cast<uint32_t *>(m.lh + FLASHSCA_LMAX);
+    m.z = reinterpret_cast<float *>(smem + p.lds_z);
+    m.ref = reinterpret_cast<float2 *>(smem + p.lds_ref);
+    m.hit = reinterpret_cast<uint32_t *>(smem + p.lds_hit);
+    m.att = reinterpret_cast<float *>(smem + p.lds_att);
+    m.acc = reinterpret_cast<float *>(smem + p.lds_acc);
+    m.tap = reinterpret_cast<uint32_t *>(smem + p.lds_tap);
+    return m;
+}
 
-    const int tid = threadIdx.x;
-    const int nthreads = blockDim.x;
-    const int wave = tid / kScaWave;
-    const int lane = tid % kScaWave;
-    const int N = p.N, Z = p.Z;
-
-    // XCD-aware tile order.  Queries are visited block by block (see
-    // query_of), so consecutive tiles cover a compact patch of the BEV whose
-    // samples land on overlapping pixels.  The k-th workgroup on XCD x takes
-    // tile (k / S) * 8S + x * S + k % S with S = p.stripe (about one block):
-    // an XCD works through whole blocks, its resident workgroups share their
-    // pixels in its L2, and the blocks of the 8 XCDs interleave over the
-    // grid (a like mix of heavy and light regions).  The tail that does not
-    // fill 8 stripes is split the same way with shorter stripes.
+// XCD-aware tile order.  Queries are visited block by block (query_of), so
+// consecutive tiles cover a compact patch of the BEV whose samples land on
+// overlapping pixels.  The k-th workgroup on XCD x takes tile
+// (k / S) * 8S + x * S + k % S with S = p.stripe (about one block): an XCD
+// works through whole blocks, its resident workgroups share their pixels in
+// its L2, and the blocks of the 8 XCDs interleave over the grid (a like mix
+// of heavy and light regions).  The tail that does not fill 8 stripes is
+// split the same way with shorter stripes.
+__device__ __forceinline__ int sca_tile(const ScaParams &p)
+{
     const int g = blockIdx.x;
     const int S8 = kScaXcds * p.stripe;
     const int full = (int)(gridDim.x / S8) * S8;
@@ -180,27 +201,32 @@ sca_fwd(const ScaParams p)
             tile = full + xcd * s2 + k;
         }
     }
-    const int b = tile / p.tiles_per_b;
-    const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
-    const int r_first = (int)(pair0 / p.heads);   // first query rank of the tile
-    const int64_t pairs_b = (int64_t)p.Q * p.heads;
+    return tile;
+}
 
+// Stage matrices, level table and anchors; phase 1: reference points and
+// hit masks of the tile's queries.  Ends with a workgroup barrier.
+__device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSmem &m, int b,
+                                                 int r_first)
+{
+    const int tid = threadIdx.x;
+    const int nthreads = blockDim.x;
+    const int N = p.N, Z = p.Z;
     for (int t = tid; t < N * 12; t += nthreads) {
         const int n = t / 12, r = t - n * 12;
-        s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
+        m.mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
     }
     if (tid < FLASHSCA_LMAX) {
-        s_lwf[tid] = p.level_wf[tid];
-        s_lhf[tid] = p.level_hf[tid];
-        s_lw[tid] = p.level_w[tid];
-        s_lh[tid] = p.level_h[tid];
-        s_lst[tid] = p.level_start[tid];
+        m.lwf[tid] = p.level_wf[tid];
+        m.lhf[tid] = p.level_hf[tid];
+        m.lw[tid] = p.level_w[tid];
+        m.lh[tid] = p.level_h[tid];
+        m.lst[tid] = p.level_start[tid];
     }
-    for (int t = tid; t < Z; t += nthreads) s_z[t] = p.z[t];
-    for (int t = tid; t < p.nq_max; t += nthreads) s_hit[t] = 0u;
+    for (int t = tid; t < Z; t += nthreads) m.z[t] = p.z[t];
+    for (int t = tid; t < p.nq_max; t += nthreads) m.hit[t] = 0u;
     __syncthreads();
 
-    // ---- phase 1: reference points of the tile's queries in every camera
     for (int t = tid; t < p.nq_max * N; t += nthreads) {
         const int qi = t / N, n = t - qi * N;
         const int rank = r_first + qi;
@@ -209,138 +235,216 @@ sca_fwd(const ScaParams p)
         query_of(rank, p.X, p.Y, i, j);
         const float x = p.x_min + ((float)i + 0.5f) * p.dx;
         const float y = p.y_min + ((float)j + 0.5f) * p.dy;
-        const float *m = s_mat + n * 12;
+        const float *mr = m.mat + n * 12;
         bool any = false;
         for (int k = 0; k < Z; ++k) {
-            const float z = s_z[k];
+            const float z = m.z[k];
             // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
-            const float up = ((m[0] * x + m[1] * y) + m[2] * z) + m[3];
-            const float vp = ((m[4] * x + m[5] * y) + m[6] * z) + m[7];
-            const float d = ((m[8] * x + m[9] * y) + m[10] * z) + m[11];
+            const float up = ((mr[0] * x + mr[1] * y) + mr[2] * z) + mr[3];
+            const float vp = ((mr[4] * x + mr[5] * y) + mr[6] * z) + mr[7];
+            const float d = ((mr[8] * x + mr[9] * y) + mr[10] * z) + mr[11];
             const bool in_front = d > p.depth_eps;
             const float dd = in_front ? d : p.depth_eps;
             const float un = (up / dd) / p.img_w;
             const float vn = (vp / dd) / p.img_h;
-            s_ref[(qi * N + n) * Z + k] = make_float2(un, vn);
+            m.ref[(qi * N + n) * Z + k] = make_float2(un, vn);
             any |= in_front && un > 0.0f && un < 1.0f && vn > 0.0f && vn < 1.0f;
         }
-        if (any) atomicOr(&s_hit[qi], 1u << n);
+        if (any) atomicOr(&m.hit[qi], 1u << n);
     }
     __syncthreads();
+}
 
-    // ---- phase 2: the slot's softmax over (level, point)
-    const int lph = p.lph;
-    const int sub = lane & (lph - 1);
-    const int slot = lane >> p.lph_shift;
-    const int64_t pair = pair0 + (int64_t)wave * p.spw + slot;
-    const bool active = pair < pairs_b;
-    const int rank = active ? (int)(pair / p.heads) : r_first;
-    const int mh = active ? (int)(pair - (int64_t)rank * p.heads) : 0;
-    const int qi = rank - r_first;
+// One (query, head) slot of a wavefront.
+struct ScaSlot {
+    int sub, slot;        // lane within the slot, slot within the wavefront
+    bool active;          // the slot holds a (query, head) pair
+    int qi;               // query index within the tile
+    int q;                // the query's index in offsets, logits and the outputs
+    int mh;               // head
+    uint32_t hits;        // hit cameras (0 for inactive slots)
+    float inv;            // 1 / max(1, hits) (1 in sum mode)
+    size_t pt0;           // first (level, point) element of the pair
+};
+
+__device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m, int b,
+                                            int64_t pair0, int r_first, int wave, int lane)
+{
+    ScaSlot s;
+    s.sub = lane & (p.lph - 1);
+    s.slot = lane >> p.lph_shift;
+    const int64_t pair = pair0 + (int64_t)wave * p.spw + s.slot;
+    s.active = pair < (int64_t)p.Q * p.heads;
+    const int rank = s.active ? (int)(pair / p.heads) : r_first;
+    s.mh = s.active ? (int)(pair - (int64_t)rank * p.heads) : 0;
+    s.qi = rank - r_first;
     int qx, qy;
     query_of(rank, p.X, p.Y, qx, qy);
-    const int q = qx * p.Y + qy;             // the query's index in offsets, logits, out
-    const uint32_t hits = active ? s_hit[qi] : 0u;
-    const int count = __popc(hits);
-    const float inv = (p.reduce == FLASHBEV_REDUCE_VALID_MEAN && count > 1) ? 1.0f / (float)count
-                                                                             : 1.0f;
-    const int LP = p.LP;
-    float *att = s_att + (size_t)(wave * p.spw + slot) * LP;
-    const size_t pt0 = (((size_t)b * p.Q + q) * p.heads + mh) * (size_t)LP;
-    if (hits) {
-        float mx = -INFINITY;
-        for (int j = sub; j < LP; j += lph) mx = fmaxf(mx, p.logits[pt0 + j]);
-        for (int s = lph >> 1; s >= 1; s >>= 1) mx = fmaxf(mx, __shfl_xor(mx, s));
-        float sum = 0.0f;
-        for (int j = sub; j < LP; j += lph) {
-            const float e = expf(p.logits[pt0 + j] - mx);
-            att[j] = e;
-            sum += e;
-        }
-        for (int s = lph >> 1; s >= 1; s >>= 1) sum += __shfl_xor(sum, s);
-        const float r = inv / sum;
-        for (int j = sub; j < LP; j += lph) att[j] *= r;
-    }   // the shuffles stay inside the slot, whose lanes all take this branch or none
+    s.q = qx * p.Y + qy;
+    s.hits = s.active ? m.hit[s.qi] : 0u;
+    const int count = __popc(s.hits);
+    s.inv = (p.reduce == FLASHBEV_REDUCE_VALID_MEAN && count > 1) ? 1.0f / (float)count : 1.0f;
+    s.pt0 = (((size_t)b * p.Q + s.q) * p.heads + s.mh) * (size_t)p.LP;
+    return s;
+}
 
-    // cameras any slot of the wavefront hits (wavefront-uniform)
+// Phase 2: att[j] = post * softmax over the slot's L*P logits (only for
+// slots with a hit camera).  The shuffles stay inside the slot, whose lanes
+// all take the branch or none.
+__device__ __forceinline__ void sca_softmax(const ScaParams &p, const ScaSlot &s, float *att,
+                                            float post)
+{
+    if (!s.hits) return;
+    const int lph = p.lph, LP = p.LP;
+    float mx = -INFINITY;
+    for (int j = s.sub; j < LP; j += lph) mx = fmaxf(mx, p.logits[s.pt0 + j]);
+    for (int o = lph >> 1; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    float sum = 0.0f;
+    for (int j = s.sub; j < LP; j += lph) {
+        const float e = expf(p.logits[s.pt0 + j] - mx);
+        att[j] = e;
+        sum += e;
+    }
+    for (int o = lph >> 1; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    const float r = post / sum;
+    for (int j = s.sub; j < LP; j += lph) att[j] *= r;
+}
+
+// Set-up of point j of a slot in one camera: tap byte offsets (kScaNoTap
+// outside the map) and the location's fractions.  Returns false when no
+// corner lies inside the map (all taps kScaNoTap).
+__device__ __forceinline__ bool sca_setup_point(const ScaParams &p, const ScaSmem &m,
+                                                const float2 *ref, const ScaSlot &s, int j,
+                                                uint32_t head_off, uint4 &o, float &ax,
+                                                float &ay)
+{
+    o = make_uint4(kScaNoTap, kScaNoTap, kScaNoTap, kScaNoTap);
+    ax = 0.0f;
+    ay = 0.0f;
+    const int l = div_small(j, p.P, p.rcp_p);
+    const int k = j - l * p.P;
+    const int zk = k - div_small(k, p.Z, p.rcp_z) * p.Z;   // anchor k mod Z
+    const float2 r = ref[zk];
+    const float2 dxy = reinterpret_cast<const float2 *>(p.offsets)[s.pt0 + j];
+    const float Wl = m.lwf[l], Hl = m.lhf[l];
+    float sx = r.x * Wl;
+    float sy = r.y * Hl;
+    sx = sx + dxy.x;
+    sy = sy + dxy.y;
+    const float xim = sx - 0.5f;
+    const float yim = sy - 0.5f;
+    if (!(xim > -1.0f && xim < Wl && yim > -1.0f && yim < Hl)) return false;
+    const float x0f = floorf(xim), y0f = floorf(yim);
+    ax = xim - x0f;
+    ay = yim - y0f;
+    const int x0 = (int)x0f, y0 = (int)y0f;
+    const int wi = m.lw[l], hi = m.lh[l];
+    const bool xl = x0 >= 0, xr = x0 + 1 < wi;
+    const bool yt = y0 >= 0, yb = y0 + 1 < hi;
+    const int row = (int)m.lst[l] + y0 * wi + x0;
+    const uint32_t rb = p.row_bytes;
+    if (xl && yt) o.x = (uint32_t)row * rb + head_off;
+    if (xr && yt) o.y = (uint32_t)(row + 1) * rb + head_off;
+    if (xl && yb) o.z = (uint32_t)(row + wi) * rb + head_off;
+    if (xr && yb) o.w = (uint32_t)(row + wi + 1) * rb + head_off;
+    return true;
+}
+
+// bilinear weights of the in-range taps, each times `a`
+__device__ __forceinline__ float4 sca_weights(const uint4 &o, float ax, float ay, float a)
+{
+    const float wt = a * (1.0f - ay), wb = a * ay;
+    return make_float4((o.x != kScaNoTap) ? wt * (1.0f - ax) : 0.0f,
+                       (o.y != kScaNoTap) ? wt * ax : 0.0f,
+                       (o.z != kScaNoTap) ? wb * (1.0f - ax) : 0.0f,
+                       (o.w != kScaNoTap) ? wb * ax : 0.0f);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sca_camera_rsrc(const ScaParams &p, int b, int n)
+{
+    const char *cam_base = static_cast<const char *>(p.value) +
+                           ((size_t)b * p.N + n) * (size_t)p.cam_bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(cam_base), (short)0,
+                                             (int)p.cam_bytes, 0x00020000);
+}
+
+// uniform over the wavefront: the cameras any slot of it hits
+__device__ __forceinline__ uint32_t sca_wave_cameras(const ScaParams &p, uint32_t hits)
+{
     uint32_t cams = 0;
-    for (int n = 0; n < N; ++n)
+    for (int n = 0; n < p.N; ++n)
         if (__ballot((hits >> n) & 1u)) cams |= 1u << n;
+    return cams;
+}
 
-    // ---- phase 3: sampling in every hit camera
+template <int DT, int LW>
+__global__ void __launch_bounds__(kScaThreads)
+sca_fwd(const ScaParams p)
+{
+    constexpr int ES = ElemSize<DT>::value;
+    constexpr int EPV = LW / ES;   // elements per lane slice
+    extern __shared__ __align__(16) unsigned char smem[];
+    const ScaSmem m = sca_smem(p, smem);
+    const int wave = threadIdx.x / kScaWave;
+    const int lane = threadIdx.x % kScaWave;
+
+    const int tile = sca_tile(p);
+    const int b = tile / p.tiles_per_b;
+    const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
+    const int r_first = (int)(pair0 / p.heads);   // first query rank of the tile
+    sca_project_tile(p, m, b, r_first);
+
+    const ScaSlot s = sca_slot(p, m, b, pair0, r_first, wave, lane);
+    const int lph = p.lph, LP = p.LP;
+    float *att = m.att + (size_t)(wave * p.spw + s.slot) * LP;
+    // attention weights with the mean over hit cameras folded in
+    sca_softmax(p, s, att, s.inv);
+    const uint32_t cams = sca_wave_cameras(p, s.hits);
+
     float acc[EPV];
 #pragma unroll
     for (int e = 0; e < EPV; ++e) acc[e] = 0.0f;
-    const uint32_t lane_off = (uint32_t)sub * LW;
-    const uint32_t head_off = (uint32_t)mh * p.head_bytes;
-    uint32_t *rec_w = s_tap + (size_t)(wave * p.spw + slot) * p.slot_stride;   // this slot
-    const float2 *off2 = reinterpret_cast<const float2 *>(p.offsets);
+    const uint32_t lane_off = (uint32_t)s.sub * LW;
+    const uint32_t head_off = (uint32_t)s.mh * p.head_bytes;
+    uint32_t *rec = m.tap + (size_t)(wave * p.spw + s.slot) * p.slot_stride;   // this slot
 
-    for (int n = 0; n < N; ++n) {
+    for (int n = 0; n < p.N; ++n) {
         if (!((cams >> n) & 1u)) continue;
-        const bool mine = (hits >> n) & 1u;
-        const char *cam_base = static_cast<const char *>(p.value) +
-                               ((size_t)b * N + n) * (size_t)p.cam_bytes;
-        const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<char *>(cam_base), (short)0, (int)p.cam_bytes, 0x00020000);
-        const float2 *ref = s_ref + (size_t)(qi * N + n) * Z;
+        const bool mine = (s.hits >> n) & 1u;
+        const __amdgpu_buffer_rsrc_t rsrc = sca_camera_rsrc(p, b, n);
+        const float2 *ref = m.ref + (size_t)(s.qi * p.N + n) * p.Z;
         for (int c0 = 0; c0 < LP; c0 += lph) {
-            // set-up of point j = c0 + sub of this slot
-            const int j = c0 + sub;
-            uint32_t o0 = kScaNoTap, o1 = kScaNoTap, o2 = kScaNoTap, o3 = kScaNoTap;
-            float w0 = 0.0f, w1 = 0.0f, w2 = 0.0f, w3 = 0.0f;
+            // set-up of point j = c0 + sub of this slot, weights a * w
+            const int j = c0 + s.sub;
+            uint4 o = make_uint4(kScaNoTap, kScaNoTap, kScaNoTap, kScaNoTap);
+            float4 w = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             if (mine && j < LP) {
-                const int l = div_small(j, p.P, p.rcp_p);
-                const int k = j - l * p.P;
-                const int zk = k - div_small(k, Z, p.rcp_z) * Z;   // anchor k mod Z
-                const float2 r = ref[zk];
-                const float2 dxy = off2[pt0 + j];
-                const float Wl = s_lwf[l], Hl = s_lhf[l];
-                float sx = r.x * Wl;
-                float sy = r.y * Hl;
-                sx = sx + dxy.x;
-                sy = sy + dxy.y;
-                const float xim = sx - 0.5f;
-                const float yim = sy - 0.5f;
-                if (xim > -1.0f && xim < Wl && yim > -1.0f && yim < Hl) {
-                    const float x0f = floorf(xim), y0f = floorf(yim);
-                    const float ax = xim - x0f, ay = yim - y0f;
-                    const int x0 = (int)x0f, y0 = (int)y0f;
-                    const int wi = s_lw[l], hi = s_lh[l];
-                    const float a = att[j];
-                    const float wt = a * (1.0f - ay), wb = a * ay;
-                    const bool xl = x0 >= 0, xr = x0 + 1 < wi;
-                    const bool yt = y0 >= 0, yb = y0 + 1 < hi;
-                    const int row = (int)s_lst[l] + y0 * wi + x0;
-                    const uint32_t rb = p.row_bytes;
-                    if (xl && yt) { o0 = (uint32_t)row * rb + head_off; w0 = wt * (1.0f - ax); }
-                    if (xr && yt) { o1 = (uint32_t)(row + 1) * rb + head_off; w1 = wt * ax; }
-                    if (xl && yb) { o2 = (uint32_t)(row + wi) * rb + head_off; w2 = wb * (1.0f - ax); }
-                    if (xr && yb) { o3 = (uint32_t)(row + wi + 1) * rb + head_off; w3 = wb * ax; }
-                }
+                float ax, ay;
+                if (sca_setup_point(p, m, ref, s, j, head_off, o, ax, ay))
+                    w = sca_weights(o, ax, ay, att[j]);
             }
-            uint32_t *mine_rec = rec_w + sub * kTapDwords;
-            *reinterpret_cast<uint4 *>(mine_rec) = make_uint4(o0, o1, o2, o3);
-            *reinterpret_cast<float4 *>(mine_rec + 4) = make_float4(w0, w1, w2, w3);
+            uint32_t *mine_rec = rec + s.sub * kRecFwd;
+            *reinterpret_cast<uint4 *>(mine_rec) = o;
+            *reinterpret_cast<float4 *>(mine_rec + 4) = w;
             wave_lds_sync();
             // gather the chunk's points: every lane of the slot, its channels
             const int npts = (LP - c0) < lph ? (LP - c0) : lph;
 #pragma unroll 4
             for (int t = 0; t < npts; ++t) {
-                const uint4 o = *reinterpret_cast<const uint4 *>(rec_w + t * kTapDwords);
-                const float4 w = *reinterpret_cast<const float4 *>(rec_w + t * kTapDwords + 4);
-                const Raw<LW> v0 = load_vec<LW>(rsrc, o.x + lane_off, 0);
-                const Raw<LW> v1 = load_vec<LW>(rsrc, o.y + lane_off, 0);
-                const Raw<LW> v2 = load_vec<LW>(rsrc, o.z + lane_off, 0);
-                const Raw<LW> v3 = load_vec<LW>(rsrc, o.w + lane_off, 0);
+                const uint4 to = *reinterpret_cast<const uint4 *>(rec + t * kRecFwd);
+                const float4 tw = *reinterpret_cast<const float4 *>(rec + t * kRecFwd + 4);
+                const Raw<LW> v0 = load_vec<LW>(rsrc, to.x + lane_off, 0);
+                const Raw<LW> v1 = load_vec<LW>(rsrc, to.y + lane_off, 0);
+                const Raw<LW> v2 = load_vec<LW>(rsrc, to.z + lane_off, 0);
+                const Raw<LW> v3 = load_vec<LW>(rsrc, to.w + lane_off, 0);
 #pragma unroll
                 for (int e = 0; e < EPV; ++e) {
-                    float s = acc[e];
-                    s = fmaf(w.x, elem<DT, LW>(v0, e), s);
-                    s = fmaf(w.y, elem<DT, LW>(v1, e), s);
-                    s = fmaf(w.z, elem<DT, LW>(v2, e), s);
-                    s = fmaf(w.w, elem<DT, LW>(v3, e), s);
-                    acc[e] = s;
+                    float a = acc[e];
+                    a = fmaf(tw.x, elem<DT, LW>(v0, e), a);
+                    a = fmaf(tw.y, elem<DT, LW>(v1, e), a);
+                    a = fmaf(tw.z, elem<DT, LW>(v2, e), a);
+                    a = fmaf(tw.w, elem<DT, LW>(v3, e), a);
+                    acc[e] = a;
                 }
             }
             wave_lds_sync();
@@ -348,36 +452,189 @@ sca_fwd(const ScaParams p)
     }
 
     // ---- store: each lane its slice of the head's channels
-    if (active) {
-        float *o = p.out + ((size_t)b * p.Q + q) * (size_t)p.C + (size_t)mh * p.D;
-        const int e0 = sub * EPV;
+    if (s.active) {
+        float *out = p.out + ((size_t)b * p.Q + s.q) * (size_t)p.C + (size_t)s.mh * p.D;
+        const int e0 = s.sub * EPV;
 #pragma unroll
         for (int e = 0; e < EPV; ++e)
-            if (e0 + e < p.D) o[e0 + e] = acc[e];
+            if (e0 + e < p.D) out[e0 + e] = acc[e];
     }
+}
+
+// Backward: gradients of value (scatter), offsets and logits.
+template <int DT, int LW>
+__global__ void __launch_bounds__(kScaThreads)
+sca_bwd(const ScaParams p)
+{
+    constexpr int ES = ElemSize<DT>::value;
+    constexpr int EPV = LW / ES;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const ScaSmem m = sca_smem(p, smem);
+    const int wave = threadIdx.x / kScaWave;
+    const int lane = threadIdx.x % kScaWave;
+
+    const int tile = sca_tile(p);
+    const int b = tile / p.tiles_per_b;
+    const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
+    const int r_first = (int)(pair0 / p.heads);
+    sca_project_tile(p, m, b, r_first);
+
+    const ScaSlot s = sca_slot(p, m, b, pair0, r_first, wave, lane);
+    const int lph = p.lph, LP = p.LP;
+    const int slot_id = wave * p.spw + s.slot;
+    float *att = m.att + (size_t)slot_id * LP;                 // softmax a_j
+    float *g_da = m.acc + (size_t)slot_id * 3 * LP;            // d a_j (before the mean)
+    float *g_dx = g_da + LP;                                   // d x_j (before the mean and a_j)
+    float *g_dy = g_dx + LP;
+    sca_softmax(p, s, att, 1.0f);
+    for (int j = s.sub; j < LP; j += lph) {
+        g_da[j] = 0.0f;
+        g_dx[j] = 0.0f;
+        g_dy[j] = 0.0f;
+    }
+    const uint32_t cams = sca_wave_cameras(p, s.hits);
+
+    // this lane's slice of the output gradient
+    const int e0 = s.sub * EPV;
+    float gs[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) {
+        gs[e] = (s.hits && e0 + e < p.D)
+                    ? p.grad_out[((size_t)b * p.Q + s.q) * (size_t)p.C + (size_t)s.mh * p.D + e0 + e]
+                    : 0.0f;
+    }
+    const uint32_t lane_off = (uint32_t)s.sub * LW;
+    const uint32_t head_off = (uint32_t)s.mh * p.head_bytes;
+    uint32_t *rec = m.tap + (size_t)slot_id * p.slot_stride;
+
+    for (int n = 0; n < p.N; ++n) {
+        if (!((cams >> n) & 1u)) continue;
+        const bool mine = (s.hits >> n) & 1u;
+        const __amdgpu_buffer_rsrc_t rsrc = sca_camera_rsrc(p, b, n);
+        const float2 *ref = m.ref + (size_t)(s.qi * p.N + n) * p.Z;
+        float *gv = p.grad_value ? p.grad_value + ((size_t)b * p.N + n) * p.cam_elems : nullptr;
+        for (int c0 = 0; c0 < LP; c0 += lph) {
+            const int j = c0 + s.sub;
+            uint4 o = make_uint4(kScaNoTap, kScaNoTap, kScaNoTap, kScaNoTap);
+            float4 w = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            float ax = 0.0f, ay = 0.0f, aa = 0.0f;
+            if (mine && j < LP) {
+                if (sca_setup_point(p, m, ref, s, j, head_off, o, ax, ay)) {
+                    w = sca_weights(o, ax, ay, 1.0f);
+                    aa = s.inv * att[j];   // the value scatter's factor: mean times a_j
+                }
+            }
+            uint32_t *mine_rec = rec + s.sub * kRecBwd;
+            *reinterpret_cast<uint4 *>(mine_rec) = o;
+            *reinterpret_cast<float4 *>(mine_rec + 4) = w;
+            *reinterpret_cast<float4 *>(mine_rec + 8) = make_float4(ax, ay, aa, 0.0f);
+            wave_lds_sync();
+            const int npts = (LP - c0) < lph ? (LP - c0) : lph;
+            // gradients of the point this lane owns (point c0 + sub)
+            float my_da = 0.0f, my_dx = 0.0f, my_dy = 0.0f;
+            for (int t = 0; t < npts; ++t) {
+                const uint4 to = *reinterpret_cast<const uint4 *>(rec + t * kRecBwd);
+                const float4 tw = *reinterpret_cast<const float4 *>(rec + t * kRecBwd + 4);
+                const float4 tf = *reinterpret_cast<const float4 *>(rec + t * kRecBwd + 8);
+                const Raw<LW> v0 = load_vec<LW>(rsrc, to.x + lane_off, 0);
+                const Raw<LW> v1 = load_vec<LW>(rsrc, to.y + lane_off, 0);
+                const Raw<LW> v2 = load_vec<LW>(rsrc, to.z + lane_off, 0);
+                const Raw<LW> v3 = load_vec<LW>(rsrc, to.w + lane_off, 0);
+                // this lane's share of sum_c V[tap, c] G[c] for the four taps
+                float d0 = 0.0f, d1 = 0.0f, d2 = 0.0f, d3 = 0.0f;
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) {
+                    d0 = fmaf(elem<DT, LW>(v0, e), gs[e], d0);
+                    d1 = fmaf(elem<DT, LW>(v1, e), gs[e], d1);
+                    d2 = fmaf(elem<DT, LW>(v2, e), gs[e], d2);
+                    d3 = fmaf(elem<DT, LW>(v3, e), gs[e], d3);
+                }
+                for (int x = lph >> 1; x >= 1; x >>= 1) {
+                    d0 += __shfl_xor(d0, x);
+                    d1 += __shfl_xor(d1, x);
+                    d2 += __shfl_xor(d2, x);
+                    d3 += __shfl_xor(d3, x);
+                }
+                const float tax = tf.x, tay = tf.y;
+                const float da = ((tw.x * d0 + tw.y * d1) + tw.z * d2) + tw.w * d3;
+                const float dx = (1.0f - tay) * (d1 - d0) + tay * (d3 - d2);
+                const float dy = (1.0f - tax) * (d2 - d0) + tax * (d3 - d1);
+                const bool own = s.sub == t;
+                my_da += own ? da : 0.0f;
+                my_dx += own ? dx : 0.0f;
+                my_dy += own ? dy : 0.0f;
+                // value gradient: mean * a * w * G[c] onto each in-range tap
+                if (gv) {
+                    const float aa_t = tf.z;
+                    const uint32_t ot[4] = {to.x, to.y, to.z, to.w};
+                    const float wt[4] = {tw.x, tw.y, tw.z, tw.w};
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (ot[c] == kScaNoTap) continue;
+                        const float coef = aa_t * wt[c];
+                        float *dst = gv + ot[c] / ES + e0;
+#pragma unroll
+                        for (int e = 0; e < EPV; ++e)
+                            if (e0 + e < p.D) unsafeAtomicAdd(dst + e, coef * gs[e]);
+                    }
+                }
+            }
+            if (mine && j < LP) {
+                g_da[j] += my_da;
+                g_dx[j] += my_dx;
+                g_dy[j] += my_dy;
+            }
+            wave_lds_sync();
+        }
+    }
+
+    // ---- softmax backward and the point gradients (lanes own points j = sub mod lph)
+    float dot = 0.0f;
+    if (s.hits)
+        for (int j = s.sub; j < LP; j += lph) dot += att[j] * g_da[j];
+    for (int x = lph >> 1; x >= 1; x >>= 1) dot += __shfl_xor(dot, x);
+    if (s.active) {
+        for (int j = s.sub; j < LP; j += lph) {
+            const float sa = s.hits ? s.inv * att[j] : 0.0f;
+            if (p.grad_logits) p.grad_logits[s.pt0 + j] = sa * (g_da[j] - dot);
+            if (p.grad_offsets)
+                reinterpret_cast<float2 *>(p.grad_offsets)[s.pt0 + j] =
+                    make_float2(sa * g_dx[j], sa * g_dy[j]);
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) sca_zero_fill(float *dst, uint64_t n)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        dst[i] = 0.0f;
 }
 
 using ScaKernelFn = void (*)(const ScaParams);
 
-template <int DT>
+template <int DT, bool BWD>
 ScaKernelFn pick_sca_lw(int lw)
 {
     switch (lw) {
-    case 16: return sca_fwd<DT, 16>;
-    case 8: return sca_fwd<DT, 8>;
-    case 4: return sca_fwd<DT, 4>;
+    case 16: return BWD ? sca_bwd<DT, 16> : sca_fwd<DT, 16>;
+    case 8: return BWD ? sca_bwd<DT, 8> : sca_fwd<DT, 8>;
+    case 4: return BWD ? sca_bwd<DT, 4> : sca_fwd<DT, 4>;
     default:
         if constexpr (DT == FLASHBEV_F32) return nullptr;
-        else return sca_fwd<DT, 2>;
+        else return BWD ? sca_bwd<DT, 2> : sca_fwd<DT, 2>;
     }
 }
 
-ScaKernelFn pick_sca(int dtype, int lw)
+ScaKernelFn pick_sca(int dtype, int lw, bool backward)
 {
     switch (dtype) {
-    case FLASHBEV_F32: return pick_sca_lw<FLASHBEV_F32>(lw);
-    case FLASHBEV_F16: return pick_sca_lw<FLASHBEV_F16>(lw);
-    default: return pick_sca_lw<FLASHBEV_BF16>(lw);
+    case FLASHBEV_F32:
+        return backward ? pick_sca_lw<FLASHBEV_F32, true>(lw) : pick_sca_lw<FLASHBEV_F32, false>(lw);
+    case FLASHBEV_F16:
+        return backward ? pick_sca_lw<FLASHBEV_F16, true>(lw) : pick_sca_lw<FLASHBEV_F16, false>(lw);
+    default:
+        return backward ? pick_sca_lw<FLASHBEV_BF16, true>(lw) : pick_sca_lw<FLASHBEV_BF16, false>(lw);
     }
 }
 
@@ -388,21 +645,35 @@ struct ScaPlan {
     size_t lds;
     int lw;
     bool empty;
+    uint64_t value_elems;   // B N S C
 };
 
 bool sca_finite(float v) { return v == v && v - v == 0.0f; }
 
 bool sca_overlaps(const void *a, size_t na, const void *b, size_t nb)
 {
-    if (!na || !nb) return false;
+    if (!na || !nb || !a || !b) return false;
     const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
     return a0 < b0 + nb && b0 < a0 + na;
 }
 
+// Device pointers of one call (forward: out; backward: grad_out and the
+// three gradients, any of which may be null).
+struct ScaBufs {
+    const float *l2i = nullptr;
+    const float *off = nullptr;
+    const float *lg = nullptr;
+    const float *out = nullptr;
+    const float *gout = nullptr;
+    const float *gvalue = nullptr;
+    const float *goff = nullptr;
+    const float *glg = nullptr;
+};
+
 // All argument checks; `need_data` requires the device pointers.
-int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_grid_spec *s,
-                  const flashbev_z_bins *zb, int32_t P, const float *off, const float *lg,
-                  const float *out, bool need_data, ScaPlan *pl)
+int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
+                  const flashbev_z_bins *zb, int32_t P, const ScaBufs &bf, bool backward,
+                  bool need_data, ScaPlan *pl)
 {
     if (!v || !s || !zb) return FLASHBEV_ERR_NULLPTR;
     if (v->dtype != FLASHBEV_F32 && v->dtype != FLASHBEV_F16 && v->dtype != FLASHBEV_BF16)
@@ -437,24 +708,54 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
         return FLASHBEV_ERR_UNSUPPORTED;
     const int LP = v->L * P;
     const uint64_t out_elems = (uint64_t)v->B * Q * v->C;
-    const bool empty = out_elems == 0;
-    const uint64_t value_bytes = (uint64_t)v->B * v->N * cam_bytes;
+    const uint64_t value_elems = (uint64_t)v->B * v->N * S * v->C;
+    const uint64_t value_bytes = value_elems * es;
     const uint64_t pts = (uint64_t)v->B * Q * v->heads * LP;
-    if (need_data && !empty) {
-        if (!out || !off || !lg) return FLASHBEV_ERR_NULLPTR;
-        if (value_bytes > 0 && !v->data) return FLASHBEV_ERR_NULLPTR;
-        if (v->N > 0 && !l2i) return FLASHBEV_ERR_NULLPTR;
-        if (((uintptr_t)v->data % es) || ((uintptr_t)l2i % 4) || ((uintptr_t)out % 4) ||
-            ((uintptr_t)off % 4) || ((uintptr_t)lg % 4))
-            return FLASHBEV_ERR_ALIGN;
+    // forward: nothing to do without outputs; backward: a requested value
+    // gradient is still zeroed
+    const bool empty = out_elems == 0;
+    if (need_data) {
         const size_t ob = out_elems * 4;
-        if (sca_overlaps(out, ob, v->data, value_bytes) ||
-            sca_overlaps(out, ob, l2i, (size_t)v->B * v->N * 64) ||
-            sca_overlaps(out, ob, off, pts * 8) || sca_overlaps(out, ob, lg, pts * 4))
-            return FLASHBEV_ERR_ALIAS;
+        if (!backward) {
+            if (!empty) {
+                if (!bf.out || !bf.off || !bf.lg) return FLASHBEV_ERR_NULLPTR;
+                if (value_bytes > 0 && !v->data) return FLASHBEV_ERR_NULLPTR;
+                if (v->N > 0 && !bf.l2i) return FLASHBEV_ERR_NULLPTR;
+                if (((uintptr_t)v->data % es) || ((uintptr_t)bf.l2i % 4) ||
+                    ((uintptr_t)bf.out % 4) || ((uintptr_t)bf.off % 8) || ((uintptr_t)bf.lg % 4))
+                    return FLASHBEV_ERR_ALIGN;
+                if (sca_overlaps(bf.out, ob, v->data, value_bytes) ||
+                    sca_overlaps(bf.out, ob, bf.l2i, (size_t)v->B * v->N * 64) ||
+                    sca_overlaps(bf.out, ob, bf.off, pts * 8) ||
+                    sca_overlaps(bf.out, ob, bf.lg, pts * 4))
+                    return FLASHBEV_ERR_ALIAS;
+            }
+        } else {
+            if (!bf.gvalue && !bf.goff && !bf.glg) return FLASHBEV_ERR_NULLPTR;
+            if (!empty) {
+                if (!bf.gout || !bf.off || !bf.lg) return FLASHBEV_ERR_NULLPTR;
+                if (value_bytes > 0 && !v->data) return FLASHBEV_ERR_NULLPTR;
+                if (v->N > 0 && !bf.l2i) return FLASHBEV_ERR_NULLPTR;
+            }
+            if (((uintptr_t)v->data % es) || ((uintptr_t)bf.l2i % 4) || ((uintptr_t)bf.gout % 4) ||
+                ((uintptr_t)bf.off % 8) || ((uintptr_t)bf.lg % 4) || ((uintptr_t)bf.gvalue % 4) ||
+                ((uintptr_t)bf.goff % 8) || ((uintptr_t)bf.glg % 4))
+                return FLASHBEV_ERR_ALIGN;
+            // every output is disjoint from every input and from the others
+            const void *ins[5] = {v->data, bf.l2i, bf.off, bf.lg, bf.gout};
+            const size_t insz[5] = {(size_t)value_bytes, (size_t)v->B * v->N * 64,
+                                    (size_t)pts * 8, (size_t)pts * 4, ob};
+            const void *outs[3] = {bf.gvalue, bf.goff, bf.glg};
+            const size_t outsz[3] = {(size_t)value_elems * 4, (size_t)pts * 8, (size_t)pts * 4};
+            for (int a = 0; a < 3; ++a) {
+                for (int i = 0; i < 5; ++i)
+                    if (sca_overlaps(outs[a], outsz[a], ins[i], insz[i])) return FLASHBEV_ERR_ALIAS;
+                for (int c = a + 1; c < 3; ++c)
+                    if (sca_overlaps(outs[a], outsz[a], outs[c], outsz[c]))
+                        return FLASHBEV_ERR_ALIAS;
+            }
+        }
     }
-    // the offsets travel as float2 loads
-    if (need_data && !empty && ((uintptr_t)off % 8)) return FLASHBEV_ERR_ALIGN;
 
     // lane slice: 16 bytes where a head row has at least four of them
     // (measured on MI355X, BEVFormer-base bfloat16: 16-byte lanes, 4 per head,
@@ -470,7 +771,7 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
     while (lph < nvec) { lph <<= 1; ++lph_shift; }
     if (lph > kScaWave) return FLASHBEV_ERR_UNSUPPORTED;
     const int spw = kScaWave / lph;
-    const int slot_stride = lph * kTapDwords + kSlotPad;
+    const int slot_stride = lph * (backward ? kRecBwd : kRecFwd) + kSlotPad;
 
     int waves = kScaWavesMax;
     int nq_max = 0;
@@ -479,21 +780,27 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
         const int tp = waves * spw;
         nq_max = (tp - 1) / v->heads + 2;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
-        lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, slot_stride);
+        lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, slot_stride, backward);
         if (lay.total <= kScaLdsBudget || waves == 1) break;
         waves >>= 1;
     }
-    if (lay.total > kScaLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
+    // many points per head: one wavefront per workgroup, with more LDS
+    if (lay.total > kScaLdsMax) return FLASHBEV_ERR_UNSUPPORTED;
     const int tile_pairs = waves * spw;
 
     ScaParams &p = pl->prm;
     memset(&p, 0, sizeof(p));
     p.value = v->data;
-    p.l2i = l2i;
-    p.offsets = off;
-    p.logits = lg;
-    p.out = const_cast<float *>(out);
+    p.l2i = bf.l2i;
+    p.offsets = bf.off;
+    p.logits = bf.lg;
+    p.out = const_cast<float *>(bf.out);
+    p.grad_out = bf.gout;
+    p.grad_value = const_cast<float *>(bf.gvalue);
+    p.grad_offsets = const_cast<float *>(bf.goff);
+    p.grad_logits = const_cast<float *>(bf.glg);
     p.cam_bytes = cam_bytes;
+    p.cam_elems = S * (uint64_t)v->C;
     p.row_bytes = (uint32_t)row;
     p.head_bytes = (uint32_t)head_bytes;
     p.B = v->B; p.N = v->N; p.C = v->C; p.heads = v->heads; p.D = D;
@@ -533,6 +840,7 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
     p.lds_ref = lay.ref;
     p.lds_hit = lay.hit;
     p.lds_att = lay.att;
+    p.lds_acc = lay.acc;
     p.lds_tap = lay.tap;
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
@@ -542,7 +850,31 @@ int make_sca_plan(const flashsca_value *v, const float *l2i, const flashbev_bev_
     pl->lds = lay.total;
     pl->lw = lw;
     pl->empty = empty;
+    pl->value_elems = value_elems;
     return FLASHBEV_OK;
+}
+
+void write_info(const ScaPlan &pl, int64_t *workgroups, int32_t *threads, int32_t *lds,
+                int32_t *lanes_per_head, int32_t *lane_bytes)
+{
+    if (workgroups) *workgroups = pl.workgroups;
+    if (threads) *threads = pl.threads;
+    if (lds) *lds = (int32_t)pl.lds;
+    if (lanes_per_head) *lanes_per_head = pl.prm.lph;
+    if (lane_bytes) *lane_bytes = pl.lw;
+}
+
+int launch(ScaKernelFn fn, ScaPlan &pl, hipStream_t st)
+{
+    const void *f = reinterpret_cast<const void *>(fn);
+    if (pl.lds > kScaLdsBudget &&
+        hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds) !=
+            hipSuccess)
+        return FLASHBEV_ERR_HIP;
+    void *args[] = {&pl.prm};
+    const hipError_t e = hipLaunchKernel(f, dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
+                                         pl.lds, st);
+    return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
 }
 
 }  // namespace
@@ -554,14 +886,23 @@ extern "C" int flashsca_launch_info(const flashsca_value *value,
                                     int32_t *lanes_per_head, int32_t *lane_bytes)
 {
     ScaPlan pl;
-    const int rc = make_sca_plan(value, nullptr, spec, anchors, P, nullptr, nullptr, nullptr,
-                                 false, &pl);
+    const int rc = make_sca_plan(value, spec, anchors, P, ScaBufs{}, false, false, &pl);
     if (rc) return rc;
-    if (workgroups) *workgroups = pl.workgroups;
-    if (threads_per_workgroup) *threads_per_workgroup = pl.threads;
-    if (lds_bytes) *lds_bytes = (int32_t)pl.lds;
-    if (lanes_per_head) *lanes_per_head = pl.prm.lph;
-    if (lane_bytes) *lane_bytes = pl.lw;
+    write_info(pl, workgroups, threads_per_workgroup, lds_bytes, lanes_per_head, lane_bytes);
+    return FLASHBEV_OK;
+}
+
+extern "C" int flashsca_backward_launch_info(const flashsca_value *value,
+                                             const flashbev_bev_grid_spec *spec,
+                                             const flashbev_z_bins *anchors, int32_t P,
+                                             int64_t *workgroups, int32_t *threads_per_workgroup,
+                                             int32_t *lds_bytes, int32_t *lanes_per_head,
+                                             int32_t *lane_bytes)
+{
+    ScaPlan pl;
+    const int rc = make_sca_plan(value, spec, anchors, P, ScaBufs{}, true, false, &pl);
+    if (rc) return rc;
+    write_info(pl, workgroups, threads_per_workgroup, lds_bytes, lanes_per_head, lane_bytes);
     return FLASHBEV_OK;
 }
 
@@ -570,16 +911,47 @@ extern "C" int flashsca_forward(const flashsca_value *value, const float *lidar2
                                 const flashbev_z_bins *anchors, int32_t P, const float *offsets,
                                 const float *logits, float *out, void *stream)
 {
+    ScaBufs bf;
+    bf.l2i = lidar2img;
+    bf.off = offsets;
+    bf.lg = logits;
+    bf.out = out;
     ScaPlan pl;
-    const int rc = make_sca_plan(value, lidar2img, spec, anchors, P, offsets, logits, out, true,
-                                 &pl);
+    const int rc = make_sca_plan(value, spec, anchors, P, bf, false, true, &pl);
     if (rc) return rc;
     if (pl.empty) return FLASHBEV_OK;
-    const ScaKernelFn fn = pick_sca(value->dtype, pl.lw);
+    const ScaKernelFn fn = pick_sca(value->dtype, pl.lw, false);
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
-    void *args[] = {&pl.prm};
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),
-                                         dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
-                                         pl.lds, reinterpret_cast<hipStream_t>(stream));
-    return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
+    return launch(fn, pl, reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" int flashsca_backward(const flashsca_value *value, const float *lidar2img,
+                                 const flashbev_bev_grid_spec *spec,
+                                 const flashbev_z_bins *anchors, int32_t P, const float *offsets,
+                                 const float *logits, const float *grad_out, float *grad_value,
+                                 float *grad_offsets, float *grad_logits, void *stream)
+{
+    ScaBufs bf;
+    bf.l2i = lidar2img;
+    bf.off = offsets;
+    bf.lg = logits;
+    bf.gout = grad_out;
+    bf.gvalue = grad_value;
+    bf.goff = grad_offsets;
+    bf.glg = grad_logits;
+    ScaPlan pl;
+    const int rc = make_sca_plan(value, spec, anchors, P, bf, true, true, &pl);
+    if (rc) return rc;
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (grad_value && pl.value_elems > 0) {
+        uint64_t blocks = (pl.value_elems + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        hipLaunchKernelGGL(sca_zero_fill, dim3((unsigned)blocks), dim3(256), 0, st, grad_value,
+                           pl.value_elems);
+        if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
+    }
+    if (pl.empty) return FLASHBEV_OK;
+    const ScaKernelFn fn = pick_sca(value->dtype, pl.lw, true);
+    if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
+    return launch(fn, pl, st);
 }

@@ -161,3 +161,59 @@ def test_binding_rejects_host_tensors():
         fb.sca_forward(torch.zeros(1, 6, 16, 8), torch.zeros(1, 6, 4, 4), [0.0],
                        fb.BevGrid(0, 1, 2, 0, 1, 2), (32, 32), ((4, 4),), 2,
                        torch.zeros(1, 4, 2, 1, 1, 2), torch.zeros(1, 4, 2, 1, 1))
+
+
+GV = 0x7F5000000000
+GO = 0x7F6000000000
+GL = 0x7F7000000000
+GOUT = 0x7F8000000000
+
+
+def bcall(gv=GV, go=GO, gl=GL, gout=GOUT, **kw):
+    """flashsca_backward with fake addresses (rejected before any HIP call
+    in every case below)."""
+    z = np.asarray(kw.pop("z", (-4.5, -2.1666667, 0.16666667, 2.5)), np.float32)
+    lh = (ctypes.c_int32 * 8)(*[h for h, _ in LEVELS], *([0] * 4))
+    lw = (ctypes.c_int32 * 8)(*[w for _, w in LEVELS], *([0] * 4))
+    v = ScaValue(kw.pop("val", VAL), 0, 1, 6, 256, 8, 4, lh, lw, 900, 1600)
+    g = GridSpec(-51.2, 0.512, 200, -51.2, 0.512, 200, 1e-5, 0)
+    zb = ZBins(z.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(z))
+    return fb._lib().flashsca_backward(ctypes.byref(v), ctypes.c_void_p(L2I), ctypes.byref(g),
+                                       ctypes.byref(zb), 8, ctypes.c_void_p(kw.pop("off", OFF)),
+                                       ctypes.c_void_p(LOG), ctypes.c_void_p(gout),
+                                       ctypes.c_void_p(gv), ctypes.c_void_p(go),
+                                       ctypes.c_void_p(gl), ctypes.c_void_p(0))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(gv=0, go=0, gl=0), "ERR_NULLPTR"),       # no gradient requested
+    (dict(gout=0), "ERR_NULLPTR"),
+    (dict(val=0), "ERR_NULLPTR"),
+    (dict(go=GO + 4), "ERR_ALIGN"),                # offsets gradient travels as float2
+    (dict(gl=GL + 2), "ERR_ALIGN"),
+    (dict(gv=GV + 1), "ERR_ALIGN"),
+    (dict(gv=VAL), "ERR_ALIAS"),                   # over the value maps
+    (dict(go=LOG), "ERR_ALIAS"),                   # over the logits
+    (dict(gl=GOUT), "ERR_ALIAS"),                  # over the output gradient
+    (dict(gl=GO + 64), "ERR_ALIAS"),               # two outputs overlap
+])
+def test_backward_argument_errors_before_any_hip_call(kw, status):
+    assert bcall(**kw) == S[status], kw
+
+
+def test_backward_launch_geometry():
+    d = dict(shape=(1, 6, sum(h * w for h, w in LEVELS), 256), dtype="f32", heads=8,
+             levels=LEVELS, anchors=[-4.5, -2.2, 0.2, 2.5],
+             grid=fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), img_hw=(900, 1600), P=8)
+    f = fb.sca_launch_info(**d)
+    b = fb.sca_launch_info(**d, backward=True)
+    # same slots and tiles; the backward also keeps per-point gradients and
+    # wider chunk records in LDS
+    assert (b["workgroups"], b["lanes_per_head"], b["lane_bytes"], b["threads"]) == \
+        (f["workgroups"], f["lanes_per_head"], f["lane_bytes"], f["threads"])
+    assert b["lds_bytes"] > f["lds_bytes"]
+    # L * P = 512 with 16 slots per wavefront: one wavefront and more than
+    # 64 KiB of LDS
+    d2 = dict(d, shape=(1, 6, 30825, 32), heads=4, P=128)
+    b = fb.sca_launch_info(**d2, backward=True)
+    assert b["threads"] == 64 and 64 * 1024 < b["lds_bytes"] <= 160 * 1024
