@@ -100,21 +100,23 @@ struct ScaParams {
     int32_t level_w[FLASHSCA_LMAX], level_h[FLASHSCA_LMAX];
     uint32_t level_start[FLASHSCA_LMAX];   // first pixel of each level
     // LDS layout (byte offsets)
-    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_acc, lds_tap;
+    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_acc, lds_gst, lds_tap;
+    float rcp_d;             // float32 1 / D for div_small
     float z[FLASHSCA_ZMAX];
 };
 
 // LDS: camera matrices [N][12]; level table [5][LMAX]; anchors [Z];
 // reference points [nq_max][N][Z] float2; hit masks [nq_max]; attention
 // weights [waves][spw][LP]; backward only: point gradients
-// [waves][spw][3][LP]; chunk records [waves][spw][slot_stride].
+// [waves][spw][3][LP] and output-gradient rows [waves][spw][D]; chunk records
+// [waves][spw][slot_stride].
 struct ScaLds {
-    uint32_t mat, lvl, z, ref, hit, att, acc, tap, total;
+    uint32_t mat, lvl, z, ref, hit, att, acc, gst, tap, total;
 };
 
 __host__ inline uint32_t sca_align16(uint32_t v) { return (v + 15u) & ~15u; }
 
-__host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int LP,
+__host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int LP, int D,
                                int slot_stride, bool backward)
 {
     ScaLds s;
@@ -126,6 +128,7 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
     s.hit = o; o = sca_align16(o + (uint32_t)nq_max * 4u);
     s.att = o; o = sca_align16(o + (uint32_t)waves * spw * LP * 4u);
     s.acc = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * LP * 12u : 0u));
+    s.gst = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * D * 4u : 0u));
     s.tap = o; o = sca_align16(o + (uint32_t)waves * spw * slot_stride * 4u);
     s.total = o;
     return s;
@@ -152,7 +155,7 @@ __device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
 
 // LDS views of one workgroup.
 struct ScaSmem {
-    float *mat, *lwf, *lhf, *z, *att, *acc;
+    float *mat, *lwf, *lhf, *z, *att, *acc, *gst;
     int32_t *lw, *lh;
     uint32_t *lst, *hit, *tap;
     float2 *ref;
@@ -172,6 +175,7 @@ __device__ __forceinline__ ScaSmem sca_smem(const ScaParams &p, unsigned char *s
     m.hit = reinterpret_cast<uint32_t *>(smem + p.lds_hit);
     m.att = reinterpret_cast<float *>(smem + p.lds_att);
     m.acc = reinterpret_cast<float *>(smem + p.lds_acc);
+    m.gst = reinterpret_cast<float *>(smem + p.lds_gst);
     m.tap = reinterpret_cast<uint32_t *>(smem + p.lds_tap);
     return m;
 }
@@ -506,6 +510,15 @@ sca_bwd(const ScaParams p)
     const uint32_t lane_off = (uint32_t)s.sub * LW;
     const uint32_t head_off = (uint32_t)s.mh * p.head_bytes;
     uint32_t *rec = m.tap + (size_t)slot_id * p.slot_stride;
+    // the wavefront's output-gradient rows, for the value scatter
+    const int D = p.D;
+    float *gst_w = m.gst + (size_t)wave * p.spw * D;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e)
+        if (e0 + e < D) gst_w[s.slot * D + e0 + e] = gs[e];
+    const uint32_t *rec_w = m.tap + (size_t)wave * p.spw * p.slot_stride;   // the wavefront's
+    const int rows_pt = p.spw * 4;           // (slot, tap) rows per point index
+    const int elems_pt = rows_pt * D;
 
     for (int n = 0; n < p.N; ++n) {
         if (!((cams >> n) & 1u)) continue;
@@ -563,19 +576,25 @@ sca_bwd(const ScaParams p)
                 my_da += own ? da : 0.0f;
                 my_dx += own ? dx : 0.0f;
                 my_dy += own ? dy : 0.0f;
-                // value gradient: mean * a * w * G[c] onto each in-range tap
-                if (gv) {
-                    const float aa_t = tf.z;
-                    const uint32_t ot[4] = {to.x, to.y, to.z, to.w};
-                    const float wt[4] = {tw.x, tw.y, tw.z, tw.w};
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) {
-                        if (ot[c] == kScaNoTap) continue;
-                        const float coef = aa_t * wt[c];
-                        float *dst = gv + ot[c] / ES + e0;
-#pragma unroll
-                        for (int e = 0; e < EPV; ++e)
-                            if (e0 + e < p.D) unsafeAtomicAdd(dst + e, coef * gs[e]);
+            }
+            // value gradient: mean * a * w * G[c] onto each in-range tap.  The
+            // wavefront walks its (point, slot, tap, channel) elements in that
+            // order, 64 consecutive channels per atomic instruction, so one
+            // instruction covers whole head rows (one 128-byte row per 32
+            // lanes for float32 D = 32) rather than a few channels of each
+            // slot's row.
+            if (gv) {
+                for (int t = 0; t < npts; ++t) {
+                    for (int E = lane; E < elems_pt; E += kScaWave) {
+                        const int row = div_small(E, D, p.rcp_d);
+                        const int ch = E - row * D;
+                        const int sl = row >> 2, c = row & 3;
+                        const uint32_t *r = rec_w + (size_t)sl * p.slot_stride + t * kRecBwd;
+                        const uint32_t ot = r[c];
+                        if (ot == kScaNoTap) continue;
+                        const float coef = __builtin_bit_cast(float, r[10]) *
+                                           __builtin_bit_cast(float, r[4 + c]);
+                        unsafeAtomicAdd(gv + ot / ES + ch, coef * gst_w[sl * D + ch]);
                     }
                 }
             }
@@ -780,7 +799,7 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
         const int tp = waves * spw;
         nq_max = (tp - 1) / v->heads + 2;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
-        lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, slot_stride, backward);
+        lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, D, slot_stride, backward);
         if (lay.total <= kScaLdsBudget || waves == 1) break;
         waves >>= 1;
     }
@@ -841,6 +860,8 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     p.lds_hit = lay.hit;
     p.lds_att = lay.att;
     p.lds_acc = lay.acc;
+    p.lds_gst = lay.gst;
+    p.rcp_d = 1.0f / (float)D;
     p.lds_tap = lay.tap;
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
