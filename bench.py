@@ -354,6 +354,28 @@ def make_sca_call(wl, inst, device):
     return call, (v, l2i, off, lg, out), stream
 
 
+def make_sca_backward_call(wl, inst, device, seed: int = 5):
+    """A prepared FlashSCA backward call computing all three gradients."""
+    import numpy as np
+    import torch
+
+    import paper_2607_10071_amd as fb
+
+    v = synth_to_storage(inst.value, wl.dtype).to(device)
+    l2i = torch.from_numpy(inst.lidar2img).to(device)
+    off = torch.from_numpy(inst.offsets).to(device)
+    lg = torch.from_numpy(inst.logits).to(device)
+    g = torch.from_numpy(np.random.default_rng([wl.cfg_id, 9, seed]).standard_normal(
+        (wl.B, wl.Q, wl.C)).astype(np.float32)).to(device)
+    gv = torch.empty((wl.B, wl.N, wl.S, wl.C), dtype=torch.float32, device=device)
+    go = torch.empty(tuple(off.shape), dtype=torch.float32, device=device)
+    gl = torch.empty(tuple(lg.shape), dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream(device)
+    call = fb.prepare_sca_backward(v, l2i, inst.z, fb.grid_of(wl), (wl.img_h, wl.img_w),
+                                   wl.levels, wl.heads, off, lg, g, gv, go, gl, stream=stream)
+    return call, (v, l2i, off, lg, g, gv, go, gl), stream
+
+
 def synth_to_storage(a, dtype):
     import synth
 
@@ -417,6 +439,10 @@ def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
              "traffic": load_traffic(f"sca_base_p{P}", SCA_KERNEL_SRC),
              "paper_4070tis": SCA_PAPER.get(P)}
         del fn, keep
+        bfn, bkeep, bstream = make_sca_backward_call(wl, inst, device)
+        tb = time_gpu(bfn, max(5, steps // 2), max(2, warmup // 2), bstream, 0.1)
+        del bfn, bkeep
+        r["backward_ms"] = round(tb["ms_per_step"], 5)
         if cpu:
             cb = sca_cpu_baseline(inst, cpu_seconds)
             counters = cb.pop("counters")
@@ -427,6 +453,9 @@ def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
             r["gather_GBs"] = round(g / sec / 1e9, 1)
             r["taps"] = counters["taps"]
             r["hits"] = counters["hits"]
+            # backward: one float atomic add per (in-range tap, channel)
+            r["backward_value_terms_G_per_s"] = round(
+                counters["taps"] * (wl.C // wl.heads) / (tb["ms_per_step"] * 1e-3) / 1e9, 1)
             r["cpu_baseline"] = cb
         rec["points"][str(P)] = r
     if bf16:
