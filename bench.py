@@ -43,9 +43,17 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2607_10071_amd", "csrc", "flashbev.hip")
 SCA_KERNEL_SRC = os.path.join(ROOT, "paper_2607_10071_amd", "csrc", "flashsca.hip")
 
 
+COMMON_SRC = os.path.join(ROOT, "paper_2607_10071_amd", "csrc", "hip_common.h")
+
+
 def kernel_hash(path: str = KERNEL_SRC) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """sha256[:16] of a kernel source together with the device helpers it
+    includes (counter data taken on other sources is stale)."""
+    h = hashlib.sha256()
+    for src in (path, COMMON_SRC):
+        with open(src, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def elem_size(dtype: str) -> int:
