@@ -99,7 +99,7 @@ def test_sca_reduce_modes(fb, device, reduce):
 @pytest.mark.parametrize("C,heads,dtype", [
     (32, 4, "f32"),      # D=8: 4-byte lanes
     (256, 8, "f32"),     # D=32: 16-byte lanes (BEVFormer)
-    (256, 8, "bf16"),    # D=32: 8-byte lanes
+    (256, 8, "bf16"),    # D=32: 16-byte lanes, two queries per wavefront
     (128, 8, "f16"),     # D=16
     (512, 8, "f32"),     # D=64: 16 lanes per head
     (256, 1, "f32"),     # D=256: one head fills a wavefront
@@ -229,3 +229,15 @@ def test_prepared_sca_matches_oracle(fb, device):
     torch.cuda.synchronize()
     ref, scale, terms, _ = oracle.sca_instance(inst)
     assert_sca_parity(out.cpu().numpy(), ref, scale, terms, wl.heads, "prepared")
+
+
+@pytest.mark.parametrize("what,kw", [
+    ("32 cameras", dict(N=32, X=6, Y=5)),
+    ("32 anchors", dict(Z=32, P=32, levels=((12, 32),), X=6, Y=5)),
+    ("L*P = 512", dict(P=64, Z=8, levels=((24, 64), (12, 32), (6, 16), (3, 8), (2, 4), (1, 2),
+                                         (1, 1), (5, 3)), X=4, Y=3)),
+    ("1 KiB head rows", dict(C=256, heads=1, X=6, Y=5)),
+    ("512-element bf16 heads", dict(C=1024, heads=2, dtype="bf16", X=5, Y=4)),
+])
+def test_sca_limits(fb, device, what, kw):
+    check(fb, small(12, **kw), device, what=what)

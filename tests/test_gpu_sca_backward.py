@@ -239,3 +239,15 @@ def test_prepared_sca_backward_matches_oracle(fb, device):
     torch.cuda.synchronize()
     gpu = {"value": gv.cpu().numpy(), "offsets": go.cpu().numpy(), "logits": gl.cpu().numpy()}
     assert_bwd_parity(gpu, oracle.sca_backward_instance(inst, g), wl, "prepared")
+
+
+@pytest.mark.parametrize("what,kw", [
+    ("32 cameras", dict(N=32, X=6, Y=5)),
+    ("32 anchors", dict(Z=32, P=32, levels=((12, 32),), X=6, Y=5)),
+    ("L*P = 512", dict(P=64, Z=8, levels=((24, 64), (12, 32), (6, 16), (3, 8), (2, 4), (1, 2),
+                                         (1, 1), (5, 3)), X=4, Y=3)),
+    ("1 KiB head rows", dict(C=256, heads=1, X=6, Y=5)),
+    ("512-element bf16 heads", dict(C=1024, heads=2, dtype="bf16", X=5, Y=4)),
+])
+def test_sca_backward_limits(fb, device, what, kw):
+    check(fb, small(12, **kw), device, what=what)
