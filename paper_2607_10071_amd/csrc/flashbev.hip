@@ -55,7 +55,15 @@ constexpr int kRecCap = 64;               // valid samples per (cell, projection
 constexpr int kRecStride = kRecCap + 1;   // odd stride: cells' lists start in different banks
 constexpr int kUnroll = 2;                // samples gathered per loop iteration
 constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
-constexpr int kStripe = 16;               // consecutive tiles per XCD stripe (backward)
+constexpr int kStripe = 16;               // consecutive tiles per XCD stripe
+// Forward calls that gather at most this many bytes of feature rows
+// (B X Y Z C elem) take contiguous bands of tiles per XCD, larger ones
+// interleaved stripes.  Measured on MI355X (bands against stripes of 16):
+// rep 23.9 -> 23.5 us, half_batch 77.6 -> 74.6, the paper's reference
+// setting 35.1 -> 32.8, long_range 105.6 -> 103.1, z_sweep 213.7 -> 212.0;
+// but with 8x the work (Z = 64, C = 1024 or a 1600 x 1600 grid at the
+// reference setting) bands lose 4% to the stripes' better balance.
+constexpr uint64_t kBandsWorkMax = 1ull << 30;
 // Offset of a tap that is not loaded: feature tensors are smaller than
 // 2 GiB and the tap steps are smaller than the tensor, so this offset plus
 // any step stays past the buffer (no 32-bit wrap) and the load returns zero
@@ -80,6 +88,7 @@ struct Params {
     float sx, sy;          // W / img_w, H / img_h (float32, computed once)
     float x_min, dx, y_min, dy, depth_eps;
     int32_t reduce;        // 0 valid mean, 1 sum
+    int32_t bands;         // 1: one contiguous band of tiles per XCD, 0: interleaved stripes
     uint32_t row_bytes;    // C * element size
     uint32_t step_x;       // byte step to the right-hand tap (0 if W == 1)
     uint32_t step_y;       // byte step to the lower tap (0 if H == 1)
@@ -149,22 +158,31 @@ sample_vt_fwd(const Params p)
     const int lane = tid % kWave;
     const int N = p.N;
 
-    // XCD-aware tile order.  Workgroups go to the 8 XCDs round-robin; the
-    // k-th workgroup on XCD x takes tile x * per + k, so each XCD works
-    // through one contiguous band of the grid (per = workgroups / 8; the
-    // last few keep the dispatch order).  A band of rows is seen by about
-    // half of the ring's cameras, whose features then fit the XCD's L2, and
-    // neighbouring tiles merge their partial output lines there.  Measured on
-    // MI355X against stripes of 16 tiles interleaved over the grid: rep
-    // 23.95 -> 23.69 us, half_batch 77.4 -> 74.6, the paper's reference
-    // setting 35.2 -> 32.9, long_range 106.0 -> 103.3 (longer stripes of 64
-    // to 256 tiles land in between).
+    // XCD-aware tile order.  Workgroups go to the 8 XCDs round-robin.
+    //  * Bands (p.bands, calls with little work): the k-th workgroup on XCD x
+    //    takes tile x * per + k, so each XCD works through one contiguous
+    //    band of the grid (per = workgroups / 8; the last few keep the
+    //    dispatch order).  A band of rows is seen by about half of the ring's
+    //    cameras, whose features then fit the XCD's L2.
+    //  * Stripes (more work): tile (k / S) * 8S + x * S + k % S, stripes of
+    //    S consecutive tiles interleaved over the grid, so that each XCD sees
+    //    a like mix of heavy and light regions and the tail stays short.
+    // Either way neighbouring tiles merge their partial output lines in one
+    // L2.  The choice is made on the host (make_plan).
     const int g = blockIdx.x;
-    const int per = (int)gridDim.x / kXcds;
     int tile = g;
-    if (g < per * kXcds) {
-        const int xcd = g % kXcds, k = g / kXcds;
-        tile = xcd * per + k;
+    if (p.bands) {
+        const int per = (int)gridDim.x / kXcds;
+        if (g < per * kXcds) {
+            const int xcd = g % kXcds, k = g / kXcds;
+            tile = xcd * per + k;
+        }
+    } else {
+        const int full = (int)(gridDim.x / (kXcds * kStripe)) * (kXcds * kStripe);
+        if (g < full) {
+            const int xcd = g % kXcds, k = g / kXcds;
+            tile = (k / kStripe) * (kXcds * kStripe) + xcd * kStripe + k % kStripe;
+        }
     }
     const int b = tile / p.tiles_per_b;
     const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
@@ -1101,6 +1119,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.x_min = s->x_min; p.dx = s->dx; p.y_min = s->y_min; p.dy = s->dy;
     p.depth_eps = s->depth_eps;
     p.reduce = s->reduce;
+    p.bands = ((uint64_t)f->B * XY * (uint64_t)zb->Z * row <= kBandsWorkMax) ? 1 : 0;
     p.row_bytes = (uint32_t)row;
     p.step_x = f->W >= 2 ? (uint32_t)row : 0u;
     p.step_y = f->H >= 2 ? (uint32_t)(row * f->W) : 0u;
