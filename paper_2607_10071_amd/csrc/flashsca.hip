@@ -183,12 +183,14 @@ __device__ __forceinline__ ScaSmem sca_smem(const ScaParams &p, unsigned char *s
 // XCD-aware tile order.  Queries are visited block by block (query_of), so
 // consecutive tiles cover a compact patch of the BEV whose samples land on
 // overlapping pixels (measured on MI355X at BEVFormer-base, P = 32: 16 x 16
-// blocks 0.927 ms, 32 x 32 0.953 ms, 64 x 64 slower still).  The k-th workgroup on XCD x takes tile
-// (k / S) * 8S + x * S + k % S with S = p.stripe (about one block): an XCD
-// works through whole blocks, its resident workgroups share their pixels in
-// its L2, and the blocks of the 8 XCDs interleave over the grid (a like mix
-// of heavy and light regions).  The tail that does not fill 8 stripes is
-// split the same way with shorter stripes.
+// blocks 0.927 ms, 32 x 32 0.953 ms, 64 x 64 slower still).  The k-th
+// workgroup on XCD x takes tile (k / S) * 8S + x * S + k % S with S =
+// p.stripe, one eighth of the tiles: each XCD works through one contiguous
+// band of blocks, whose samples come from few cameras and share pixels in
+// its L2 (against stripes of one block interleaved over the grid: P = 8
+// 0.282 -> 0.268 ms, P = 32 0.927 -> 0.900 ms, bfloat16 0.487 -> 0.467 ms,
+// backward 4.37 -> 4.31 ms).  The few tiles past 8 S are split the same way
+// with shorter stripes.
 __device__ __forceinline__ int sca_tile(const ScaParams &p)
 {
     const int g = blockIdx.x;
@@ -838,8 +840,9 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     const uint64_t pairs_b = Q * (uint64_t)v->heads;
     p.tiles_per_b = (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
     {
-        const int64_t st = (int64_t)kScaBlock * kScaBlock * v->heads / tile_pairs;
-        p.stripe = (int32_t)(st < 1 ? 1 : (st > 4096 ? 4096 : st));
+        // one contiguous band of tiles per XCD (see sca_tile)
+        const int64_t nt = (int64_t)v->B * p.tiles_per_b / kScaXcds;
+        p.stripe = (int32_t)(nt < 1 ? 1 : nt);
     }
     p.nq_max = nq_max;
     p.slot_stride = slot_stride;
