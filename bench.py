@@ -260,6 +260,60 @@ def measure_backward(wl, inst, device, steps, warmup, taps=None) -> dict:
     return rec
 
 
+def backward_cpu_baseline(inst, min_seconds: float = 3.0) -> dict:
+    """The backward oracle (float64, OpenMP) on the same workload, repeated
+    until ``min_seconds`` have passed."""
+    import numpy as np
+
+    import oracle
+
+    wl = inst.wl
+    threads = min(16, os.cpu_count() or 1)
+    g = np.random.default_rng([wl.cfg_id, 7]).standard_normal(
+        (wl.B, wl.C, wl.X, wl.Y)).astype(np.float32)
+    oracle.backward_instance(inst, g, nthreads=threads)  # warm-up
+    n, t0 = 0, time.perf_counter()
+    while True:
+        oracle.backward_instance(inst, g, nthreads=threads)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    per = el / n
+    return {"value": round(wl.samples / per / 1e9, 4), "unit": "Gsamples/s", "cores": threads,
+            "kind": "oracle", "ms_per_call": round(per * 1e3, 2),
+            "sample": f"the whole {wl.name} workload, {n} calls in {el:.1f} s"}
+
+
+def sca_backward_cpu_baseline(min_seconds: float = 3.0) -> dict:
+    """The FlashSCA backward oracle on a bounded sample of BEVFormer-base: the
+    same cameras, value maps, heads, levels and points, with a 64 x 64 grid of
+    queries over the same +-51.2 m (one call at 200 x 200 takes about 11 s)."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    wl = synth.sca_config("sca_base", X=64, Y=64, dx=102.4 / 64, dy=102.4 / 64)
+    inst = synth.make_sca_workload(wl)
+    threads = min(16, os.cpu_count() or 1)
+    g = np.random.default_rng([wl.cfg_id, 9, 5]).standard_normal(
+        (wl.B, wl.Q, wl.C)).astype(np.float32)
+    # outputs allocated once (their first touch is not the oracle's work)
+    bufs = oracle.sca_backward_instance(inst, g, nthreads=threads, with_scales=False)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        oracle.sca_backward_instance(inst, g, nthreads=threads, with_scales=False, buffers=bufs)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    per = el / n
+    return {"value": round(wl.B * wl.Q / per / 1e6, 4), "unit": "Mqueries/s", "cores": threads,
+            "kind": "oracle", "ms_per_call": round(per * 1e3, 1),
+            "sample": f"BEVFormer-base with a 64 x 64 query grid (P = 8), {n} calls in {el:.1f} s"}
+
+
 def peak_operator_memory(wl, inst, device) -> int:
     import torch
 
@@ -672,6 +726,8 @@ def main(argv=None) -> int:
                                             max(20, args.steps // 2), args.warmup)
         bwd["paper_context"] = {"flashbev_a6000_backward_ms": 3.27,
                                 "tensorized_a6000_backward_ms": 17.90}
+        if not args.no_cpu_baseline:
+            bwd[wl.name]["cpu_baseline"] = backward_cpu_baseline(inst)
         ceil = rec.get("ceilings_GBs", {}).get("float_atomic_Gops")
         if ceil and "terms_G_per_s" in bwd[wl.name]:
             bwd[wl.name]["float_atomic_ceiling_Gops"] = ceil
@@ -680,6 +736,8 @@ def main(argv=None) -> int:
         # FlashSCA (Sec. 4.5, Table 7) at BEVFormer-base defaults
         rec["sca"] = measure_sca(device, max(20, args.steps // 4), args.warmup,
                                  not args.no_cpu_baseline, 3.0)
+        if not args.no_cpu_baseline:
+            rec["sca"]["backward_cpu_baseline"] = sca_backward_cpu_baseline()
 
     print(json.dumps(rec), flush=True)
     return 0

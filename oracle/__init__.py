@@ -317,7 +317,8 @@ def sca_instance(inst, reduce="mean", nthreads=0, libpath=None):
 
 
 def sca_backward(value, lidar2img, z, offsets, logits, grad_out, levels, heads, img_hw, X, Y,
-                 x_min, dx, y_min, dy, depth_eps=1e-5, reduce="mean", nthreads=0, libpath=None):
+                 x_min, dx, y_min, dy, depth_eps=1e-5, reduce="mean", nthreads=0, libpath=None,
+                 with_scales=True, buffers=None):
     """Gradients of the FlashSCA forward with respect to the value maps, the
     offsets and the logits, for output gradient ``grad_out`` [B, X*Y, C].
 
@@ -326,6 +327,9 @@ def sca_backward(value, lidar2img, z, offsets, logits, grad_out, levels, heads, 
     [B, X*Y, heads, L, P, 2] with ``offsets_scale``; ``logits``
     [B, X*Y, heads, L, P] with ``logits_scale``; int32 ``point_terms``
     [B, X*Y, heads, L, P] (in-range corners per point over hit cameras).
+    ``with_scales=False`` skips the scales and term counts (None in the
+    result); ``buffers`` may hold preallocated float64 ``value``,
+    ``offsets`` and ``logits`` arrays of those shapes, which are reused.
     """
     v = np.ascontiguousarray(value, dtype=np.float32)
     m = np.ascontiguousarray(lidar2img, dtype=np.float32)
@@ -340,26 +344,41 @@ def sca_backward(value, lidar2img, z, offsets, logits, grad_out, levels, heads, 
     assert g.shape == (B, Q, C) and lg.shape == (B, Q, heads, L, P) and off.shape == lg.shape + (2,)
     p = sca_problem(B, N, C, heads, levels, P, len(zz), img_hw, X, Y, x_min, dx, y_min, dy,
                     depth_eps, reduce)
-    r = {
-        "value": np.empty((B, N, S, C)), "value_scale": np.empty((B, N, S, C)),
-        "value_terms": np.empty((B, N, S, heads), dtype=np.int32),
-        "offsets": np.empty((B, Q, heads, L, P, 2)), "offsets_scale": np.empty((B, Q, heads, L, P, 2)),
-        "logits": np.empty((B, Q, heads, L, P)), "logits_scale": np.empty((B, Q, heads, L, P)),
-        "point_terms": np.empty((B, Q, heads, L, P), dtype=np.int32),
-    }
+    shapes = {"value": (B, N, S, C), "offsets": (B, Q, heads, L, P, 2),
+              "logits": (B, Q, heads, L, P)}
+    r = {}
+    for k, shp in shapes.items():
+        buf = (buffers or {}).get(k)
+        if buf is not None:
+            assert buf.shape == shp and buf.dtype == np.float64 and buf.flags.c_contiguous
+            r[k] = buf
+        else:
+            r[k] = np.empty(shp)
+    if with_scales:
+        r.update({"value_scale": np.empty((B, N, S, C)),
+                  "value_terms": np.empty((B, N, S, heads), dtype=np.int32),
+                  "offsets_scale": np.empty((B, Q, heads, L, P, 2)),
+                  "logits_scale": np.empty((B, Q, heads, L, P)),
+                  "point_terms": np.empty((B, Q, heads, L, P), dtype=np.int32)})
+    else:
+        r.update({k: None for k in ("value_scale", "value_terms", "offsets_scale",
+                                    "logits_scale", "point_terms")})
+    ptr = lambda a: _ptr(a) if a is not None else None
     rc = _sca_lib(libpath).sca_oracle_backward(
         ctypes.byref(p), _ptr(v), _ptr(m), _ptr(zz), _ptr(off), _ptr(lg), _ptr(g),
-        _ptr(r["value"]), _ptr(r["value_scale"]), _ptr(r["value_terms"]), _ptr(r["offsets"]),
-        _ptr(r["offsets_scale"]), _ptr(r["logits"]), _ptr(r["logits_scale"]),
-        _ptr(r["point_terms"]), int(nthreads))
+        _ptr(r["value"]), ptr(r["value_scale"]), ptr(r["value_terms"]), _ptr(r["offsets"]),
+        ptr(r["offsets_scale"]), _ptr(r["logits"]), ptr(r["logits_scale"]),
+        ptr(r["point_terms"]), int(nthreads))
     if rc:
         raise ValueError(f"sca_oracle_backward failed: {rc}")
     return r
 
 
-def sca_backward_instance(inst, grad_out, reduce="mean", nthreads=0, libpath=None):
+def sca_backward_instance(inst, grad_out, reduce="mean", nthreads=0, libpath=None,
+                          with_scales=True, buffers=None):
     """FlashSCA backward oracle on a ``synth.ScaInstance``."""
     wl = inst.wl
     return sca_backward(inst.value, inst.lidar2img, inst.z, inst.offsets, inst.logits, grad_out,
                         wl.levels, wl.heads, (wl.img_h, wl.img_w), wl.X, wl.Y, wl.x_min, wl.dx,
-                        wl.y_min, wl.dy, wl.depth_eps, reduce, nthreads, libpath)
+                        wl.y_min, wl.dy, wl.depth_eps, reduce, nthreads, libpath, with_scales,
+                        buffers)
