@@ -51,7 +51,7 @@ constexpr int kWavesMax = 4;                 // wavefronts per workgroup (2 or 4
 constexpr int kThreadsMax = kWave * kWavesMax;  // 256
 constexpr int kCpwMax = 8;                // cells per wavefront group (upper bound)
 constexpr int kCellsPerWave = 6;          // a wavefront covers at least this many cells per tile
-constexpr int kRecCap = 64;               // valid samples per (cell, projection pass)
+constexpr int kRecCap = 64;               // valid samples per (cell, projection pass), at most
 constexpr int kRecStride = kRecCap + 1;   // odd stride: cells' lists start in different banks
 constexpr int kUnroll = 2;                // samples gathered per loop iteration
 constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
@@ -98,6 +98,7 @@ struct Params {
     float rcp_n, rcp_lpc;  // float32 1 / max(N, 1) and 1 / lpc
     int32_t zc;            // heights per projection pass
     int32_t otile_ld;      // row pitch (floats) of the LDS output tile, odd
+    int32_t rec_stride;    // records per cell list: one pass's samples, rounded up, odd
     // LDS layout (byte offsets)
     uint32_t lds_z, lds_w, lds_off, lds_otile;
     float z[FLASHBEV_ZMAX];
@@ -109,9 +110,9 @@ __device__ __forceinline__ float bcast(float v, int lane)
 }
 
 // LDS layout of one workgroup: camera matrices [N][12], heights [Z], sample
-// records [waves][cpw][kRecStride] (weights as float4, offsets as u32), and
-// the output tile [C][otile_ld].  The record stride and the tile pitch are
-// odd so that different cells and channels fall into different LDS banks.
+// records [waves][cpw][rs] (weights as float4, offsets as u32), and the
+// output tile [C][otile_ld].  The record stride and the tile pitch are odd so
+// that different cells and channels fall into different LDS banks.
 struct LdsLayout {
     uint32_t z, w, off, otile, total;
 };
@@ -119,16 +120,16 @@ struct LdsLayout {
 __host__ __device__ inline uint32_t align16(uint32_t v) { return (v + 15u) & ~15u; }
 
 __host__ __device__ inline LdsLayout lds_layout(int N, int Z, int waves, int cpw, int C,
-                                                int otile_ld)
+                                                int otile_ld, int rs = kRecStride)
 {
     LdsLayout l;
     uint32_t o = align16((uint32_t)N * 12u * 4u);
     l.z = o;
     o = align16(o + (uint32_t)Z * 4u);
     l.w = o;
-    o = align16(o + (uint32_t)waves * cpw * kRecStride * 16u);
+    o = align16(o + (uint32_t)waves * cpw * rs * 16u);
     l.off = o;
-    o = align16(o + (uint32_t)waves * cpw * kRecStride * 4u);
+    o = align16(o + (uint32_t)waves * cpw * rs * 4u);
     l.otile = o;
     o = align16(o + (uint32_t)C * otile_ld * 4u);
     l.total = o;
@@ -152,6 +153,7 @@ sample_vt_fwd(const Params p)
     float *s_tile = reinterpret_cast<float *>(smem + p.lds_otile);
 
     const int cpw = p.cpw;
+    const int RS = p.rec_stride;
     const int tid = threadIdx.x;
     const int nthreads = blockDim.x;  // waves * 64
     const int wave = tid / kWave;
@@ -217,8 +219,8 @@ sample_vt_fwd(const Params p)
         __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p.feat), (short)0,
                                           (int)p.feat_bytes, 0x00020000);
 
-    float4 *wl = s_w + (size_t)wave * cpw * kRecStride;
-    uint32_t *ol = s_off + (size_t)wave * cpw * kRecStride;
+    float4 *wl = s_w + (size_t)wave * cpw * RS;
+    uint32_t *ol = s_off + (size_t)wave * cpw * RS;
     const int wcells = p.rounds * cpw;
     const int q_wave = q_tile + wave * wcells;
     const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
@@ -273,7 +275,7 @@ sample_vt_fwd(const Params p)
                     const int den = __popcll((mask >> zshift) & nmask);
                     const int pos = __builtin_amdgcn_mbcnt_hi(
                         (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    wl[m * kRecStride + pos] =
+                    wl[m * RS + pos] =
                         make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
                 }
                 const int cnt = __popcll(mask);
@@ -298,7 +300,7 @@ sample_vt_fwd(const Params p)
                     pm = ge ? pf : pm;
                 }
                 if (idx < total) {
-                    const int slotk = m * kRecStride + (idx - pm);
+                    const int slotk = m * RS + (idx - pm);
                     const float4 pr = wl[slotk];
                     const float u = pr.x, v = pr.y;
                     const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
@@ -338,8 +340,8 @@ sample_vt_fwd(const Params p)
             for (int m = 0; m < ncell; ++m) {
                 const int c = __builtin_amdgcn_readlane(cnt_lane, m);
                 if (lane >= c && lane < maxpad) {
-                    wl[m * kRecStride + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                    ol[m * kRecStride + lane] = kNoTap;
+                    wl[m * RS + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    ol[m * RS + lane] = kNoTap;
                 }
             }
             wave_lds_sync();
@@ -348,8 +350,8 @@ sample_vt_fwd(const Params p)
             // kUnroll samples per iteration keep 4*kUnroll tap loads in
             // flight per lane.
             if (g_active) {
-                const float4 *wv = wl + m_lds * kRecStride;
-                const uint32_t *ov = ol + m_lds * kRecStride;
+                const float4 *wv = wl + m_lds * RS;
+                const uint32_t *ov = ol + m_lds * RS;
                 for (int k = 0; k < maxpad; k += kUnroll) {
                     float4 w[kUnroll];
                     uint32_t base[kUnroll];
@@ -1087,11 +1089,18 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     if ((cpw <= 2 || vpl >= 2) &&
         (uint64_t)f->B * (uint64_t)s->X * (uint64_t)s->Y <= (uint64_t)waves * cpw * kOneRoundTilesMax)
         rounds = 1;
+    // heights per projection pass; a cell's list holds one pass's valid
+    // samples (at most zc N <= 64), padded to whole gather iterations
+    int zc = f->N > 0 ? kWave / f->N : 1;
+    if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
+    if (zc < 1) zc = 1;
+    const int rec_cap = (zc * (f->N > 0 ? f->N : 1) + kUnroll - 1) / kUnroll * kUnroll;
+    const int rs = rec_cap | 1;
     auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
-    LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
+    LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds), rs);
     while (lay.total > kLdsBudget && rounds > 1) {
         --rounds;
-        lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds));
+        lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds), rs);
     }
     if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
     // a wavefront's cells fit its lanes (centre precompute) and a tile fits
@@ -1128,10 +1137,9 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.cpw = cpw;
     p.rcp_n = 1.0f / (float)(f->N > 0 ? f->N : 1);
     p.rcp_lpc = 1.0f / (float)lpc;
-    int zc = f->N > 0 ? kWave / f->N : 1;
-    if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
-    p.zc = zc < 1 ? 1 : zc;
+    p.zc = zc;
     p.otile_ld = otile_ld;
+    p.rec_stride = rs;
     p.lds_z = lay.z;
     p.lds_w = lay.w;
     p.lds_off = lay.off;
