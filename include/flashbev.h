@@ -28,6 +28,9 @@
  * Thread safety: the library keeps no state; calls are asynchronous on the
  * given stream and may be issued from several threads.  It never allocates
  * device or host memory, never prints and never aborts.
+ *
+ * Device: kernels run on the calling thread's current HIP device, which must
+ * hold every buffer of the call and the stream.
  */
 #ifndef FLASHBEV_H
 #define FLASHBEV_H

@@ -43,6 +43,8 @@
  *
  * Thread safety: no state; calls are asynchronous on the given stream and
  * may come from several threads.  No allocation, no printing, no abort.
+ * Kernels run on the calling thread's current HIP device, which must hold
+ * every buffer of the call and the stream.
  */
 #ifndef FLASHSCA_H
 #define FLASHSCA_H

@@ -213,10 +213,12 @@ def sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int
     z = _z_array(z_bins)
     f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
                         grid, z, reduce)
-    s = _stream_handle(stream, features.device)
-    rc = _lib().flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
-                                   ctypes.byref(g), ctypes.byref(zb),
-                                   ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
+    dev = _one_device(features, lidar2img, out)
+    s = _stream_handle(stream, dev)
+    with _on_device(dev):
+        rc = _lib().flashbev_sample_vt(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
+                                       ctypes.byref(g), ctypes.byref(zb),
+                                       ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
     if rc != 0:
         raise FlashBevError(rc)
     return out
@@ -229,7 +231,29 @@ def _stream_handle(stream, device):
         return torch.cuda.current_stream(device).cuda_stream
     if isinstance(stream, int):
         return stream
+    if stream.device != device:
+        raise ValueError(f"stream is on {stream.device}, the tensors on {device}")
     return stream.cuda_stream
+
+
+def _one_device(*tensors):
+    """The CUDA device the given tensors (None entries skipped) share."""
+    devs = {t.device for t in tensors if t is not None}
+    if len(devs) != 1:
+        raise ValueError("all tensors of a call must be on one CUDA device, got "
+                         + ", ".join(sorted(str(d) for d in devs)))
+    return devs.pop()
+
+
+def _on_device(device):
+    """Makes ``device`` current around a C call: the entry points launch on the
+    calling thread's current device."""
+    import contextlib
+    import torch
+
+    if torch.cuda.current_device() == device.index:
+        return contextlib.nullcontext()
+    return torch.cuda.device(device)
 
 
 def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int],
@@ -268,12 +292,13 @@ def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple
                           torch.bfloat16: "bf16"}[features_dtype]
     z = _z_array(z_bins)
     f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
-    s = _stream_handle(stream, grad_out.device)
-    rc = _lib().flashbev_sample_vt_backward(ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()),
-                                            ctypes.byref(g), ctypes.byref(zb),
-                                            ctypes.c_void_p(grad_out.data_ptr()),
-                                            ctypes.c_void_p(grad_features.data_ptr()),
-                                            ctypes.c_void_p(s))
+    dev = _one_device(grad_out, lidar2img, grad_features)
+    s = _stream_handle(stream, dev)
+    with _on_device(dev):
+        rc = _lib().flashbev_sample_vt_backward(
+            ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
+            ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(s))
     if rc != 0:
         raise FlashBevError(rc, "flashbev_sample_vt_backward")
     return grad_features
@@ -351,14 +376,22 @@ class _Prepared:
     the call again with no Python-side allocation.  It keeps the tensors and
     structures it refers to alive."""
 
-    def __init__(self, fn, args, keep, what):
+    def __init__(self, fn, args, keep, what, device):
+        import torch
+
         self._fn = fn
         self._args = args
         self._keep = keep
         self._what = what
+        self._dev = device.index
+        self._cuda = torch.cuda
 
     def __call__(self) -> None:
-        rc = self._fn(*self._args)
+        if self._cuda.current_device() == self._dev:
+            rc = self._fn(*self._args)
+        else:
+            with self._cuda.device(self._dev):
+                rc = self._fn(*self._args)
         if rc != 0:
             raise FlashBevError(rc, self._what)
 
@@ -378,11 +411,12 @@ def prepare_sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw, out,
     z = _z_array(z_bins)
     f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
                         grid, z, reduce)
-    s = _stream_handle(stream, features.device)
+    dev = _one_device(features, lidar2img, out)
+    s = _stream_handle(stream, dev)
     args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
             ctypes.byref(zb), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
     return _Prepared(_lib().flashbev_sample_vt, args,
-                     (features, lidar2img, out, z, f, g, zb), "flashbev_sample_vt")
+                     (features, lidar2img, out, z, f, g, zb), "flashbev_sample_vt", dev)
 
 
 def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw,
@@ -402,13 +436,14 @@ def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_h
                           torch.bfloat16: "bf16"}[features_dtype]
     z = _z_array(z_bins)
     f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
-    s = _stream_handle(stream, grad_out.device)
+    dev = _one_device(grad_out, lidar2img, grad_features)
+    s = _stream_handle(stream, dev)
     args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
             ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
             ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(s))
     return _Prepared(_lib().flashbev_sample_vt_backward, args,
                      (grad_out, lidar2img, grad_features, z, f, g, zb),
-                     "flashbev_sample_vt_backward")
+                     "flashbev_sample_vt_backward", dev)
 
 
 # ---------------------------------------------------------------------------
@@ -488,12 +523,14 @@ def sca_forward(value, lidar2img, anchors, grid: BevGrid, img_hw: Tuple[int, int
     z = _z_array(anchors)
     v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
                             img_hw, grid, z, reduce)
-    s = _stream_handle(stream, value.device)
-    rc = _lib().flashsca_forward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
-                                 ctypes.byref(g), ctypes.byref(zb), P,
-                                 ctypes.c_void_p(offsets.data_ptr()),
-                                 ctypes.c_void_p(logits.data_ptr()),
-                                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
+    dev = _one_device(value, lidar2img, offsets, logits, out)
+    s = _stream_handle(stream, dev)
+    with _on_device(dev):
+        rc = _lib().flashsca_forward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
+                                     ctypes.byref(g), ctypes.byref(zb), P,
+                                     ctypes.c_void_p(offsets.data_ptr()),
+                                     ctypes.c_void_p(logits.data_ptr()),
+                                     ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(s))
     if rc != 0:
         raise FlashBevError(rc, "flashsca_forward")
     return out
@@ -548,13 +585,15 @@ def prepare_sca_forward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels
     z = _z_array(anchors)
     v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
                             img_hw, grid, z, reduce)
-    s = _stream_handle(stream, value.device)
+    dev = _one_device(value, lidar2img, offsets, logits, out)
+    s = _stream_handle(stream, dev)
     args = (ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
             ctypes.byref(zb), ctypes.c_int32(P), ctypes.c_void_p(offsets.data_ptr()),
             ctypes.c_void_p(logits.data_ptr()), ctypes.c_void_p(out.data_ptr()),
             ctypes.c_void_p(s))
     return _Prepared(_lib().flashsca_forward, args,
-                     (value, lidar2img, offsets, logits, out, z, v, g, zb), "flashsca_forward")
+                     (value, lidar2img, offsets, logits, out, z, v, g, zb), "flashsca_forward",
+                     dev)
 
 
 def _sca_bwd_outputs(value, Q, heads, L, P, grad_value, grad_offsets, grad_logits, want):
@@ -598,14 +637,17 @@ def sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, levels, heads
     z = _z_array(anchors)
     v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
                             img_hw, grid, z, reduce)
-    s = _stream_handle(stream, value.device)
+    dev = _one_device(value, lidar2img, offsets, logits, grad_out, *outs.values())
+    s = _stream_handle(stream, dev)
     ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
-    rc = _lib().flashsca_backward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
-                                  ctypes.byref(g), ctypes.byref(zb), P,
-                                  ctypes.c_void_p(offsets.data_ptr()),
-                                  ctypes.c_void_p(logits.data_ptr()),
-                                  ctypes.c_void_p(grad_out.data_ptr()), ptr(outs["value"]),
-                                  ptr(outs["offsets"]), ptr(outs["logits"]), ctypes.c_void_p(s))
+    with _on_device(dev):
+        rc = _lib().flashsca_backward(ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()),
+                                      ctypes.byref(g), ctypes.byref(zb), P,
+                                      ctypes.c_void_p(offsets.data_ptr()),
+                                      ctypes.c_void_p(logits.data_ptr()),
+                                      ctypes.c_void_p(grad_out.data_ptr()), ptr(outs["value"]),
+                                      ptr(outs["offsets"]), ptr(outs["logits"]),
+                                      ctypes.c_void_p(s))
     if rc != 0:
         raise FlashBevError(rc, "flashsca_backward")
     return outs
@@ -622,7 +664,8 @@ def prepare_sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, level
     z = _z_array(anchors)
     v, g, zb = _sca_structs(value.shape, _dtype_code(value), value.data_ptr(), heads, levels,
                             img_hw, grid, z, reduce)
-    s = _stream_handle(stream, value.device)
+    dev = _one_device(value, lidar2img, offsets, logits, grad_out, *outs.values())
+    s = _stream_handle(stream, dev)
     ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
     args = (ctypes.byref(v), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
             ctypes.byref(zb), ctypes.c_int32(P), ctypes.c_void_p(offsets.data_ptr()),
@@ -630,4 +673,4 @@ def prepare_sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, level
             ptr(outs["value"]), ptr(outs["offsets"]), ptr(outs["logits"]), ctypes.c_void_p(s))
     return _Prepared(_lib().flashsca_backward, args,
                      (value, lidar2img, offsets, logits, grad_out, outs, z, v, g, zb),
-                     "flashsca_backward")
+                     "flashsca_backward", dev)

@@ -1470,9 +1470,15 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
     uint64_t blocks = (pl.gfeat_elems / 4 + 255) / 256;
     if (blocks < 1) blocks = 1;
     if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(zero_fill, dim3((unsigned)blocks), dim3(256), 0, st, grad_features,
-                       pl.gfeat_elems);
-    if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
+    {
+        // the launch's own status (hipGetLastError could report an earlier call's)
+        float *dst = grad_features;
+        uint64_t n = pl.gfeat_elems;
+        void *fargs[] = {&dst, &n};
+        if (hipLaunchKernel(reinterpret_cast<const void *>(zero_fill), dim3((unsigned)blocks),
+                            dim3(256), fargs, 0, st) != hipSuccess)
+            return FLASHBEV_ERR_HIP;
+    }
     if (pl.workgroups == 0) return FLASHBEV_OK;
     void *args[] = {&pl.prm};
     const void *fn = reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled));

@@ -976,9 +976,13 @@ extern "C" int flashsca_backward(const flashsca_value *value, const float *lidar
     if (grad_value && pl.value_elems > 0) {
         uint64_t blocks = (pl.value_elems + 255) / 256;
         if (blocks > 8192) blocks = 8192;
-        hipLaunchKernelGGL(sca_zero_fill, dim3((unsigned)blocks), dim3(256), 0, st, grad_value,
-                           pl.value_elems);
-        if (hipGetLastError() != hipSuccess) return FLASHBEV_ERR_HIP;
+        // the launch's own status (hipGetLastError could report an earlier call's)
+        float *dst = grad_value;
+        uint64_t n = pl.value_elems;
+        void *fargs[] = {&dst, &n};
+        if (hipLaunchKernel(reinterpret_cast<const void *>(sca_zero_fill), dim3((unsigned)blocks),
+                            dim3(256), fargs, 0, st) != hipSuccess)
+            return FLASHBEV_ERR_HIP;
     }
     if (pl.empty) return FLASHBEV_OK;
     const ScaKernelFn fn = pick_sca(value->dtype, pl.lw, true);

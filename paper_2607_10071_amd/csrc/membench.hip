@@ -97,6 +97,14 @@ atomic_kernel(float *buf, uint32_t nrows, int32_t iters)
 
 }  // namespace
 
+// Launch status of this launch alone (hipGetLastError could report an
+// earlier call's error).
+static int launch_status(const void *fn, int32_t workgroups, void **args, void *stream)
+{
+    return hipLaunchKernel(fn, dim3((unsigned)workgroups), dim3(kThreads), args, 0,
+                           (hipStream_t)stream) == hipSuccess ? 0 : -4;
+}
+
 extern "C" {
 
 int flashbev_membench_gather(const void *buf, uint64_t buf_bytes, int32_t row_bytes,
@@ -114,10 +122,12 @@ int flashbev_membench_gather(const void *buf, uint64_t buf_bytes, int32_t row_by
     const int lpc = row_bytes / 16;
     int cpw = 64 / lpc;
     if (cpw > 8) cpw = 8;
-    hipLaunchKernelGGL(gather_kernel, dim3(workgroups), dim3(kThreads), 0, (hipStream_t)stream,
-                       buf, (uint32_t)nrows, (uint32_t)row_bytes, (uint32_t)row_pitch, iters, lpc,
-                       cpw, sink);
-    return hipGetLastError() == hipSuccess ? 0 : -4;
+    const void *a0 = buf;
+    uint32_t a1 = (uint32_t)nrows, a2 = (uint32_t)row_bytes, a3 = (uint32_t)row_pitch;
+    int32_t a4 = iters, a5 = lpc, a6 = cpw;
+    float *a7 = sink;
+    void *args[] = {&a0, &a1, &a2, &a3, &a4, &a5, &a6, &a7};
+    return launch_status(reinterpret_cast<const void *>(gather_kernel), workgroups, args, stream);
 }
 
 int flashbev_membench_stream(const void *buf, uint64_t bytes, int32_t workgroups, float *sink,
@@ -125,9 +135,11 @@ int flashbev_membench_stream(const void *buf, uint64_t bytes, int32_t workgroups
 {
     if (!buf || !sink) return -1;
     if (bytes == 0 || bytes % (16u * kThreads) || workgroups < 1 || ((uintptr_t)buf % 16)) return -2;
-    hipLaunchKernelGGL(stream_kernel, dim3(workgroups), dim3(kThreads), 0, (hipStream_t)stream,
-                       (const uint4 *)buf, bytes / 16, sink);
-    return hipGetLastError() == hipSuccess ? 0 : -4;
+    const uint4 *a0 = (const uint4 *)buf;
+    uint64_t a1 = bytes / 16;
+    float *a2 = sink;
+    void *args[] = {&a0, &a1, &a2};
+    return launch_status(reinterpret_cast<const void *>(stream_kernel), workgroups, args, stream);
 }
 
 }  // extern "C"
@@ -138,7 +150,9 @@ extern "C" int flashbev_membench_atomic(float *buf, uint64_t buf_floats, int32_t
     if (!buf) return -1;
     if (buf_floats < 64 || iters < 1 || workgroups < 1 || ((uintptr_t)buf % 4)) return -2;
     if (buf_floats / 64 > 0xFFFFFFFFull) return -3;
-    hipLaunchKernelGGL(atomic_kernel, dim3(workgroups), dim3(kThreads), 0, (hipStream_t)stream, buf,
-                       (uint32_t)(buf_floats / 64), iters);
-    return hipGetLastError() == hipSuccess ? 0 : -4;
+    float *a0 = buf;
+    uint32_t a1 = (uint32_t)(buf_floats / 64);
+    int32_t a2 = iters;
+    void *args[] = {&a0, &a1, &a2};
+    return launch_status(reinterpret_cast<const void *>(atomic_kernel), workgroups, args, stream);
 }

@@ -212,6 +212,16 @@ def test_binding_rejects_host_tensors():
                                       "f32", f)
 
 
+def test_binding_requires_one_device_per_call():
+    import torch
+    a, b = torch.zeros(2), torch.zeros(2, device="meta")
+    assert fb._one_device(a, None, torch.ones(3)) == torch.device("cpu")
+    with pytest.raises(ValueError, match="one CUDA device"):
+        fb._one_device(a, b)
+    with pytest.raises(ValueError):
+        fb._one_device(None)
+
+
 def test_backward_launch_info_geometry():
     """Tiled mode where pixel ids fit 20 bits and a wavefront holds at least
     two cells; LDS within the tiled budget; direct mode otherwise."""
