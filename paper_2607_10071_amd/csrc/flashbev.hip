@@ -73,6 +73,11 @@ constexpr uint64_t kFeatBytesMax = 0x7FFFFFFFull;
 constexpr uint32_t kLdsBudget = 64u * 1024u;   // dynamic LDS per workgroup
 constexpr uint64_t kOneRoundTilesMax = 262144;  // grids up to this many one-round tiles
 constexpr uint32_t kLdsBudgetBwd = 80u * 1024u;  // tiled backward: two workgroups per CU
+constexpr int kBwdTileWaves = 8;                 // tiled backward: wavefronts per workgroup
+constexpr int kBwdThreadsMax = kWave * kBwdTileWaves;
+// a term-list entry packs (wavefront << 14) | (record index << 2) | tap
+static_assert(kCpwMax * kRecStride < (1 << 12), "record index must fit 12 bits");
+static_assert(kBwdTileWaves <= (1 << 18), "wavefront index must fit the entry");
 
 struct Params {
     const void *feat;
@@ -445,8 +450,16 @@ sample_vt_fwd(const Params p)
 // FMAs.  At the end each row goes to the gradient with one global atomic per
 // channel.  Taps that find the table full go straight to global atomics.  The
 // direct mode (no table) serves shapes whose rows or pixel ids do not fit.
+//
+// Occupancy decides the tiled mode's speed (measured on MI355X: one 4-wave
+// workgroup per CU runs at half the speed of two).  So a workgroup has 8
+// wavefronts and 80 KiB of LDS (two per CU, 16 wavefronts), and a height
+// pass covers half the heights a wavefront could project at once.  That
+// keeps the per-pass records and term list small and leaves room for rows.
+// The rows then need only hold the pixels of about one pass: when the rows in
+// use plus those the last pass claimed exceed the tile's rows, the tile adds
+// its rows to the gradient and starts again with an empty table.
 constexpr uint32_t kSlotNone = 0xFFFFu;   // tap not in the tile's table
-constexpr uint32_t kPixNone = 0xFFFFFFFFu; // LDS row claimed but not used
 constexpr int kKeyBits = 20;              // pixel ids (plus one) per batch element < 2^20
 constexpr uint32_t kKeyMask = (1u << kKeyBits) - 1u;
 constexpr int kSlotMax = (1 << (32 - kKeyBits)) - 1;  // 4095 rows per tile
@@ -471,6 +484,7 @@ struct BwdParams {
     float rcp_n, rcp_lpc;
     int32_t zc;
     int32_t gtile_ld;        // row pitch (floats) of the LDS output-gradient tile, odd
+    int32_t rec_stride;      // records per cell list: one pass's samples, odd
     uint32_t lds_z, lds_w, lds_off, lds_gtile;
     // tiled mode
     int32_t tx, ty;          // tile rows (along x) and columns (along y)
@@ -567,7 +581,7 @@ __device__ __forceinline__ uint32_t tile_row_of(const uint32_t *tbl, uint32_t h)
 }
 
 template <int KPL, bool TILED>
-__global__ void __launch_bounds__(kThreadsMax)
+__global__ void __launch_bounds__(kBwdThreadsMax)
 sample_vt_bwd(const BwdParams p)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -594,6 +608,7 @@ sample_vt_bwd(const BwdParams p)
     const int N = p.N;
     const int C = p.C;
     const int T = p.tile_cells;
+    const int RS = p.rec_stride;
 
     // XCD-aware tile order: the k-th workgroup on XCD x takes tile
     // (k / S) * 8S + x * S + k % S, stripes of S consecutive tiles that
@@ -673,9 +688,9 @@ sample_vt_bwd(const BwdParams p)
     const bool in_group = m_g < cpw;
     const int m_lds = in_group ? m_g : 0;
 
-    float4 *wl = s_w + (size_t)wave * cpw * kRecStride;
-    uint32_t *ol = s_off + (size_t)wave * cpw * kRecStride;
-    uint2 *sl = s_slot + (size_t)wave * cpw * kRecStride;
+    float4 *wl = s_w + (size_t)wave * cpw * RS;
+    uint32_t *ol = s_off + (size_t)wave * cpw * RS;
+    uint2 *sl = s_slot + (size_t)wave * cpw * RS;
     const int wcells = p.rounds * cpw;
     const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
     const uint32_t pix0 = cam0 * (uint32_t)p.H * (uint32_t)p.W;
@@ -711,6 +726,9 @@ sample_vt_bwd(const BwdParams p)
         }
 
         for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
+            // rows in use as this pass starts (the last pass ended with a barrier)
+            uint32_t used0 = 0;
+            if constexpr (TILED) used0 = s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap;
             // ---- projection, mask and compaction (as in the forward)
             const int zi = z0 + zl;
             const bool l_ok = p_role && zi < p.Z;
@@ -723,7 +741,7 @@ sample_vt_bwd(const BwdParams p)
                 if ((cvmask >> (r * cpw + m)) & 1ull)
                     cnt = bwd_project_cell(p, mr, t2u, t2v, t2d, bcast(xs, r * cpw + m),
                                            bcast(ys, r * cpw + m), l_ok, zshift, nmask, n_p,
-                                           wl + m * kRecStride);
+                                           wl + m * RS);
                 cnt_lane = lane == m ? cnt : cnt_lane;
                 pre_lane = lane == m ? total : pre_lane;
                 total += cnt;
@@ -743,7 +761,7 @@ sample_vt_bwd(const BwdParams p)
                     pm = ge ? pf : pm;
                 }
                 if (idx < total) {
-                    const int slotk = m * kRecStride + (idx - pm);
+                    const int slotk = m * RS + (idx - pm);
                     const float4 pr = wl[slotk];
                     const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
                     int xa, ya;
@@ -793,7 +811,7 @@ sample_vt_bwd(const BwdParams p)
                         pm = ge ? pf : pm;
                     }
                     if (idx < total) {
-                        const uint2 sh = sl[m * kRecStride + (idx - pm)];
+                        const uint2 sh = sl[m * RS + (idx - pm)];
                         const uint32_t hh[4] = {sh.x & 0xFFFFu, sh.x >> 16, sh.y & 0xFFFFu, sh.y >> 16};
                         bool none = false;
 #pragma unroll
@@ -841,7 +859,7 @@ sample_vt_bwd(const BwdParams p)
                         pm = ge ? pf : pm;
                     }
                     if (idx < total) {
-                        const int slotk = m * kRecStride + (idx - pm);
+                        const int slotk = m * RS + (idx - pm);
                         const uint2 sh = sl[slotk];
                         const uint32_t rr[4] = {tile_row_of(s_tbl, sh.x & 0xFFFFu), tile_row_of(s_tbl, sh.x >> 16),
                                                 tile_row_of(s_tbl, sh.y & 0xFFFFu), tile_row_of(s_tbl, sh.y >> 16)};
@@ -861,9 +879,9 @@ sample_vt_bwd(const BwdParams p)
             // mode only taps without an LDS row (table full) come here.
             const int mycnt = __shfl(cnt_lane, m_lds);
             if (g_active && (!TILED || s_cnt[1] != 0u)) {
-                const float4 *wv = wl + m_lds * kRecStride;
-                const uint32_t *ov = ol + m_lds * kRecStride;
-                const uint2 *sv = sl + m_lds * kRecStride;
+                const float4 *wv = wl + m_lds * RS;
+                const uint32_t *ov = ol + m_lds * RS;
+                const uint2 *sv = sl + m_lds * RS;
                 for (int k = 0; k < mycnt; ++k) {
                     const float4 w = wv[k];
                     const float wt[4] = {w.x, w.y, w.z, w.w};
@@ -895,7 +913,7 @@ sample_vt_bwd(const BwdParams p)
                 __syncthreads();
                 const int nr = (int)(s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap);
                 const float *s_wf = reinterpret_cast<const float *>(s_w);
-                const int wstride = cpw * kRecStride;
+                const int wstride = cpw * RS;
                 const int nwaves = nthreads / kWave;
                 for (int row = wave; row < nr; row += nwaves) {
                     const uint32_t e0 = s_rbase[row], n = s_rbase[row + 1] - e0;
@@ -908,7 +926,7 @@ sample_vt_bwd(const BwdParams p)
                             const uint32_t ent = s_list[e0 + k0 + lane];
                             const uint32_t we = ent >> 14, sk = (ent >> 2) & 0xFFFu, t = ent & 3u;
                             wi = s_wf[((we * wstride) + sk) * 4u + t];
-                            coli = we * wcells + r * cpw + sk / kRecStride;
+                            coli = we * wcells + r * cpw + sk / RS;
                         }
                         for (int c0 = 0; c0 < C; c0 += kWave) {
                             const int c = c0 + lane;
@@ -925,6 +943,24 @@ sample_vt_bwd(const BwdParams p)
                     }
                 }
                 __syncthreads();
+                // ---- if the next pass may not fit (it may claim as many rows
+                // as this one did), add the rows to the gradient now and start
+                // again with an empty table
+                const uint32_t used = s_cnt[0] < (uint32_t)p.cap ? s_cnt[0] : (uint32_t)p.cap;
+                if (z0 + p.zc < p.Z && used + (used - used0) > (uint32_t)p.cap) {
+                    const int n_el = (int)used * C;
+                    for (int t = tid; t < n_el; t += nthreads) {
+                        const int row = div_small(t, C, p.rcp_c);
+                        const float v = s_acc[t];
+                        if (v != 0.0f)
+                            unsafeAtomicAdd(p.gfeat + (size_t)(pix0 + s_spix[row]) * C + (t - row * C), v);
+                        s_acc[t] = 0.0f;
+                    }
+                    for (uint32_t t = tid; t <= p.tbl_mask; t += nthreads) s_tbl[t] = 0u;
+                    __syncthreads();
+                    if (tid == 0) { s_cnt[0] = 0u; s_cnt[1] = 0u; }
+                    __syncthreads();
+                }
             } else {
                 wave_lds_sync();
             }
@@ -938,10 +974,9 @@ sample_vt_bwd(const BwdParams p)
         const int n_el = (int)used * C;
         for (int t = tid; t < n_el; t += nthreads) {
             const int row = div_small(t, C, p.rcp_c);
-            const uint32_t q = s_spix[row];
             const float v = s_acc[t];
-            if (q != kPixNone && v != 0.0f)
-                unsafeAtomicAdd(p.gfeat + (size_t)(pix0 + q) * C + (t - row * C), v);
+            if (v != 0.0f)
+                unsafeAtomicAdd(p.gfeat + (size_t)(pix0 + s_spix[row]) * C + (t - row * C), v);
         }
     }
 }
@@ -1249,18 +1284,20 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     if (rounds * cpw > kWave) return FLASHBEV_ERR_UNSUPPORTED;
     int tile_cells = waves * rounds * cpw;
 
-    // tiled mode: 4 wavefronts of one group each on a 2-D tile with four
-    // cells per tile row; LDS holds the per-wave records, the row table, the
-    // pass's sorted term list (sized for the pass's largest possible number
-    // of terms) and as many per-pixel rows as the budget leaves
+    // tiled mode: kBwdTileWaves wavefronts of one group each on a 2-D tile
+    // with four cells per tile row; LDS holds the per-wave records, the row
+    // table, the pass's sorted term list (sized for the pass's largest
+    // possible number of terms) and as many per-pixel rows as the budget
+    // leaves
     const uint64_t npix = (uint64_t)f->N * f->H * f->W;
     bool tiled = false;
     int t_waves = 0, t_tx = 0, t_ty = 0, t_cap = 0, t_zc = 0;
     uint32_t t_mask = 0, l_slot = 0, l_tbl = 0, l_spix = 0, l_acc = 0, l_cnt = 0, l_total = 0;
     uint32_t l_rcnt = 0, l_rbase = 0, l_rfill = 0, l_list = 0;
     int t_pitch = 0;
+    int t_rs = kRecStride;
     if (npix + 1 < (1u << kKeyBits) && cpw >= 2 && f->N > 0) {
-        t_waves = kWavesMax;
+        t_waves = kBwdTileWaves;
         const int T = t_waves * cpw;
         t_ty = (T % 4 == 0) ? 4 : T;
         t_tx = T / t_ty;
@@ -1268,10 +1305,14 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
         int zc_max = kWave / f->N;
         if (zc_max > zb->Z && zb->Z > 0) zc_max = zb->Z;
         if (zc_max < 1) zc_max = 1;
-        for (int zc_try = zc_max; zc_try >= 1 && !tiled; zc_try = zc_try > 1 ? zc_try / 2 : 0) {
-            const LdsLayout base = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
+        // passes of half the heights a wavefront can project at once, fewer
+        // where the LDS needs it; records sized to one pass
+        for (int zc_try = zc_max > 1 ? zc_max / 2 : 1; zc_try >= 1 && !tiled;
+             zc_try = zc_try > 1 ? zc_try / 2 : 0) {
+            const int rs_try = ((zc_try * f->N + 1) / 2 * 2) | 1;
+            const LdsLayout base = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch, rs_try);
             uint32_t o = base.total;
-            const uint32_t lslot = o; o = align16(o + (uint32_t)t_waves * cpw * kRecStride * 8u);
+            const uint32_t lslot = o; o = align16(o + (uint32_t)t_waves * cpw * rs_try * 8u);
             const uint32_t lcnt = o; o = align16(o + 16u);
             const uint32_t entries_max = 4u * (uint32_t)t_waves * cpw * (uint32_t)(zc_try * f->N);
             const uint32_t llist = o; o = align16(o + entries_max * 4u);
@@ -1311,6 +1352,7 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
                 t_cap = cap;
                 t_mask = entries - 1u;
                 t_zc = zc_try;
+                t_rs = rs_try;
                 tiled = true;
             }
         }
@@ -1364,7 +1406,8 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
     p.zc = tiled ? t_zc : (zc < 1 ? 1 : zc);
     p.gtile_ld = tiled ? t_pitch : pitch(rounds);
-    if (tiled) lay = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch);
+    if (tiled) lay = lds_layout(f->N, zb->Z, t_waves, cpw, f->C, t_pitch, t_rs);
+    p.rec_stride = tiled ? t_rs : kRecStride;
     p.lds_z = lay.z;
     p.lds_w = lay.w;
     p.lds_off = lay.off;

@@ -224,7 +224,8 @@ def test_binding_requires_one_device_per_call():
 
 def test_backward_launch_info_geometry():
     """Tiled mode where pixel ids fit 20 bits and a wavefront holds at least
-    two cells; LDS within the tiled budget; direct mode otherwise."""
+    two cells: 8-wavefront workgroups within the tiled LDS budget (two per
+    CU); direct mode otherwise."""
     grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
     for dtype, C, tiled in (("f32", 80, True), ("bf16", 128, True), ("f16", 64, True),
                             ("f32", 32, True), ("f32", 1, True), ("f32", 1024, False),
@@ -234,10 +235,10 @@ def test_backward_launch_info_geometry():
         assert info["lanes_per_cell"] == lpc, (C, info)
         assert (info["rows_per_tile"] > 0) == tiled, (C, info)
         if tiled:
-            assert info["rows_per_tile"] >= 16 and info["threads"] == 256
+            assert info["rows_per_tile"] >= 16 and info["threads"] == 512
             assert info["lds_bytes"] <= 80 * 1024
             cpw = min(8, 64 // lpc)
-            T = 4 * cpw
+            T = 8 * cpw
             ty = 4 if T % 4 == 0 else T
             assert info["workgroups"] == math.ceil(200 / (T // ty)) * math.ceil(200 / ty)
         else:
