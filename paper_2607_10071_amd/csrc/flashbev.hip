@@ -928,18 +928,30 @@ sample_vt_bwd(const BwdParams p)
                             wi = s_wf[((we * wstride) + sk) * 4u + t];
                             coli = we * wcells + r * cpw + sk / RS;
                         }
-                        for (int c0 = 0; c0 < C; c0 += kWave) {
-                            const int c = c0 + lane;
-                            const float *gc = s_g + (c < C ? c : C - 1) * p.gtile_ld;
-                            float sum = 0.0f;
+                        // channels lane and lane + 64 (C <= 128 in the tiled mode):
+                        // each term's weight and column are read once for both
+                        const int ca = lane, cb = lane + kWave;
+                        const float *ga = s_g + (ca < C ? ca : C - 1) * p.gtile_ld;
+                        const float *gb = s_g + (cb < C ? cb : C - 1) * p.gtile_ld;
+                        float sa = 0.0f, sb = 0.0f;
+                        if (C > kWave) {
                             for (uint32_t k = 0; k < kn; ++k) {
                                 const float w = __builtin_bit_cast(
                                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
                                 const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
-                                sum = fmaf(w, gc[col], sum);
+                                sa = fmaf(w, ga[col], sa);
+                                sb = fmaf(w, gb[col], sb);
                             }
-                            if (c < C) s_acc[row * C + c] += sum;
+                        } else {
+                            for (uint32_t k = 0; k < kn; ++k) {
+                                const float w = __builtin_bit_cast(
+                                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
+                                const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
+                                sa = fmaf(w, ga[col], sa);
+                            }
                         }
+                        if (ca < C) s_acc[row * C + ca] += sa;
+                        if (cb < C) s_acc[row * C + cb] += sb;
                     }
                 }
                 __syncthreads();
@@ -1296,7 +1308,8 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     uint32_t l_rcnt = 0, l_rbase = 0, l_rfill = 0, l_list = 0;
     int t_pitch = 0;
     int t_rs = kRecStride;
-    if (npix + 1 < (1u << kKeyBits) && cpw >= 2 && f->N > 0) {
+    // (cpw >= 2 implies C <= 128: the row sums cover channels in two blocks of 64)
+    if (npix + 1 < (1u << kKeyBits) && cpw >= 2 && f->C <= 2 * kWave && f->N > 0) {
         t_waves = kBwdTileWaves;
         const int T = t_waves * cpw;
         t_ty = (T % 4 == 0) ? 4 : T;
