@@ -609,6 +609,7 @@ sample_vt_bwd(const BwdParams p)
     const int C = p.C;
     const int T = p.tile_cells;
     const int RS = p.rec_stride;
+    const float rcp_rs = 1.0f / (float)RS;  // record index -> cell without an integer divide
 
     // XCD-aware tile order: the k-th workgroup on XCD x takes tile
     // (k / S) * 8S + x * S + k % S, stripes of S consecutive tiles that
@@ -926,7 +927,7 @@ sample_vt_bwd(const BwdParams p)
                             const uint32_t ent = s_list[e0 + k0 + lane];
                             const uint32_t we = ent >> 14, sk = (ent >> 2) & 0xFFFu, t = ent & 3u;
                             wi = s_wf[((we * wstride) + sk) * 4u + t];
-                            coli = we * wcells + r * cpw + sk / RS;
+                            coli = we * wcells + r * cpw + div_small((int)sk, RS, rcp_rs);
                         }
                         // channels lane and lane + 64 (C <= 128 in the tiled mode):
                         // each term's weight and column are read once for both
