@@ -8,6 +8,11 @@ approximate reciprocal of den_z, the product with g), and float32 atomic
 addition of K terms in any order adds at most (K - 1) roundings of partial
 sums no larger than S.  Elements no term reaches must be exactly zero.
 All calls go through the C ABI via the thin binding.
+
+The full-size workloads cover every path of the tiled scatter: long_range's
+heavy tiles claim more distinct pixels in a pass than a tile has LDS rows
+(those taps go to global atomics), and the height sweep up to Z = 64 runs up
+to 16 passes per tile, so tiles flush their rows and start again mid-tile.
 """
 import numpy as np
 import pytest
