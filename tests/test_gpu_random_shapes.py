@@ -34,7 +34,7 @@ def _fbev_workload(seed):
         z_lo=-5.0, z_hi=float(r.uniform(0.0, 6.0)), Z=int(r.integers(1, 13)))
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(40))
 def test_forward_random_shapes(device, seed):
     import paper_2607_10071_amd as fb
     inst = synth.make_workload(_fbev_workload(seed))
@@ -42,7 +42,7 @@ def test_forward_random_shapes(device, seed):
     tp.check_instance(fb, inst, device, reduce, what=f"random forward {seed}")
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(40))
 def test_backward_random_shapes(device, seed):
     import paper_2607_10071_amd as fb
     wl = _fbev_workload(100 + seed)
@@ -69,7 +69,7 @@ def _sca_workload(seed):
         dy=2 * half / Y, offset_noise=float(r.uniform(0.0, 3.0)))
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(40))
 def test_sca_forward_random_shapes(device, seed):
     import paper_2607_10071_amd as fb
     inst = synth.make_sca_workload(_sca_workload(seed))
@@ -77,7 +77,7 @@ def test_sca_forward_random_shapes(device, seed):
     ts.check(fb, inst, device, reduce, what=f"random sca {seed}")
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(40))
 def test_sca_backward_random_shapes(device, seed):
     import paper_2607_10071_amd as fb
     inst = synth.make_sca_workload(_sca_workload(100 + seed))
