@@ -31,6 +31,11 @@
  *
  * Device: kernels run on the calling thread's current HIP device, which must
  * hold every buffer of the call and the stream.
+ *
+ * The one side effect beyond the stream: a launch that needs more than 64 KiB
+ * of LDS per workgroup (the backward's tiled mode) first raises that kernel's
+ * dynamic-LDS limit with hipFuncSetAttribute, a per-process setting that is
+ * idempotent and safe to repeat from several threads.
  */
 #ifndef FLASHBEV_H
 #define FLASHBEV_H

@@ -44,7 +44,10 @@
  * Thread safety: no state; calls are asynchronous on the given stream and
  * may come from several threads.  No allocation, no printing, no abort.
  * Kernels run on the calling thread's current HIP device, which must hold
- * every buffer of the call and the stream.
+ * every buffer of the call and the stream.  A launch that needs more than
+ * 64 KiB of LDS per workgroup (many points per head) first raises that
+ * kernel's dynamic-LDS limit with hipFuncSetAttribute, a per-process setting
+ * that is idempotent.
  */
 #ifndef FLASHSCA_H
 #define FLASHSCA_H
