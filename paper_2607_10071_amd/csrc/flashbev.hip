@@ -75,6 +75,7 @@ constexpr uint64_t kOneRoundTilesMax = 262144;  // grids up to this many one-rou
 constexpr uint32_t kLdsBudgetBwd = 80u * 1024u;  // tiled backward: two workgroups per CU
 constexpr int kBwdTileWaves = 8;                 // tiled backward: wavefronts per workgroup
 constexpr int kBwdThreadsMax = kWave * kBwdTileWaves;
+constexpr int kBwdTiledCMax = 512;               // tiled backward: widest rows (channels)
 // a term-list entry packs (wavefront << 14) | (record index << 2) | tap
 static_assert(kCpwMax * kRecStride < (1 << 12), "record index must fit 12 bits");
 static_assert(kBwdTileWaves <= (1 << 18), "wavefront index must fit the entry");
@@ -449,7 +450,8 @@ sample_vt_fwd(const Params p)
 // a fill), and one wavefront per row sums its terms into the row with plain
 // FMAs.  At the end each row goes to the gradient with one global atomic per
 // channel.  Taps that find the table full go straight to global atomics.  The
-// direct mode (no table) serves shapes whose rows or pixel ids do not fit.
+// direct mode (no table) serves shapes whose rows (more than 512 channels) or
+// pixel ids do not fit.
 //
 // Occupancy decides the tiled mode's speed (measured on MI355X: one 4-wave
 // workgroup per CU runs at half the speed of two).  So a workgroup has 8
@@ -580,7 +582,7 @@ __device__ __forceinline__ uint32_t tile_row_of(const uint32_t *tbl, uint32_t h)
     return r == kRowUnset ? kSlotNone : r;
 }
 
-template <int KPL, bool TILED>
+template <int KPL, bool TILED, bool WIDE>
 __global__ void __launch_bounds__(kBwdThreadsMax)
 sample_vt_bwd(const BwdParams p)
 {
@@ -929,30 +931,56 @@ sample_vt_bwd(const BwdParams p)
                             wi = s_wf[((we * wstride) + sk) * 4u + t];
                             coli = we * wcells + r * cpw + div_small((int)sk, RS, rcp_rs);
                         }
-                        // channels lane and lane + 64 (C <= 128 in the tiled mode):
-                        // each term's weight and column are read once for both
-                        const int ca = lane, cb = lane + kWave;
-                        const float *ga = s_g + (ca < C ? ca : C - 1) * p.gtile_ld;
-                        const float *gb = s_g + (cb < C ? cb : C - 1) * p.gtile_ld;
-                        float sa = 0.0f, sb = 0.0f;
-                        if (C > kWave) {
-                            for (uint32_t k = 0; k < kn; ++k) {
-                                const float w = __builtin_bit_cast(
-                                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
-                                const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
-                                sa = fmaf(w, ga[col], sa);
-                                sb = fmaf(w, gb[col], sb);
+                        if constexpr (!WIDE) {
+                            // channels lane and lane + 64 (C <= 128 in the tiled mode):
+                            // each term's weight and column are read once for both
+                            const int ca = lane, cb = lane + kWave;
+                            const float *ga = s_g + (ca < C ? ca : C - 1) * p.gtile_ld;
+                            const float *gb = s_g + (cb < C ? cb : C - 1) * p.gtile_ld;
+                            float sa = 0.0f, sb = 0.0f;
+                            if (C > kWave) {
+                                for (uint32_t k = 0; k < kn; ++k) {
+                                    const float w = __builtin_bit_cast(
+                                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
+                                    const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
+                                    sa = fmaf(w, ga[col], sa);
+                                    sb = fmaf(w, gb[col], sb);
+                                }
+                            } else {
+                                for (uint32_t k = 0; k < kn; ++k) {
+                                    const float w = __builtin_bit_cast(
+                                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
+                                    const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
+                                    sa = fmaf(w, ga[col], sa);
+                                }
                             }
+                            if (ca < C) s_acc[row * C + ca] += sa;
+                            if (cb < C) s_acc[row * C + cb] += sb;
                         } else {
+                            // wide rows (128 < C <= kBwdTiledCMax): channel blocks
+                            // b * 64 + lane for b < KPL, each term read once for all
+                            float sk[KPL];
+                            int gofs[KPL];
+#pragma unroll
+                            for (int b = 0; b < KPL; ++b) {
+                                sk[b] = 0.0f;
+                                const int c = b * kWave + lane;
+                                gofs[b] = (c < C ? c : C - 1) * p.gtile_ld;
+                            }
                             for (uint32_t k = 0; k < kn; ++k) {
                                 const float w = __builtin_bit_cast(
                                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wi), (int)k));
                                 const uint32_t col = (uint32_t)__builtin_amdgcn_readlane((int)coli, (int)k);
-                                sa = fmaf(w, ga[col], sa);
+#pragma unroll
+                                for (int b = 0; b < KPL; ++b)
+                                    if (b * kWave < C) sk[b] = fmaf(w, s_g[gofs[b] + (int)col], sk[b]);
+                            }
+#pragma unroll
+                            for (int b = 0; b < KPL; ++b) {
+                                const int c = b * kWave + lane;
+                                if (b * kWave < C && c < C) s_acc[row * C + c] += sk[b];
                             }
                         }
-                        if (ca < C) s_acc[row * C + ca] += sa;
-                        if (cb < C) s_acc[row * C + cb] += sb;
                     }
                 }
                 __syncthreads();
@@ -1214,6 +1242,7 @@ struct BwdPlan {
     size_t lds;
     int kpl;
     bool tiled;
+    bool wide;              // tiled with more than 128 channels
     uint64_t gfeat_elems;
 };
 
@@ -1223,15 +1252,22 @@ template <bool TILED>
 BwdKernelFn pick_bwd_kpl(int kpl)
 {
     switch (kpl) {
-    case 4: return sample_vt_bwd<4, TILED>;
-    case 8: return sample_vt_bwd<8, TILED>;
-    case 16: return sample_vt_bwd<16, TILED>;
-    default: return sample_vt_bwd<32, TILED>;
+    case 4: return sample_vt_bwd<4, TILED, false>;
+    case 8: return sample_vt_bwd<8, TILED, false>;
+    case 16: return sample_vt_bwd<16, TILED, false>;
+    default: return sample_vt_bwd<32, TILED, false>;
     }
 }
 
-BwdKernelFn pick_bwd(int kpl, bool tiled)
+// tiled mode with rows wider than 128 channels (KPL 4 or 8 there)
+BwdKernelFn pick_bwd_wide(int kpl)
 {
+    return kpl <= 4 ? sample_vt_bwd<4, true, true> : sample_vt_bwd<8, true, true>;
+}
+
+BwdKernelFn pick_bwd(int kpl, bool tiled, bool wide)
+{
+    if (wide) return pick_bwd_wide(kpl);
     return tiled ? pick_bwd_kpl<true>(kpl) : pick_bwd_kpl<false>(kpl);
 }
 
@@ -1309,8 +1345,8 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     uint32_t l_rcnt = 0, l_rbase = 0, l_rfill = 0, l_list = 0;
     int t_pitch = 0;
     int t_rs = kRecStride;
-    // (cpw >= 2 implies C <= 128: the row sums cover channels in two blocks of 64)
-    if (npix + 1 < (1u << kKeyBits) && cpw >= 2 && f->C <= 2 * kWave && f->N > 0) {
+    // rows up to kBwdTiledCMax channels (wider ones leave too few LDS rows)
+    if (npix + 1 < (1u << kKeyBits) && f->C <= kBwdTiledCMax && f->N > 0) {
         t_waves = kBwdTileWaves;
         const int T = t_waves * cpw;
         t_ty = (T % 4 == 0) ? 4 : T;
@@ -1434,6 +1470,8 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     pl->lds = tiled ? l_total : lay.total;
     pl->kpl = kpl;
     pl->tiled = tiled;
+    pl->wide = tiled && f->C > 2 * kWave;
+    if (pl->wide && kpl > 8) return FLASHBEV_ERR_UNSUPPORTED;
     pl->gfeat_elems = gelems;
     return FLASHBEV_OK;
 }
@@ -1538,7 +1576,7 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
     }
     if (pl.workgroups == 0) return FLASHBEV_OK;
     void *args[] = {&pl.prm};
-    const void *fn = reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled));
+    const void *fn = reinterpret_cast<const void *>(pick_bwd(pl.kpl, pl.tiled, pl.wide));
     if (pl.lds > 65536 &&
         hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds) != hipSuccess)
         return FLASHBEV_ERR_HIP;

@@ -223,12 +223,13 @@ def test_binding_requires_one_device_per_call():
 
 
 def test_backward_launch_info_geometry():
-    """Tiled mode where pixel ids fit 20 bits and a wavefront holds at least
-    two cells: 8-wavefront workgroups within the tiled LDS budget (two per
+    """Tiled mode where pixel ids fit 20 bits and rows have at most 512
+    channels: 8-wavefront workgroups within the tiled LDS budget (two per
     CU); direct mode otherwise."""
     grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
     for dtype, C, tiled in (("f32", 80, True), ("bf16", 128, True), ("f16", 64, True),
-                            ("f32", 32, True), ("f32", 1, True), ("f32", 1024, False),
+                            ("f32", 32, True), ("f32", 1, True), ("f32", 256, True),
+                            ("bf16", 512, True), ("f32", 513, False), ("f32", 1024, False),
                             ("bf16", 2048, False)):
         info = fb.backward_launch_info((1, 6, 32, 88, C), dtype, np.zeros(8), grid, (256, 704))
         lpc = min(64, (C + 3) // 4)

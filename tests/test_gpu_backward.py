@@ -81,9 +81,12 @@ def test_backward_workloads_full(fb, device, wl):
     assert terms.sum() > 0
 
 
-def test_backward_paper_reference_setting(fb, device):
-    inst = synth.make_workload(synth.config("paper_ref"))
-    check(fb, inst, device, what="paper_ref")
+@pytest.mark.parametrize("C", [128, 256])
+def test_backward_paper_reference_setting(fb, device, C):
+    """The paper's reference setting in full; C = 256 takes the tiled mode's
+    wide-row path (channel blocks beyond two per lane)."""
+    inst = synth.make_workload(synth.config("paper_ref", C=C))
+    check(fb, inst, device, what=f"paper_ref C={C}")
 
 
 @pytest.mark.parametrize("reduce", ["mean", "sum"])
@@ -93,7 +96,9 @@ def test_backward_reduce_modes(fb, device, reduce):
 
 
 @pytest.mark.parametrize("C,dtype", [(1, "f32"), (5, "f32"), (7, "bf16"), (36, "f16"),
-                                     (260, "f32"), (1024, "f32"), (2048, "bf16")])
+                                     (128, "f32"), (129, "f32"), (192, "f32"), (256, "bf16"),
+                                     (260, "f32"), (512, "f32"), (512, "f16"),
+                                     (1024, "f32"), (2048, "bf16")])
 def test_backward_channel_counts(fb, device, C, dtype):
     wl = synth.config("tiny").with_(C=C, dtype=dtype, X=21, Y=19)
     check(fb, synth.make_workload(wl), device, what=f"C={C} {dtype}")
