@@ -58,10 +58,33 @@ def _compile(srcs, lib: str, verbose: bool) -> str:
     return lib
 
 
+# a C++ program that drives the forward through the C ABI alone (plain HIP
+# memory and streams); the GPU tests run it (test infrastructure)
+C_ABI_SRC = os.path.join(ROOT, "tests", "c_abi_forward.cpp")
+C_ABI_EXE = os.path.join(ROOT, "tests", "c_abi_forward")
+
+
+def _build_c_abi_program(verbose: bool) -> str:
+    tmp = C_ABI_EXE + ".tmp"
+    cmd = [hipcc(), "-O2", "-std=c++17", "-Wall", f"-I{INCLUDE}", C_ABI_SRC, "-o", tmp,
+           f"-L{HERE}", "-lflashbev", "-Wl,-rpath,$ORIGIN/../paper_2607_10071_amd"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError(f"hipcc failed with status {r.returncode}")
+    os.replace(tmp, C_ABI_EXE)
+    return C_ABI_EXE
+
+
 def build(verbose: bool = False) -> str:
-    """Compile the operator library and the micro-benchmark library."""
+    """Compile the operator library, the micro-benchmark library and the
+    C-ABI test program."""
     _compile([MEMBENCH_SRC], MEMBENCH_LIB, verbose)
-    return _compile([SRC, SCA_SRC], LIB, verbose)
+    lib = _compile([SRC, SCA_SRC], LIB, verbose)
+    _build_c_abi_program(verbose)
+    return lib
 
 
 if __name__ == "__main__":
