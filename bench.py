@@ -714,6 +714,15 @@ def main(argv=None) -> int:
             "frac": round(g_ach / peak, 4) if peak else None,
             "gather_bytes_per_launch": gather_bytes,
             "valid_samples": counters["valid_samples"], "taps": counters["taps"]}
+        # the rates beside Gsamples/s: valid samples, channel taps (T C) and the
+        # FMAs of the gather (4 C V: every valid sample's four taps, in range
+        # or not, times the channels), per second of launch time
+        fma = 4 * wl.C * counters["valid_samples"]
+        rec["rates"] = {
+            "valid_Gsamples_per_s": round(counters["valid_samples"] / launch_s / 1e9, 3),
+            "channel_taps_G_per_s": round(counters["taps"] * wl.C / launch_s / 1e9, 2),
+            "fma_per_launch": fma,
+            "TFMA_per_s": round(fma / launch_s / 1e12, 3)}
 
     if not args.no_extra:
         # backward (gradient w.r.t. the features) on the same workload and on
