@@ -80,9 +80,9 @@ def tensorized_footprint(wl) -> dict:
     return {"features3d_bytes": f3d, "alg1_all_writes_bytes": allw}
 
 
-def load_traffic(workload: str, src: str = KERNEL_SRC):
-    """HBM traffic per launch from committed rocprofv3 counter passes, if
-    they were taken on the current kernel source."""
+def load_counters(workload: str, src: str = KERNEL_SRC):
+    """The committed rocprofv3 counter summary of a workload (HBM bytes per
+    launch, L2 hit rate), if it was taken on the current kernel source."""
     path = os.path.join(PROFILE_DIR, "traffic.json")
     if not os.path.exists(path):
         return None
@@ -91,7 +91,20 @@ def load_traffic(workload: str, src: str = KERNEL_SRC):
     rec = data.get(workload)
     if not rec or rec.get("kernel_sha") != kernel_hash(src):
         return None
-    return rec.get("bytes_per_launch")
+    return rec
+
+
+def load_traffic(workload: str, src: str = KERNEL_SRC):
+    """HBM traffic per launch from committed rocprofv3 counter passes, if
+    they were taken on the current kernel source."""
+    rec = load_counters(workload, src)
+    return rec.get("bytes_per_launch") if rec else None
+
+
+def load_l2_hit(workload: str, src: str = KERNEL_SRC):
+    """L2 hit rate of the committed counter passes (current source only)."""
+    rec = load_counters(workload, src)
+    return rec.get("l2_hit_rate") if rec else None
 
 
 def settle(fn, seconds: float = 0.3) -> None:
@@ -499,6 +512,7 @@ def measure_sca(device, steps: int, warmup: int, cpu: bool, cpu_seconds: float,
              "hbm_frac": round(alg / sec / 1e9 / HBM_PEAK_GBS, 5),
              "peak_op_memory_bytes": sca_peak_memory(wl, inst, device),
              "traffic": load_traffic(f"sca_base_p{P}", SCA_KERNEL_SRC),
+             "l2_hit_rate": load_l2_hit(f"sca_base_p{P}", SCA_KERNEL_SRC),
              "paper_4070tis": SCA_PAPER.get(P)}
         del fn, keep
         bfn, bkeep, bstream = make_sca_backward_call(wl, inst, device)
@@ -672,7 +686,8 @@ def main(argv=None) -> int:
         "latency_ms": round(t["ms_per_step"], 5),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
-                     "traffic": traffic, "algorithmic_bytes_per_launch": alg,
+                     "traffic": traffic, "l2_hit_rate": load_l2_hit(wl.name),
+                     "algorithmic_bytes_per_launch": alg,
                      "kernel": "sample_vt_fwd", "launch": info},
         "peak_op_memory_bytes": peak_mem,
         "output_bytes": wl.B * wl.C * wl.X * wl.Y * 4,
