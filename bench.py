@@ -574,7 +574,7 @@ def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
     import oracle
 
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    _, _, counters = oracle.run_instance(inst, nthreads=threads)  # warm-up
+    ref, scale, counters = oracle.run_instance(inst, nthreads=threads)  # warm-up
     reps, t = 0, 0.0
     while t < min_seconds and reps < 5000:
         t0 = time.perf_counter()
@@ -586,7 +586,26 @@ def cpu_baseline(inst, min_seconds: float = 10.0) -> dict:
             "kind": "oracle", "ms_per_call": per * 1e3,
             "sample": f"the whole {inst.wl.name} workload ({inst.wl.samples} samples) "
                       f"evaluated {reps} times in {t:.1f} s",
-            "counters": counters}
+            "counters": counters, "ref": ref, "scale": scale}
+
+
+def parity_stats(gpu, ref, scale) -> dict:
+    """The GPU output against the oracle's: max and mean absolute error, mean
+    relative error, cosine similarity (the paper's Table 2 columns) and the
+    largest error over the oracle's magnitude scale (the parity bar's form)."""
+    import numpy as np
+
+    g = gpu.astype(np.float64).ravel()
+    r = ref.ravel()
+    s = scale.ravel()
+    err = np.abs(g - r)
+    nz = s > 0
+    cos = float(np.dot(g, r) / max(np.linalg.norm(g) * np.linalg.norm(r), 1e-300))
+    return {"vs": "CPU oracle (float64)", "elements": int(g.size),
+            "max_abs": float(err.max(initial=0.0)), "mean_abs": float(err.mean()) if g.size else 0.0,
+            "mean_rel": float((err[nz] / np.maximum(np.abs(r[nz]), 1e-12)).mean()) if nz.any() else 0.0,
+            "cosine": cos, "max_scaled": float((err[nz] / s[nz]).max(initial=0.0)),
+            "exact_zeros_where_no_tap": bool(np.all(g[~nz] == 0.0))}
 
 
 def main(argv=None) -> int:
@@ -663,6 +682,7 @@ def main(argv=None) -> int:
     info = fb.launch_info((wl.B, wl.N, wl.H, wl.W, wl.C), wl.dtype, inst.z, fb.grid_of(wl),
                           (wl.img_h, wl.img_w), data_ptr=feats.data_ptr())
     peak_mem = peak_operator_memory(wl, inst, device)
+    gpu_out = out.cpu().numpy()  # after the timed region: for the parity record
     del fn, feats, l2i, out
     row_bytes = wl.C * elem_size(wl.dtype)
 
@@ -717,6 +737,7 @@ def main(argv=None) -> int:
     if not args.no_cpu_baseline:
         cb = cpu_baseline(inst, args.cpu_seconds)
         counters = cb.pop("counters")
+        rec["parity"] = parity_stats(gpu_out, cb.pop("ref"), cb.pop("scale"))
         rec["cpu_baseline"] = cb
         # gather roofline: the in-range bilinear taps of the workload (counted
         # by the oracle above) times the feature row, over the launch time,
