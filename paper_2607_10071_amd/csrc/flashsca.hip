@@ -67,6 +67,14 @@ constexpr uint32_t kScaLdsMax = 160u * 1024u;      // gfx950's LDS per workgroup
 constexpr int kRecFwd = 8;
 constexpr int kRecBwd = 12;
 constexpr int kSlotPad = 4;
+// Backward row merge, per wavefront: a chunk has lph * spw * 4 = 256 (slot,
+// point, tap) rows.  An open-addressing table of 256 keys (tap offsets) with
+// the head of each key's member list, the members' links, the list of keys
+// in use and its length: 256 + 256 dwords, 2 x 256 halfwords, one counter.
+constexpr int kMrgRows = 4 * kScaWave;
+constexpr int kMrgWords = 2 * kMrgRows + kMrgRows + 4;
+constexpr uint32_t kMrgEmpty = 0xFFFFFFFFu;   // no key (tap offsets are below 2^31)
+constexpr uint32_t kMrgEnd = 0xFFFFFFFFu;     // end of a member list
 
 struct ScaParams {
     const void *value;
@@ -87,7 +95,8 @@ struct ScaParams {
     int32_t lph;             // lanes per slot (power of two)
     int32_t lph_shift;       // log2(lph)
     int32_t spw;             // slots per wavefront
-    int32_t tile_pairs;      // (query, head) pairs per workgroup
+    int32_t tile_pairs;      // forward: (query, head) pairs per workgroup
+    int32_t head_groups;     // backward: tiles of one query group (heads / waves, rounded up)
     int32_t tiles_per_b;
     int32_t stripe;          // consecutive tiles an XCD takes in turn (about one block)
     int32_t nq_max;          // queries a tile can touch
@@ -100,18 +109,19 @@ struct ScaParams {
     int32_t level_w[FLASHSCA_LMAX], level_h[FLASHSCA_LMAX];
     uint32_t level_start[FLASHSCA_LMAX];   // first pixel of each level
     // LDS layout (byte offsets)
-    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_acc, lds_gst, lds_tap;
+    uint32_t lds_mat, lds_lvl, lds_z, lds_ref, lds_hit, lds_att, lds_gst, lds_tap;
+    uint32_t lds_mrg;
     float rcp_d;             // float32 1 / D for div_small
     float z[FLASHSCA_ZMAX];
 };
 
 // LDS: camera matrices [N][12]; level table [5][LMAX]; anchors [Z];
-// reference points [nq_max][N][Z] float2; hit masks [nq_max]; attention
-// weights [waves][spw][LP]; backward only: point gradients
-// [waves][spw][3][LP] and output-gradient rows [waves][spw][D]; chunk records
-// [waves][spw][slot_stride].
+// reference points [nq_max][N][Z] float2; hit masks [nq_max]; forward only:
+// attention weights [waves][spw][LP]; backward only: output-gradient rows
+// [waves][spw][D]; chunk records [waves][spw][slot_stride]; backward only:
+// row-merge tables [waves][kMrgWords].
 struct ScaLds {
-    uint32_t mat, lvl, z, ref, hit, att, acc, gst, tap, total;
+    uint32_t mat, lvl, z, ref, hit, att, gst, tap, mrg, total;
 };
 
 __host__ inline uint32_t sca_align16(uint32_t v) { return (v + 15u) & ~15u; }
@@ -126,10 +136,10 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
     s.z = o; o = sca_align16(o + (uint32_t)Z * 4u);
     s.ref = o; o = sca_align16(o + (uint32_t)nq_max * N * Z * 8u);
     s.hit = o; o = sca_align16(o + (uint32_t)nq_max * 4u);
-    s.att = o; o = sca_align16(o + (uint32_t)waves * spw * LP * 4u);
-    s.acc = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * LP * 12u : 0u));
+    s.att = o; o = sca_align16(o + (backward ? 0u : (uint32_t)waves * spw * LP * 4u));
     s.gst = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * D * 4u : 0u));
     s.tap = o; o = sca_align16(o + (uint32_t)waves * spw * slot_stride * 4u);
+    s.mrg = o; o = sca_align16(o + (backward ? (uint32_t)waves * kMrgWords * 4u : 0u));
     s.total = o;
     return s;
 }
@@ -155,9 +165,9 @@ __device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
 
 // LDS views of one workgroup.
 struct ScaSmem {
-    float *mat, *lwf, *lhf, *z, *att, *acc, *gst;
+    float *mat, *lwf, *lhf, *z, *att, *gst;
     int32_t *lw, *lh;
-    uint32_t *lst, *hit, *tap;
+    uint32_t *lst, *hit, *tap, *mrg;
     float2 *ref;
 };
 
@@ -174,9 +184,9 @@ __device__ __forceinline__ ScaSmem sca_smem(const ScaParams &p, unsigned char *s
     m.ref = reinterpret_cast<float2 *>(smem + p.lds_ref);
     m.hit = reinterpret_cast<uint32_t *>(smem + p.lds_hit);
     m.att = reinterpret_cast<float *>(smem + p.lds_att);
-    m.acc = reinterpret_cast<float *>(smem + p.lds_acc);
     m.gst = reinterpret_cast<float *>(smem + p.lds_gst);
     m.tap = reinterpret_cast<uint32_t *>(smem + p.lds_tap);
+    m.mrg = reinterpret_cast<uint32_t *>(smem + p.lds_mrg);
     return m;
 }
 
@@ -295,6 +305,33 @@ __device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m
     return s;
 }
 
+// A slot of the backward.  Its tiles are head-major: a tile holds spw
+// consecutive queries (ranks r_first ...) and `waves` heads, slot s of
+// wavefront w being query r_first + s and head hg * waves + w.  The slots of a
+// wavefront then share their head, so their taps on one pixel are the same
+// value-gradient row and can be merged before the scatter.
+__device__ __forceinline__ ScaSlot sca_slot_bwd(const ScaParams &p, const ScaSmem &m, int b,
+                                                int r_first, int hg, int wave, int lane)
+{
+    ScaSlot s;
+    s.sub = lane & (p.lph - 1);
+    s.slot = lane >> p.lph_shift;
+    const int waves = (int)(blockDim.x / kScaWave);
+    const int rank = r_first + s.slot;
+    const int mh = hg * waves + wave;
+    s.active = rank < p.Q && mh < p.heads;
+    s.mh = s.active ? mh : 0;
+    s.qi = s.active ? s.slot : 0;
+    int qx, qy;
+    query_of(s.active ? rank : r_first, p.X, p.Y, qx, qy);
+    s.q = qx * p.Y + qy;
+    s.hits = s.active ? m.hit[s.qi] : 0u;
+    const int count = __popc(s.hits);
+    s.inv = (p.reduce == FLASHBEV_REDUCE_VALID_MEAN && count > 1) ? 1.0f / (float)count : 1.0f;
+    s.pt0 = (((size_t)b * p.Q + s.q) * p.heads + s.mh) * (size_t)p.LP;
+    return s;
+}
+
 // Phase 2: att[j] = post * softmax over the slot's L*P logits (only for
 // slots with a hit camera).  The shuffles stay inside the slot, whose lanes
 // all take the branch or none.
@@ -315,6 +352,25 @@ __device__ __forceinline__ void sca_softmax(const ScaParams &p, const ScaSlot &s
     for (int o = lph >> 1; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
     const float r = post / sum;
     for (int j = s.sub; j < LP; j += lph) att[j] *= r;
+}
+
+// The same softmax's maximum and 1 / sum, for weights recomputed on the fly
+// as expf(logit - mx) * rcp (the values sca_softmax stores with post = 1).
+__device__ __forceinline__ void sca_softmax_stats(const ScaParams &p, const ScaSlot &s, float &mx,
+                                                  float &rcp)
+{
+    mx = 0.0f;
+    rcp = 0.0f;
+    if (!s.hits) return;
+    const int lph = p.lph, LP = p.LP;
+    float m = -INFINITY;
+    for (int j = s.sub; j < LP; j += lph) m = fmaxf(m, p.logits[s.pt0 + j]);
+    for (int o = lph >> 1; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float sum = 0.0f;
+    for (int j = s.sub; j < LP; j += lph) sum += expf(p.logits[s.pt0 + j] - m);
+    for (int o = lph >> 1; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    mx = m;
+    rcp = 1.0f / sum;
 }
 
 // Set-up of point j of a slot in one camera: tap byte offsets (kScaNoTap
@@ -486,23 +542,17 @@ sca_bwd(const ScaParams p)
 
     const int tile = sca_tile(p);
     const int b = tile / p.tiles_per_b;
-    const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
-    const int r_first = (int)(pair0 / p.heads);
+    const int tb = tile - b * p.tiles_per_b;
+    const int qg = tb / p.head_groups;
+    const int r_first = qg * p.spw;
     sca_project_tile(p, m, b, r_first);
 
-    const ScaSlot s = sca_slot(p, m, b, pair0, r_first, wave, lane);
+    const ScaSlot s = sca_slot_bwd(p, m, b, r_first, tb - qg * p.head_groups, wave, lane);
     const int lph = p.lph, LP = p.LP;
     const int slot_id = wave * p.spw + s.slot;
-    float *att = m.att + (size_t)slot_id * LP;                 // softmax a_j
-    float *g_da = m.acc + (size_t)slot_id * 3 * LP;            // d a_j (before the mean)
-    float *g_dx = g_da + LP;                                   // d x_j (before the mean and a_j)
-    float *g_dy = g_dx + LP;
-    sca_softmax(p, s, att, 1.0f);
-    for (int j = s.sub; j < LP; j += lph) {
-        g_da[j] = 0.0f;
-        g_dx[j] = 0.0f;
-        g_dy[j] = 0.0f;
-    }
+    // softmax a_j = expf(logit_j - mx) * rcp, recomputed where needed
+    float mx, rcp;
+    sca_softmax_stats(p, s, mx, rcp);
     const uint32_t cams = sca_wave_cameras(p, s.hits);
 
     // this lane's slice of the output gradient
@@ -524,24 +574,43 @@ sca_bwd(const ScaParams p)
     for (int e = 0; e < EPV; ++e)
         if (e0 + e < D) gst_w[s.slot * D + e0 + e] = gs[e];
     const uint32_t *rec_w = m.tap + (size_t)wave * p.spw * p.slot_stride;   // the wavefront's
-    const int rows_pt = p.spw * 4;           // (slot, tap) rows per point index
-    const int elems_pt = rows_pt * D;
+    const int spw_shift = __builtin_ctz((unsigned)p.spw);
+    // the wavefront's row-merge table, empty
+    uint32_t *tkey = m.mrg + (size_t)wave * kMrgWords;
+    uint32_t *thead = tkey + kMrgRows;
+    uint16_t *tnext = reinterpret_cast<uint16_t *>(thead + kMrgRows);
+    uint16_t *tuniq = tnext + kMrgRows;
+    uint32_t *tcount = thead + kMrgRows + kMrgRows;
+    for (int h = lane; h < kMrgRows; h += kScaWave) {
+        tkey[h] = kMrgEmpty;
+        thead[h] = kMrgEnd;
+    }
+    if (lane == 0) *tcount = 0u;
 
-    for (int n = 0; n < p.N; ++n) {
-        if (!((cams >> n) & 1u)) continue;
-        const bool mine = (s.hits >> n) & 1u;
-        const __amdgpu_buffer_rsrc_t rsrc = sca_camera_rsrc(p, b, n);
-        const float2 *ref = m.ref + (size_t)(s.qi * p.N + n) * p.Z;
-        float *gv = p.grad_value ? p.grad_value + ((size_t)b * p.N + n) * p.cam_elems : nullptr;
-        for (int c0 = 0; c0 < LP; c0 += lph) {
-            const int j = c0 + s.sub;
+    // Chunks of lph points (lane sub owns point c0 + sub), each over the
+    // cameras the wavefront's slots hit.  The owner keeps its point's
+    // gradients in registers across the cameras, so no per-point state stays
+    // in LDS.
+    float dot = 0.0f;   // sum of a_j d a_j over this lane's points
+    for (int c0 = 0; c0 < LP; c0 += lph) {
+        const int j = c0 + s.sub;
+        const bool own = s.hits && j < LP;
+        const float a_j = own ? expf(p.logits[s.pt0 + j] - mx) * rcp : 0.0f;
+        const int npts = (LP - c0) < lph ? (LP - c0) : lph;
+        float g_da = 0.0f, g_dx = 0.0f, g_dy = 0.0f;   // before the mean (and a_j for x, y)
+        for (int n = 0; n < p.N; ++n) {
+            if (!((cams >> n) & 1u)) continue;
+            const bool mine = own && ((s.hits >> n) & 1u);
+            const __amdgpu_buffer_rsrc_t rsrc = sca_camera_rsrc(p, b, n);
+            const float2 *ref = m.ref + (size_t)(s.qi * p.N + n) * p.Z;
+            float *gv = p.grad_value ? p.grad_value + ((size_t)b * p.N + n) * p.cam_elems : nullptr;
             uint4 o = make_uint4(kScaNoTap, kScaNoTap, kScaNoTap, kScaNoTap);
             float4 w = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             float ax = 0.0f, ay = 0.0f, aa = 0.0f;
-            if (mine && j < LP) {
+            if (mine) {
                 if (sca_setup_point(p, m, ref, s, j, head_off, o, ax, ay)) {
                     w = sca_weights(o, ax, ay, 1.0f);
-                    aa = s.inv * att[j];   // the value scatter's factor: mean times a_j
+                    aa = s.inv * a_j;   // the value scatter's factor: mean times a_j
                 }
             }
             uint32_t *mine_rec = rec + s.sub * kRecBwd;
@@ -549,7 +618,6 @@ sca_bwd(const ScaParams p)
             *reinterpret_cast<float4 *>(mine_rec + 4) = w;
             *reinterpret_cast<float4 *>(mine_rec + 8) = make_float4(ax, ay, aa, 0.0f);
             wave_lds_sync();
-            const int npts = (LP - c0) < lph ? (LP - c0) : lph;
             // gradients of the point this lane owns (point c0 + sub)
             float my_da = 0.0f, my_dx = 0.0f, my_dy = 0.0f;
             for (int t = 0; t < npts; ++t) {
@@ -580,53 +648,115 @@ sca_bwd(const ScaParams p)
                 const float da = ((tw.x * d0 + tw.y * d1) + tw.z * d2) + tw.w * d3;
                 const float dx = (1.0f - tay) * (d1 - d0) + tay * (d3 - d2);
                 const float dy = (1.0f - tax) * (d2 - d0) + tax * (d3 - d1);
-                const bool own = s.sub == t;
-                my_da += own ? da : 0.0f;
-                my_dx += own ? dx : 0.0f;
-                my_dy += own ? dy : 0.0f;
+                const bool owner = s.sub == t;
+                my_da += owner ? da : 0.0f;
+                my_dx += owner ? dx : 0.0f;
+                my_dy += owner ? dy : 0.0f;
             }
             // value gradient: mean * a * w * G[c] onto each in-range tap.  The
-            // wavefront walks its (point, slot, tap, channel) elements in that
-            // order, 64 consecutive channels per atomic instruction, so one
-            // instruction covers whole head rows (one 128-byte row per 32
-            // lanes for float32 D = 32) rather than a few channels of each
-            // slot's row.
+            // chunk's (point, slot, tap) rows r = (t spw + slot) 4 + tap go
+            // into the table by tap offset; rows on the same pixel (the
+            // slots share the head) land on one key and are summed before a
+            // single scatter of the key's row.  The wavefront then walks its
+            // distinct rows, 64 consecutive channels per atomic instruction,
+            // so one instruction covers whole head rows (one 128-byte row per
+            // 32 lanes for float32 D = 32).
             if (gv) {
-                for (int t = 0; t < npts; ++t) {
-                    for (int E = lane; E < elems_pt; E += kScaWave) {
-                        const int row = div_small(E, D, p.rcp_d);
-                        const int ch = E - row * D;
-                        const int sl = row >> 2, c = row & 3;
-                        const uint32_t *r = rec_w + (size_t)sl * p.slot_stride + t * kRecBwd;
-                        const uint32_t ot = r[c];
-                        if (ot == kScaNoTap) continue;
-                        const float coef = __builtin_bit_cast(float, r[10]) *
-                                           __builtin_bit_cast(float, r[4 + c]);
-                        unsafeAtomicAdd(gv + ot / ES + ch, coef * gst_w[sl * D + ch]);
+                const int nrows = npts << (spw_shift + 2);
+                for (int r = lane; r < nrows; r += kScaWave) {
+                    const int ts = r >> 2;
+                    const int sl = ts & (p.spw - 1);
+                    const uint32_t *rr = rec_w + (size_t)sl * p.slot_stride +
+                                         (ts >> spw_shift) * kRecBwd;
+                    const uint32_t key = rr[r & 3];
+                    if (key == kScaNoTap) continue;
+                    uint32_t h = (key * 0x9E3779B1u) >> 24;   // 256 buckets
+                    bool placed = false;
+                    for (int probe = 0; probe < kMrgRows; ++probe) {
+                        const uint32_t old = atomicCAS(&tkey[h], kMrgEmpty, key);
+                        if (old == kMrgEmpty) {
+                            tuniq[atomicAdd(tcount, 1u)] = (uint16_t)h;
+                            placed = true;
+                            break;
+                        }
+                        if (old == key) {
+                            placed = true;
+                            break;
+                        }
+                        h = (h + 1) & (kMrgRows - 1);
+                    }
+                    if (placed) {
+                        tnext[r] = (uint16_t)atomicExch(&thead[h], (uint32_t)r);
+                    } else {
+                        // unreachable (the table holds every row of a chunk);
+                        // the row is then scattered alone
+                        const float coef = __builtin_bit_cast(float, rr[10]) *
+                                           __builtin_bit_cast(float, rr[4 + (r & 3)]);
+                        for (int ch = 0; ch < D; ++ch)
+                            unsafeAtomicAdd(gv + key / ES + ch, coef * gst_w[sl * D + ch]);
                     }
                 }
+                wave_lds_sync();
+                const int nel = (int)*tcount * D;
+                for (int E = lane; E < nel; E += kScaWave) {
+                    const int u = div_small(E, D, p.rcp_d);
+                    const int ch = E - u * D;
+                    const uint32_t h = tuniq[u] & (kMrgRows - 1);
+                    const uint32_t key = tkey[h];
+                    uint32_t r = thead[h];
+                    float val = 0.0f;
+                    for (int k = 0; k < kMrgRows && r < (uint32_t)nrows; ++k) {
+                        const int ts = (int)(r >> 2);
+                        const int sl = ts & (p.spw - 1);
+                        const uint32_t *rr = rec_w + (size_t)sl * p.slot_stride +
+                                             (ts >> spw_shift) * kRecBwd;
+                        const float coef = __builtin_bit_cast(float, rr[10]) *
+                                           __builtin_bit_cast(float, rr[4 + (r & 3)]);
+                        val = fmaf(coef, gst_w[sl * D + ch], val);
+                        const uint32_t nx = tnext[r];
+                        r = (nx == 0xFFFFu) ? kMrgEnd : nx;
+                    }
+                    if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
+                }
+                wave_lds_sync();
+                for (int h = lane; h < kMrgRows; h += kScaWave) {
+                    tkey[h] = kMrgEmpty;
+                    thead[h] = kMrgEnd;
+                }
+                if (lane == 0) *tcount = 0u;
             }
-            if (mine && j < LP) {
-                g_da[j] += my_da;
-                g_dx[j] += my_dx;
-                g_dy[j] += my_dy;
-            }
+            g_da += my_da;
+            g_dx += my_dx;
+            g_dy += my_dy;
             wave_lds_sync();
+        }
+        if (own) {
+            dot += a_j * g_da;
+            const float sa = s.inv * a_j;
+            if (p.grad_offsets)
+                reinterpret_cast<float2 *>(p.grad_offsets)[s.pt0 + j] =
+                    make_float2(sa * g_dx, sa * g_dy);
+            // d a_j for now; the softmax backward below finishes it
+            if (p.grad_logits) p.grad_logits[s.pt0 + j] = g_da;
         }
     }
 
-    // ---- softmax backward and the point gradients (lanes own points j = sub mod lph)
-    float dot = 0.0f;
-    if (s.hits)
-        for (int j = s.sub; j < LP; j += lph) dot += att[j] * g_da[j];
+    // ---- softmax backward (lanes own points j = sub mod lph; each lane
+    // reads back only what it wrote itself)
     for (int x = lph >> 1; x >= 1; x >>= 1) dot += __shfl_xor(dot, x);
     if (s.active) {
         for (int j = s.sub; j < LP; j += lph) {
-            const float sa = s.hits ? s.inv * att[j] : 0.0f;
-            if (p.grad_logits) p.grad_logits[s.pt0 + j] = sa * (g_da[j] - dot);
-            if (p.grad_offsets)
-                reinterpret_cast<float2 *>(p.grad_offsets)[s.pt0 + j] =
-                    make_float2(sa * g_dx[j], sa * g_dy[j]);
+            if (s.hits) {
+                if (p.grad_logits) {
+                    const float sa = s.inv * (expf(p.logits[s.pt0 + j] - mx) * rcp);
+                    p.grad_logits[s.pt0 + j] = sa * (p.grad_logits[s.pt0 + j] - dot);
+                }
+            } else {
+                // no hit camera: the point gradients are zero
+                if (p.grad_logits) p.grad_logits[s.pt0 + j] = 0.0f;
+                if (p.grad_offsets)
+                    reinterpret_cast<float2 *>(p.grad_offsets)[s.pt0 + j] = make_float2(0.0f, 0.0f);
+            }
         }
     }
 }
@@ -800,12 +930,16 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     const int spw = kScaWave / lph;
     const int slot_stride = lph * (backward ? kRecBwd : kRecFwd) + kSlotPad;
 
+    // the backward's head-major tiles take one head per wavefront: no more
+    // wavefronts than heads
     int waves = kScaWavesMax;
+    if (backward && waves > v->heads) waves = v->heads >= 2 ? 2 : 1;
     int nq_max = 0;
     ScaLds lay{};
     for (;;) {
         const int tp = waves * spw;
-        nq_max = (tp - 1) / v->heads + 2;
+        // forward: tp consecutive (query, head) pairs; backward: spw queries
+        nq_max = backward ? spw : (tp - 1) / v->heads + 2;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
         lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, D, slot_stride, backward);
         if (lay.total <= kScaLdsBudget || waves == 1) break;
@@ -838,7 +972,11 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     p.spw = spw;
     p.tile_pairs = tile_pairs;
     const uint64_t pairs_b = Q * (uint64_t)v->heads;
-    p.tiles_per_b = (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
+    p.head_groups = (v->heads + waves - 1) / waves;
+    // forward: tile_pairs consecutive pairs; backward: spw queries x `waves` heads
+    // (at most Q heads tiles, within 2^31 - 1)
+    p.tiles_per_b = backward ? (int32_t)(((Q + spw - 1) / spw) * (uint64_t)p.head_groups)
+                             : (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
     {
         // one contiguous band of tiles per XCD (see sca_tile)
         const int64_t nt = (int64_t)v->B * p.tiles_per_b / kScaXcds;
@@ -868,10 +1006,10 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     p.lds_ref = lay.ref;
     p.lds_hit = lay.hit;
     p.lds_att = lay.att;
-    p.lds_acc = lay.acc;
     p.lds_gst = lay.gst;
     p.rcp_d = 1.0f / (float)D;
     p.lds_tap = lay.tap;
+    p.lds_mrg = lay.mrg;
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
     pl->workgroups = empty ? 0 : (int64_t)v->B * p.tiles_per_b;
