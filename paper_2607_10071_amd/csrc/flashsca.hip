@@ -147,9 +147,11 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
 // Cell (i, j) of the query of rank r in the blocked visiting order: the grid
 // is cut into bands of kScaBlock rows; a band into blocks of kScaBlock
 // columns (the last band and block may be narrower); blocks follow each other
-// along the band, and a block's cells are row-major.  A bijection of
+// along the band.  A block's cells are row-major, or with `zorder` a full
+// block's are in Z order (rank bits alternate column, row, column, ...), so
+// that 2^k consecutive ranks form a 2 x 4, 4 x 4, ... patch.  A bijection of
 // [0, X Y) onto the cells.
-__device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
+__device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j, bool zorder = false)
 {
     const int band_cells = kScaBlock * Y;
     const int R = r / band_cells;
@@ -158,6 +160,12 @@ __device__ __forceinline__ void query_of(int r, int X, int Y, int &i, int &j)
     const int c = s / (h * kScaBlock);
     const int t = s - c * h * kScaBlock;
     const int w = min(kScaBlock, Y - c * kScaBlock);
+    if (zorder && h == kScaBlock && w == kScaBlock) {
+        const uint32_t u = (uint32_t)t;
+        i = R * kScaBlock + (int)(((u >> 1) & 1u) | ((u >> 2) & 2u) | ((u >> 3) & 4u) | ((u >> 4) & 8u));
+        j = c * kScaBlock + (int)((u & 1u) | ((u >> 1) & 2u) | ((u >> 2) & 4u) | ((u >> 3) & 8u));
+        return;
+    }
     const int ti = t / w;
     i = R * kScaBlock + ti;
     j = c * kScaBlock + (t - ti * w);
@@ -224,7 +232,7 @@ __device__ __forceinline__ int sca_tile(const ScaParams &p)
 // Stage matrices, level table and anchors; phase 1: reference points and
 // hit masks of the tile's queries.  Ends with a workgroup barrier.
 __device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSmem &m, int b,
-                                                 int r_first)
+                                                 int r_first, bool zorder = false)
 {
     const int tid = threadIdx.x;
     const int nthreads = blockDim.x;
@@ -249,7 +257,7 @@ __device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSm
         const int rank = r_first + qi;
         if (rank >= p.Q) continue;
         int i, j;
-        query_of(rank, p.X, p.Y, i, j);
+        query_of(rank, p.X, p.Y, i, j, zorder);
         const float x = p.x_min + ((float)i + 0.5f) * p.dx;
         const float y = p.y_min + ((float)j + 0.5f) * p.dy;
         const float *mr = m.mat + n * 12;
@@ -306,10 +314,13 @@ __device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m
 }
 
 // A slot of the backward.  Its tiles are head-major: a tile holds spw
-// consecutive queries (ranks r_first ...) and `waves` heads, slot s of
-// wavefront w being query r_first + s and head hg * waves + w.  The slots of a
-// wavefront then share their head, so their taps on one pixel are the same
-// value-gradient row and can be merged before the scatter.
+// consecutive queries (ranks r_first ..., in the Z order of query_of) and
+// `waves` heads, slot s of wavefront w being query r_first + s and head
+// hg * waves + w.  The slots of a wavefront then share their head and cover a
+// compact patch of cells, so their taps on one pixel are the same
+// value-gradient row and can be merged before the scatter (BEVFormer-base,
+// P = 8, per chunk of 8 points: 1.83x fewer rows for 1 x 8 strips of queries,
+// 2.05x for 2 x 4 patches, 2.85x for 4 x 4).
 __device__ __forceinline__ ScaSlot sca_slot_bwd(const ScaParams &p, const ScaSmem &m, int b,
                                                 int r_first, int hg, int wave, int lane)
 {
@@ -323,7 +334,7 @@ __device__ __forceinline__ ScaSlot sca_slot_bwd(const ScaParams &p, const ScaSme
     s.mh = s.active ? mh : 0;
     s.qi = s.active ? s.slot : 0;
     int qx, qy;
-    query_of(s.active ? rank : r_first, p.X, p.Y, qx, qy);
+    query_of(s.active ? rank : r_first, p.X, p.Y, qx, qy, true);
     s.q = qx * p.Y + qy;
     s.hits = s.active ? m.hit[s.qi] : 0u;
     const int count = __popc(s.hits);
@@ -545,7 +556,7 @@ sca_bwd(const ScaParams p)
     const int tb = tile - b * p.tiles_per_b;
     const int qg = tb / p.head_groups;
     const int r_first = qg * p.spw;
-    sca_project_tile(p, m, b, r_first);
+    sca_project_tile(p, m, b, r_first, true);
 
     const ScaSlot s = sca_slot_bwd(p, m, b, r_first, tb - qg * p.head_groups, wave, lane);
     const int lph = p.lph, LP = p.LP;
