@@ -1345,8 +1345,11 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     uint32_t l_rcnt = 0, l_rbase = 0, l_rfill = 0, l_list = 0;
     int t_pitch = 0;
     int t_rs = kRecStride;
-    // rows up to kBwdTiledCMax channels (wider ones leave too few LDS rows)
-    if (npix + 1 < (1u << kKeyBits) && f->C <= kBwdTiledCMax && f->N > 0) {
+    // rows up to kBwdTiledCMax channels (wider ones leave too few LDS rows);
+    // grid sides that leave a tile's cell coordinates (side + tile side)
+    // within int32
+    if (npix + 1 < (1u << kKeyBits) && f->C <= kBwdTiledCMax && f->N > 0 &&
+        (uint64_t)s->X + 2u * kWave < 0x7FFFFFFFull && (uint64_t)s->Y + 2u * kWave < 0x7FFFFFFFull) {
         t_waves = kBwdTileWaves;
         const int T = t_waves * cpw;
         t_ty = (T % 4 == 0) ? 4 : T;
@@ -1423,8 +1426,11 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     if (tiled) {
         p.tx = t_tx;
         p.ty = t_ty;
-        p.tiles_y = (s->Y + t_ty - 1) / t_ty;
-        p.tiles_per_b = ((s->X + t_tx - 1) / t_tx) * p.tiles_y;
+        const int64_t tiles_y = ((int64_t)s->Y + t_ty - 1) / t_ty;
+        const int64_t tiles = (((int64_t)s->X + t_tx - 1) / t_tx) * tiles_y;
+        if (tiles > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
+        p.tiles_y = (int32_t)tiles_y;
+        p.tiles_per_b = (int32_t)tiles;
         p.rcp_ty = 1.0f / (float)t_ty;
         p.rcp_c = 1.0f / (float)f->C;
         p.cap = t_cap;

@@ -67,14 +67,16 @@ constexpr uint32_t kScaLdsMax = 160u * 1024u;      // gfx950's LDS per workgroup
 constexpr int kRecFwd = 8;
 constexpr int kRecBwd = 12;
 constexpr int kSlotPad = 4;
-// Backward row merge, per wavefront: a chunk has lph * spw * 4 = 256 (slot,
-// point, tap) rows.  An open-addressing table of 256 keys (tap offsets) with
-// the head of each key's member list, the members' links, the list of keys
-// in use and its length: 256 + 256 dwords, 2 x 256 halfwords, one counter.
+// Backward row merge, per workgroup: a chunk has lph * spw * 4 = 256 (point,
+// slot, tap) rows per wavefront.  An open-addressing table of 256 keys (tap
+// offsets) per wavefront with the head of each key's member list, the
+// members' links, the list of keys in use and its length: per wavefront
+// 256 + 256 dwords and 2 x 256 halfwords, and one counter.
 constexpr int kMrgRows = 4 * kScaWave;
-constexpr int kMrgWords = 2 * kMrgRows + kMrgRows + 4;
+constexpr int kMrgWaveBytes = kMrgRows * 12;
 constexpr uint32_t kMrgEmpty = 0xFFFFFFFFu;   // no key (tap offsets are below 2^31)
 constexpr uint32_t kMrgEnd = 0xFFFFFFFFu;     // end of a member list
+constexpr uint16_t kMrgEnd16 = 0xFFFFu;       // the same, as a stored link
 
 struct ScaParams {
     const void *value;
@@ -96,7 +98,7 @@ struct ScaParams {
     int32_t lph_shift;       // log2(lph)
     int32_t spw;             // slots per wavefront
     int32_t tile_pairs;      // forward: (query, head) pairs per workgroup
-    int32_t head_groups;     // backward: tiles of one query group (heads / waves, rounded up)
+    int32_t mrg_shift;       // backward: 32 - log2(rows of the merge table)
     int32_t tiles_per_b;
     int32_t stripe;          // consecutive tiles an XCD takes in turn (about one block)
     int32_t nq_max;          // queries a tile can touch
@@ -116,10 +118,12 @@ struct ScaParams {
 };
 
 // LDS: camera matrices [N][12]; level table [5][LMAX]; anchors [Z];
-// reference points [nq_max][N][Z] float2; hit masks [nq_max]; forward only:
+// reference points [nq_max][N][Z] float2; hit masks [nq_max] and their union;
+// forward only:
 // attention weights [waves][spw][LP]; backward only: output-gradient rows
 // [waves][spw][D]; chunk records [waves][spw][slot_stride]; backward only:
-// row-merge tables [waves][kMrgWords].
+// the row-merge table (keys, list heads [waves * 256] dwords; links, keys in
+// use [waves * 256] halfwords; a counter).
 struct ScaLds {
     uint32_t mat, lvl, z, ref, hit, att, gst, tap, mrg, total;
 };
@@ -135,11 +139,11 @@ __host__ ScaLds sca_lds_layout(int N, int Z, int nq_max, int waves, int spw, int
     s.lvl = o; o = sca_align16(o + 5u * FLASHSCA_LMAX * 4u);
     s.z = o; o = sca_align16(o + (uint32_t)Z * 4u);
     s.ref = o; o = sca_align16(o + (uint32_t)nq_max * N * Z * 8u);
-    s.hit = o; o = sca_align16(o + (uint32_t)nq_max * 4u);
+    s.hit = o; o = sca_align16(o + (uint32_t)(nq_max + 1) * 4u);
     s.att = o; o = sca_align16(o + (backward ? 0u : (uint32_t)waves * spw * LP * 4u));
     s.gst = o; o = sca_align16(o + (backward ? (uint32_t)waves * spw * D * 4u : 0u));
     s.tap = o; o = sca_align16(o + (uint32_t)waves * spw * slot_stride * 4u);
-    s.mrg = o; o = sca_align16(o + (backward ? (uint32_t)waves * kMrgWords * 4u : 0u));
+    s.mrg = o; o = sca_align16(o + (backward ? (uint32_t)waves * kMrgWaveBytes + 16u : 0u));
     s.total = o;
     return s;
 }
@@ -230,7 +234,8 @@ __device__ __forceinline__ int sca_tile(const ScaParams &p)
 }
 
 // Stage matrices, level table and anchors; phase 1: reference points and
-// hit masks of the tile's queries.  Ends with a workgroup barrier.
+// hit masks of the tile's queries and their union.  Ends with a workgroup
+// barrier.
 __device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSmem &m, int b,
                                                  int r_first, bool zorder = false)
 {
@@ -249,7 +254,7 @@ __device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSm
         m.lst[tid] = p.level_start[tid];
     }
     for (int t = tid; t < Z; t += nthreads) m.z[t] = p.z[t];
-    for (int t = tid; t < p.nq_max; t += nthreads) m.hit[t] = 0u;
+    for (int t = tid; t <= p.nq_max; t += nthreads) m.hit[t] = 0u;
     __syncthreads();
 
     for (int t = tid; t < p.nq_max * N; t += nthreads) {
@@ -275,7 +280,10 @@ __device__ __forceinline__ void sca_project_tile(const ScaParams &p, const ScaSm
             m.ref[(qi * N + n) * Z + k] = make_float2(un, vn);
             any |= in_front && un > 0.0f && un < 1.0f && vn > 0.0f && vn < 1.0f;
         }
-        if (any) atomicOr(&m.hit[qi], 1u << n);
+        if (any) {
+            atomicOr(&m.hit[qi], 1u << n);
+            atomicOr(&m.hit[p.nq_max], 1u << n);   // the tile's cameras
+        }
     }
     __syncthreads();
 }
@@ -313,26 +321,25 @@ __device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m
     return s;
 }
 
-// A slot of the backward.  Its tiles are head-major: a tile holds spw
-// consecutive queries (ranks r_first ..., in the Z order of query_of) and
-// `waves` heads, slot s of wavefront w being query r_first + s and head
-// hg * waves + w.  The slots of a wavefront then share their head and cover a
-// compact patch of cells, so their taps on one pixel are the same
-// value-gradient row and can be merged before the scatter (BEVFormer-base,
-// P = 8, per chunk of 8 points: 1.83x fewer rows for 1 x 8 strips of queries,
-// 2.05x for 2 x 4 patches, 2.85x for 4 x 4).
+// A slot of the backward.  A backward tile holds waves * spw consecutive
+// queries (ranks r_first ..., in the Z order of query_of) of one head, slot s
+// of wavefront w being query r_first + w spw + s.  All slots of the tile then
+// share their head and cover a compact patch of cells, so their taps on one
+// pixel are the same value-gradient row and are merged before the scatter
+// (BEVFormer-base, P = 8, per chunk of 8 points: 1.83x fewer rows for 1 x 8
+// strips of queries, 2.05x for 2 x 4 patches, 2.85x for 4 x 4, 3.85x for
+// 4 x 8).
 __device__ __forceinline__ ScaSlot sca_slot_bwd(const ScaParams &p, const ScaSmem &m, int b,
-                                                int r_first, int hg, int wave, int lane)
+                                                int r_first, int head, int wave, int lane)
 {
     ScaSlot s;
     s.sub = lane & (p.lph - 1);
     s.slot = lane >> p.lph_shift;
-    const int waves = (int)(blockDim.x / kScaWave);
-    const int rank = r_first + s.slot;
-    const int mh = hg * waves + wave;
-    s.active = rank < p.Q && mh < p.heads;
-    s.mh = s.active ? mh : 0;
-    s.qi = s.active ? s.slot : 0;
+    const int qi = wave * p.spw + s.slot;
+    const int rank = r_first + qi;
+    s.active = rank < p.Q;
+    s.mh = head;
+    s.qi = s.active ? qi : 0;
     int qx, qy;
     query_of(s.active ? rank : r_first, p.X, p.Y, qx, qy, true);
     s.q = qx * p.Y + qy;
@@ -550,21 +557,25 @@ sca_bwd(const ScaParams p)
     const ScaSmem m = sca_smem(p, smem);
     const int wave = threadIdx.x / kScaWave;
     const int lane = threadIdx.x % kScaWave;
+    const int tid = threadIdx.x;
+    const int nthreads = blockDim.x;
 
+    // tiles: (query group, head), the heads of a query group consecutive
     const int tile = sca_tile(p);
     const int b = tile / p.tiles_per_b;
     const int tb = tile - b * p.tiles_per_b;
-    const int qg = tb / p.head_groups;
-    const int r_first = qg * p.spw;
+    const int qg = tb / p.heads;
+    const int r_first = qg * (nthreads / kScaWave) * p.spw;
     sca_project_tile(p, m, b, r_first, true);
 
-    const ScaSlot s = sca_slot_bwd(p, m, b, r_first, tb - qg * p.head_groups, wave, lane);
+    const ScaSlot s = sca_slot_bwd(p, m, b, r_first, tb - qg * p.heads, wave, lane);
     const int lph = p.lph, LP = p.LP;
     const int slot_id = wave * p.spw + s.slot;
     // softmax a_j = expf(logit_j - mx) * rcp, recomputed where needed
     float mx, rcp;
     sca_softmax_stats(p, s, mx, rcp);
-    const uint32_t cams = sca_wave_cameras(p, s.hits);
+    // uniform over the workgroup: the cameras any of its queries hits
+    const uint32_t cams = m.hit[p.nq_max];
 
     // this lane's slice of the output gradient
     const int e0 = s.sub * EPV;
@@ -578,30 +589,30 @@ sca_bwd(const ScaParams p)
     const uint32_t lane_off = (uint32_t)s.sub * LW;
     const uint32_t head_off = (uint32_t)s.mh * p.head_bytes;
     uint32_t *rec = m.tap + (size_t)slot_id * p.slot_stride;
-    // the wavefront's output-gradient rows, for the value scatter
+    // the slots' output-gradient rows, for the value scatter
     const int D = p.D;
-    float *gst_w = m.gst + (size_t)wave * p.spw * D;
 #pragma unroll
     for (int e = 0; e < EPV; ++e)
-        if (e0 + e < D) gst_w[s.slot * D + e0 + e] = gs[e];
-    const uint32_t *rec_w = m.tap + (size_t)wave * p.spw * p.slot_stride;   // the wavefront's
+        if (e0 + e < D) m.gst[slot_id * D + e0 + e] = gs[e];
     const int spw_shift = __builtin_ctz((unsigned)p.spw);
-    // the wavefront's row-merge table, empty
-    uint32_t *tkey = m.mrg + (size_t)wave * kMrgWords;
-    uint32_t *thead = tkey + kMrgRows;
-    uint16_t *tnext = reinterpret_cast<uint16_t *>(thead + kMrgRows);
-    uint16_t *tuniq = tnext + kMrgRows;
-    uint32_t *tcount = thead + kMrgRows + kMrgRows;
-    for (int h = lane; h < kMrgRows; h += kScaWave) {
+    // the workgroup's row-merge table: row R = wavefront * 256 + (t spw + slot) 4 + tap
+    const int trows = (nthreads / kScaWave) * kMrgRows;
+    uint32_t *tkey = m.mrg;
+    uint32_t *thead = tkey + trows;
+    uint16_t *tnext = reinterpret_cast<uint16_t *>(thead + trows);
+    uint16_t *tuniq = tnext + trows;
+    uint32_t *tcount = reinterpret_cast<uint32_t *>(tuniq + trows);
+    for (int h = tid; h < trows; h += nthreads) {
         tkey[h] = kMrgEmpty;
         thead[h] = kMrgEnd;
     }
-    if (lane == 0) *tcount = 0u;
+    if (tid == 0) *tcount = 0u;
+    __syncthreads();
 
     // Chunks of lph points (lane sub owns point c0 + sub), each over the
-    // cameras the wavefront's slots hit.  The owner keeps its point's
-    // gradients in registers across the cameras, so no per-point state stays
-    // in LDS.
+    // cameras the tile's queries hit.  The owner keeps its point's gradients
+    // in registers across the cameras, so no per-point state stays in LDS.
+    // Both loops are uniform over the workgroup (its barriers need that).
     float dot = 0.0f;   // sum of a_j d a_j over this lane's points
     for (int c0 = 0; c0 < LP; c0 += lph) {
         const int j = c0 + s.sub;
@@ -664,26 +675,29 @@ sca_bwd(const ScaParams p)
                 my_dx += owner ? dx : 0.0f;
                 my_dy += owner ? dy : 0.0f;
             }
-            // value gradient: mean * a * w * G[c] onto each in-range tap.  The
-            // chunk's (point, slot, tap) rows r = (t spw + slot) 4 + tap go
-            // into the table by tap offset; rows on the same pixel (the
-            // slots share the head) land on one key and are summed before a
-            // single scatter of the key's row.  The wavefront then walks its
-            // distinct rows, 64 consecutive channels per atomic instruction,
-            // so one instruction covers whole head rows (one 128-byte row per
-            // 32 lanes for float32 D = 32).
+            g_da += my_da;
+            g_dx += my_dx;
+            g_dy += my_dy;
+            // value gradient: mean * a * w * G[c] onto each in-range tap.  Each
+            // wavefront puts its (point, slot, tap) rows into the table by tap
+            // offset; rows on the same pixel (all slots share the head) land
+            // on one key and are summed before a single scatter of the key's
+            // row.  The workgroup then walks the distinct rows, 64 consecutive
+            // channels per atomic instruction, so one instruction covers whole
+            // head rows (one 128-byte row per 32 lanes for float32 D = 32).
             if (gv) {
                 const int nrows = npts << (spw_shift + 2);
                 for (int r = lane; r < nrows; r += kScaWave) {
                     const int ts = r >> 2;
-                    const int sl = ts & (p.spw - 1);
-                    const uint32_t *rr = rec_w + (size_t)sl * p.slot_stride +
+                    const uint32_t *rr = m.tap +
+                                         (size_t)(wave * p.spw + (ts & (p.spw - 1))) * p.slot_stride +
                                          (ts >> spw_shift) * kRecBwd;
                     const uint32_t key = rr[r & 3];
                     if (key == kScaNoTap) continue;
-                    uint32_t h = (key * 0x9E3779B1u) >> 24;   // 256 buckets
+                    const uint32_t R = (uint32_t)(wave * kMrgRows + r);
+                    uint32_t h = (key * 0x9E3779B1u) >> p.mrg_shift;
                     bool placed = false;
-                    for (int probe = 0; probe < kMrgRows; ++probe) {
+                    for (int probe = 0; probe < trows; ++probe) {
                         const uint32_t old = atomicCAS(&tkey[h], kMrgEmpty, key);
                         if (old == kMrgEmpty) {
                             tuniq[atomicAdd(tcount, 1u)] = (uint16_t)h;
@@ -694,52 +708,53 @@ sca_bwd(const ScaParams p)
                             placed = true;
                             break;
                         }
-                        h = (h + 1) & (kMrgRows - 1);
+                        h = (h + 1) & (uint32_t)(trows - 1);
                     }
                     if (placed) {
-                        tnext[r] = (uint16_t)atomicExch(&thead[h], (uint32_t)r);
+                        tnext[R] = (uint16_t)atomicExch(&thead[h], R);
                     } else {
                         // unreachable (the table holds every row of a chunk);
                         // the row is then scattered alone
+                        const int sl = wave * p.spw + (ts & (p.spw - 1));
                         const float coef = __builtin_bit_cast(float, rr[10]) *
                                            __builtin_bit_cast(float, rr[4 + (r & 3)]);
                         for (int ch = 0; ch < D; ++ch)
-                            unsafeAtomicAdd(gv + key / ES + ch, coef * gst_w[sl * D + ch]);
+                            unsafeAtomicAdd(gv + key / ES + ch, coef * m.gst[sl * D + ch]);
                     }
                 }
-                wave_lds_sync();
+                __syncthreads();
                 const int nel = (int)*tcount * D;
-                for (int E = lane; E < nel; E += kScaWave) {
+                for (int E = tid; E < nel; E += nthreads) {
                     const int u = div_small(E, D, p.rcp_d);
                     const int ch = E - u * D;
-                    const uint32_t h = tuniq[u] & (kMrgRows - 1);
+                    const uint32_t h = tuniq[u] & (uint32_t)(trows - 1);
                     const uint32_t key = tkey[h];
-                    uint32_t r = thead[h];
+                    uint32_t R = thead[h];
                     float val = 0.0f;
-                    for (int k = 0; k < kMrgRows && r < (uint32_t)nrows; ++k) {
-                        const int ts = (int)(r >> 2);
-                        const int sl = ts & (p.spw - 1);
-                        const uint32_t *rr = rec_w + (size_t)sl * p.slot_stride +
+                    for (int k = 0; k < trows && R < (uint32_t)trows; ++k) {
+                        const int wv = (int)(R >> 8);              // R / kMrgRows
+                        const int ts = (int)((R & (kMrgRows - 1)) >> 2);
+                        const int sl = wv * p.spw + (ts & (p.spw - 1));
+                        const uint32_t *rr = m.tap + (size_t)sl * p.slot_stride +
                                              (ts >> spw_shift) * kRecBwd;
                         const float coef = __builtin_bit_cast(float, rr[10]) *
-                                           __builtin_bit_cast(float, rr[4 + (r & 3)]);
-                        val = fmaf(coef, gst_w[sl * D + ch], val);
-                        const uint32_t nx = tnext[r];
-                        r = (nx == 0xFFFFu) ? kMrgEnd : nx;
+                                           __builtin_bit_cast(float, rr[4 + (R & 3)]);
+                        val = fmaf(coef, m.gst[sl * D + ch], val);
+                        const uint16_t nx = tnext[R];
+                        R = (nx == kMrgEnd16) ? kMrgEnd : nx;
                     }
                     if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
                 }
-                wave_lds_sync();
-                for (int h = lane; h < kMrgRows; h += kScaWave) {
+                __syncthreads();
+                for (int h = tid; h < trows; h += nthreads) {
                     tkey[h] = kMrgEmpty;
                     thead[h] = kMrgEnd;
                 }
-                if (lane == 0) *tcount = 0u;
+                if (tid == 0) *tcount = 0u;
+                __syncthreads();
+            } else {
+                wave_lds_sync();
             }
-            g_da += my_da;
-            g_dx += my_dx;
-            g_dy += my_dy;
-            wave_lds_sync();
         }
         if (own) {
             dot += a_j * g_da;
@@ -941,16 +956,13 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     const int spw = kScaWave / lph;
     const int slot_stride = lph * (backward ? kRecBwd : kRecFwd) + kSlotPad;
 
-    // the backward's head-major tiles take one head per wavefront: no more
-    // wavefronts than heads
     int waves = kScaWavesMax;
-    if (backward && waves > v->heads) waves = v->heads >= 2 ? 2 : 1;
     int nq_max = 0;
     ScaLds lay{};
     for (;;) {
         const int tp = waves * spw;
-        // forward: tp consecutive (query, head) pairs; backward: spw queries
-        nq_max = backward ? spw : (tp - 1) / v->heads + 2;
+        // forward: tp consecutive (query, head) pairs; backward: tp queries
+        nq_max = backward ? tp : (tp - 1) / v->heads + 2;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
         lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, D, slot_stride, backward);
         if (lay.total <= kScaLdsBudget || waves == 1) break;
@@ -983,11 +995,15 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     p.spw = spw;
     p.tile_pairs = tile_pairs;
     const uint64_t pairs_b = Q * (uint64_t)v->heads;
-    p.head_groups = (v->heads + waves - 1) / waves;
-    // forward: tile_pairs consecutive pairs; backward: spw queries x `waves` heads
-    // (at most Q heads tiles, within 2^31 - 1)
-    p.tiles_per_b = backward ? (int32_t)(((Q + spw - 1) / spw) * (uint64_t)p.head_groups)
+    // forward: tile_pairs consecutive pairs; backward: tile_pairs queries of
+    // one head (at most Q heads tiles, within 2^31 - 1)
+    p.tiles_per_b = backward ? (int32_t)(((Q + tile_pairs - 1) / tile_pairs) * (uint64_t)v->heads)
                              : (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
+    {
+        int lg = 0;
+        while ((kMrgRows * waves) >> (lg + 1)) ++lg;
+        p.mrg_shift = 32 - lg;   // merge-table rows: 256 per wavefront
+    }
     {
         // one contiguous band of tiles per XCD (see sca_tile)
         const int64_t nt = (int64_t)v->B * p.tiles_per_b / kScaXcds;

@@ -253,3 +253,16 @@ def test_backward_launch_info_geometry():
     assert info["workgroups"] == 0
     with pytest.raises(fb.FlashBevError):
         fb.backward_launch_info((1, 6, 32, 88, 80), "f32", np.zeros(300), grid, (256, 704))
+
+
+@pytest.mark.parametrize("X,Y", [(1, 2**31 - 1), (2**31 - 1, 1), (2**31 - 64, 1), (1, 2**31 - 200)])
+def test_backward_plan_on_extreme_grid_sides(X, Y):
+    # a grid side near 2^31 must not overflow the tiled backward's tile count
+    # (found by the property test: 1 x (2^31 - 1) gave a negative count)
+    grid = fb.BevGrid(-50.0, 0.5, X, -50.0, 0.5, Y)
+    try:
+        info = fb.backward_launch_info((1, 1, 1, 1, 1), "f32", np.zeros(1, np.float32), grid, (1, 1))
+    except fb.FlashBevError as e:
+        assert e.status != 0
+        return
+    assert 0 < info["workgroups"] <= 2**31 - 1

@@ -207,12 +207,12 @@ def test_backward_launch_geometry():
              grid=fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), img_hw=(900, 1600), P=8)
     f = fb.sca_launch_info(**d)
     b = fb.sca_launch_info(**d, backward=True)
-    # same lanes and launch size; the backward's tiles are head-major (8
-    # queries x 4 heads, one head per wavefront) and it keeps output-gradient
-    # rows, wider chunk records and row-merge tables in LDS
+    # same lanes and launch size; a backward tile holds 32 queries (4
+    # wavefronts of 8) of one head, and the backward keeps output-gradient
+    # rows, wider chunk records and a row-merge table in LDS
     assert (b["workgroups"], b["lanes_per_head"], b["lane_bytes"], b["threads"]) == \
         (f["workgroups"], f["lanes_per_head"], f["lane_bytes"], f["threads"])
-    assert b["workgroups"] == (200 * 200 // 8) * (8 // 4)
+    assert b["workgroups"] == (200 * 200 // 32) * 8
     assert b["lds_bytes"] > f["lds_bytes"]
     # the backward keeps no per-point state in LDS: its size does not grow
     # with L * P, while the forward's attention weights do
@@ -220,12 +220,13 @@ def test_backward_launch_geometry():
     b2 = fb.sca_launch_info(**d2, backward=True)
     assert b2["lds_bytes"] == fb.sca_launch_info(**dict(d2, P=8), backward=True)["lds_bytes"]
     assert b2["threads"] == 256 and b2["lds_bytes"] <= 64 * 1024
-    # 16 queries (slots) per wavefront, one head each: Q / 16 tiles of 4 heads
-    assert b2["workgroups"] == 200 * 200 // 16
+    # 16 queries (slots) per wavefront, 64 per tile: Q / 64 tiles per head
+    assert b2["workgroups"] == 200 * 200 // 64 * 4
     # L * P = 512 with 16 slots per wavefront: the forward's attention
     # weights leave room for one wavefront within the 64 KiB budget
     f2 = fb.sca_launch_info(**d2)
     assert f2["threads"] == 64 and 32 * 1024 < f2["lds_bytes"] <= 64 * 1024
-    # fewer heads than wavefronts: one wavefront per head
+    # one head: still four wavefronts, of 4 queries each (D = 32 float32,
+    # 8-byte lanes), one head per tile
     b3 = fb.sca_launch_info(**dict(d, shape=(1, 6, 30825, 32), heads=1), backward=True)
-    assert b3["threads"] == 64
+    assert b3["threads"] == 256 and b3["workgroups"] == -(-200 * 200 // (4 * 64 // b3["lanes_per_head"]))
