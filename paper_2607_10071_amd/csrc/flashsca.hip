@@ -60,23 +60,25 @@ constexpr uint32_t kScaNoTap = 0x80000000u;
 constexpr uint64_t kScaCamBytesMax = 0x7FFFFFFFull;
 constexpr uint32_t kScaLdsBudget = 64u * 1024u;    // preferred dynamic LDS per workgroup
 constexpr uint32_t kScaLdsMax = 160u * 1024u;      // gfx950's LDS per workgroup
-// A chunk record per lane: 4 tap offsets and 4 weights (forward); the
-// backward adds the location's fractions and the point's attention weight
-// (12 dwords).  A 4-dword pad per slot puts the slots' broadcast reads in
-// different banks.
+// A chunk record per lane: 4 tap offsets and 4 weights (forward); 4 tap
+// offsets, the location's fractions and the point's scatter factor (mean *
+// a_j) in the backward, whose readers recompute the weights from the
+// fractions (8 dwords each).  A 4-dword pad per slot puts the slots'
+// broadcast reads in different banks.
 constexpr int kRecFwd = 8;
-constexpr int kRecBwd = 12;
+constexpr int kRecBwd = 8;
 constexpr int kSlotPad = 4;
 // Backward row merge, per workgroup: a chunk has lph * spw * 4 = 256 (point,
-// slot, tap) rows per wavefront.  An open-addressing table of 256 keys (tap
-// offsets) per wavefront with the head of each key's member list, the
-// members' links, the list of keys in use and its length: per wavefront
-// 256 + 256 dwords and 2 x 256 halfwords, and one counter.
+// slot, tap) rows per wavefront.  Per wavefront's 256 rows: an open-addressing
+// table of keys (tap offsets) with the head of each key's member list, and per
+// row its factor (mean * a * w) and a link word (offset of its slot's
+// output-gradient row << 16 | next member); the keys in use (halfwords) and
+// their number.
 constexpr int kMrgRows = 4 * kScaWave;
-constexpr int kMrgWaveBytes = kMrgRows * 12;
+constexpr int kMrgWaveBytes = kMrgRows * 18;
 constexpr uint32_t kMrgEmpty = 0xFFFFFFFFu;   // no key (tap offsets are below 2^31)
 constexpr uint32_t kMrgEnd = 0xFFFFFFFFu;     // end of a member list
-constexpr uint16_t kMrgEnd16 = 0xFFFFu;       // the same, as a stored link
+constexpr uint32_t kMrgEnd16 = 0xFFFFu;       // the same, as a stored link
 
 struct ScaParams {
     const void *value;
@@ -122,8 +124,8 @@ struct ScaParams {
 // forward only:
 // attention weights [waves][spw][LP]; backward only: output-gradient rows
 // [waves][spw][D]; chunk records [waves][spw][slot_stride]; backward only:
-// the row-merge table (keys, list heads [waves * 256] dwords; links, keys in
-// use [waves * 256] halfwords; a counter).
+// the row-merge table (keys, list heads, row factors, row links
+// [waves * 256] dwords; keys in use [waves * 256] halfwords; a counter).
 struct ScaLds {
     uint32_t mat, lvl, z, ref, hit, att, gst, tap, mrg, total;
 };
@@ -599,8 +601,9 @@ sca_bwd(const ScaParams p)
     const int trows = (nthreads / kScaWave) * kMrgRows;
     uint32_t *tkey = m.mrg;
     uint32_t *thead = tkey + trows;
-    uint16_t *tnext = reinterpret_cast<uint16_t *>(thead + trows);
-    uint16_t *tuniq = tnext + trows;
+    float *rcoef = reinterpret_cast<float *>(thead + trows);
+    uint32_t *rlink = reinterpret_cast<uint32_t *>(rcoef + trows);
+    uint16_t *tuniq = reinterpret_cast<uint16_t *>(rlink + trows);
     uint32_t *tcount = reinterpret_cast<uint32_t *>(tuniq + trows);
     for (int h = tid; h < trows; h += nthreads) {
         tkey[h] = kMrgEmpty;
@@ -627,25 +630,21 @@ sca_bwd(const ScaParams p)
             const float2 *ref = m.ref + (size_t)(s.qi * p.N + n) * p.Z;
             float *gv = p.grad_value ? p.grad_value + ((size_t)b * p.N + n) * p.cam_elems : nullptr;
             uint4 o = make_uint4(kScaNoTap, kScaNoTap, kScaNoTap, kScaNoTap);
-            float4 w = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             float ax = 0.0f, ay = 0.0f, aa = 0.0f;
             if (mine) {
-                if (sca_setup_point(p, m, ref, s, j, head_off, o, ax, ay)) {
-                    w = sca_weights(o, ax, ay, 1.0f);
+                if (sca_setup_point(p, m, ref, s, j, head_off, o, ax, ay))
                     aa = s.inv * a_j;   // the value scatter's factor: mean times a_j
-                }
             }
             uint32_t *mine_rec = rec + s.sub * kRecBwd;
             *reinterpret_cast<uint4 *>(mine_rec) = o;
-            *reinterpret_cast<float4 *>(mine_rec + 4) = w;
-            *reinterpret_cast<float4 *>(mine_rec + 8) = make_float4(ax, ay, aa, 0.0f);
+            *reinterpret_cast<float4 *>(mine_rec + 4) = make_float4(ax, ay, aa, 0.0f);
             wave_lds_sync();
             // gradients of the point this lane owns (point c0 + sub)
             float my_da = 0.0f, my_dx = 0.0f, my_dy = 0.0f;
             for (int t = 0; t < npts; ++t) {
                 const uint4 to = *reinterpret_cast<const uint4 *>(rec + t * kRecBwd);
-                const float4 tw = *reinterpret_cast<const float4 *>(rec + t * kRecBwd + 4);
-                const float4 tf = *reinterpret_cast<const float4 *>(rec + t * kRecBwd + 8);
+                const float4 tf = *reinterpret_cast<const float4 *>(rec + t * kRecBwd + 4);
+                const float4 tw = sca_weights(to, tf.x, tf.y, 1.0f);
                 Raw<LW> v0{}, v1{}, v2{}, v3{};
                 if (to.x != kScaNoTap) v0 = load_vec<LW>(rsrc, to.x + lane_off, 0);
                 if (to.y != kScaNoTap) v1 = load_vec<LW>(rsrc, to.y + lane_off, 0);
@@ -711,13 +710,23 @@ sca_bwd(const ScaParams p)
                         h = (h + 1) & (uint32_t)(trows - 1);
                     }
                     if (placed) {
-                        tnext[R] = (uint16_t)atomicExch(&thead[h], R);
+                        const int sl = wave * p.spw + (ts & (p.spw - 1));
+                        // the tap's bilinear weight, as sca_weights forms it
+                        const float fx = __builtin_bit_cast(float, rr[4]);
+                        const float fy = __builtin_bit_cast(float, rr[5]);
+                        const float wr = (r & 2) ? fy : 1.0f - fy;
+                        const float wc = (r & 1) ? fx : 1.0f - fx;
+                        rcoef[R] = __builtin_bit_cast(float, rr[6]) * (wr * wc);
+                        rlink[R] = ((uint32_t)(sl * D) << 16) |
+                                   (atomicExch(&thead[h], R) & kMrgEnd16);
                     } else {
                         // unreachable (the table holds every row of a chunk);
                         // the row is then scattered alone
                         const int sl = wave * p.spw + (ts & (p.spw - 1));
-                        const float coef = __builtin_bit_cast(float, rr[10]) *
-                                           __builtin_bit_cast(float, rr[4 + (r & 3)]);
+                        const float fx = __builtin_bit_cast(float, rr[4]);
+                        const float fy = __builtin_bit_cast(float, rr[5]);
+                        const float coef = __builtin_bit_cast(float, rr[6]) *
+                                           (((r & 2) ? fy : 1.0f - fy) * ((r & 1) ? fx : 1.0f - fx));
                         for (int ch = 0; ch < D; ++ch)
                             unsafeAtomicAdd(gv + key / ES + ch, coef * m.gst[sl * D + ch]);
                     }
@@ -732,15 +741,9 @@ sca_bwd(const ScaParams p)
                     uint32_t R = thead[h];
                     float val = 0.0f;
                     for (int k = 0; k < trows && R < (uint32_t)trows; ++k) {
-                        const int wv = (int)(R >> 8);              // R / kMrgRows
-                        const int ts = (int)((R & (kMrgRows - 1)) >> 2);
-                        const int sl = wv * p.spw + (ts & (p.spw - 1));
-                        const uint32_t *rr = m.tap + (size_t)sl * p.slot_stride +
-                                             (ts >> spw_shift) * kRecBwd;
-                        const float coef = __builtin_bit_cast(float, rr[10]) *
-                                           __builtin_bit_cast(float, rr[4 + (R & 3)]);
-                        val = fmaf(coef, m.gst[sl * D + ch], val);
-                        const uint16_t nx = tnext[R];
+                        const uint32_t lk = rlink[R];
+                        val = fmaf(rcoef[R], m.gst[(lk >> 16) + ch], val);
+                        const uint32_t nx = lk & kMrgEnd16;
                         R = (nx == kMrgEnd16) ? kMrgEnd : nx;
                     }
                     if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
@@ -971,6 +974,8 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     // many points per head: one wavefront per workgroup, with more LDS
     if (lay.total > kScaLdsMax) return FLASHBEV_ERR_UNSUPPORTED;
     const int tile_pairs = waves * spw;
+    // the backward's row links hold an output-gradient row offset in 16 bits
+    if (backward && (uint64_t)tile_pairs * D > 0xFFFFu) return FLASHBEV_ERR_UNSUPPORTED;
 
     ScaParams &p = pl->prm;
     memset(&p, 0, sizeof(p));
