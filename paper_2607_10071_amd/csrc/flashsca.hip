@@ -949,6 +949,11 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     // always a width dividing the head row, the full row and the base address
     int lw = 16;
     while (lw > es && (uint64_t)lw * 4 > head_bytes) lw >>= 1;
+    // the backward takes 8 lanes per head where it can (BEVFormer-base
+    // bfloat16, B = 2: 8-byte lanes 3.13 ms against 16-byte 3.53 ms at
+    // P = 8, 9.8 against 11.1 ms at P = 32): 8 queries per wavefront, 8
+    // points per chunk and the LDS of four workgroups per CU
+    if (backward) while (lw > es && (uint64_t)lw * 8 > head_bytes) lw >>= 1;
     while (lw > es && ((head_bytes % lw) != 0 || (row % lw) != 0 ||
                        (((uintptr_t)v->data) % lw) != 0))
         lw >>= 1;

@@ -220,8 +220,16 @@ def test_backward_launch_geometry():
     b2 = fb.sca_launch_info(**d2, backward=True)
     assert b2["lds_bytes"] == fb.sca_launch_info(**dict(d2, P=8), backward=True)["lds_bytes"]
     assert b2["threads"] == 256 and b2["lds_bytes"] <= 64 * 1024
-    # 16 queries (slots) per wavefront, 64 per tile: Q / 64 tiles per head
-    assert b2["workgroups"] == 200 * 200 // 64 * 4
+    # the backward takes 8 lanes per head where it can: D = 8 float32 in
+    # 4-byte lanes, 8 queries per wavefront, 32 per tile: Q / 32 tiles per head
+    assert (b2["lanes_per_head"], b2["lane_bytes"]) == (8, 4)
+    assert b2["workgroups"] == 200 * 200 // 32 * 4
+    # bfloat16 BEVFormer-base: 8-byte lanes in the backward, 16-byte ones in
+    # the forward
+    bb = fb.sca_launch_info(**dict(d, dtype="bf16"), backward=True)
+    fbf = fb.sca_launch_info(**dict(d, dtype="bf16"))
+    assert (bb["lanes_per_head"], bb["lane_bytes"]) == (8, 8)
+    assert (fbf["lanes_per_head"], fbf["lane_bytes"]) == (4, 16)
     # L * P = 512 with 16 slots per wavefront: the forward's attention
     # weights leave room for one wavefront within the 64 KiB budget
     f2 = fb.sca_launch_info(**d2)
