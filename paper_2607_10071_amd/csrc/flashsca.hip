@@ -740,11 +740,24 @@ sca_bwd(const ScaParams p)
                     const uint32_t key = tkey[h];
                     uint32_t R = thead[h];
                     float val = 0.0f;
-                    for (int k = 0; k < trows && R < (uint32_t)trows; ++k) {
-                        const uint32_t lk = rlink[R];
-                        val = fmaf(rcoef[R], m.gst[(lk >> 16) + ch], val);
-                        const uint32_t nx = lk & kMrgEnd16;
-                        R = (nx == kMrgEnd16) ? kMrgEnd : nx;
+                    if (R < (uint32_t)trows) {
+                        // the next member's link and factor are read while
+                        // this member's output-gradient element is
+                        uint32_t lk = rlink[R];
+                        float c = rcoef[R];
+                        for (int k = 0; k < trows; ++k) {
+                            const float g = m.gst[(lk >> 16) + ch];
+                            const uint32_t nx = lk & kMrgEnd16;
+                            const bool more = nx < (uint32_t)trows;
+                            const uint32_t Rn = more ? nx : R;
+                            const uint32_t lkn = rlink[Rn];
+                            const float cn = rcoef[Rn];
+                            val = fmaf(c, g, val);
+                            if (!more) break;
+                            R = Rn;
+                            lk = lkn;
+                            c = cn;
+                        }
                     }
                     if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
                 }
