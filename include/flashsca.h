@@ -135,14 +135,16 @@ int flashsca_forward(const flashsca_value *value, const float *lidar2img,
  *   grad_out       device, [B, X Y, C] float32, 4-byte aligned.
  *   grad_value     device, [B, N, S, C] float32 (whatever the value dtype),
  *                  4-byte aligned, or NULL to skip it.  Fully overwritten (a
- *                  fill kernel zeroes it first, on the same stream); the sum
- *                  over terms uses float32 atomic adds, so its rounding order
- *                  (not its terms) varies from run to run.
+ *                  fill kernel zeroes it first, on the same stream); terms
+ *                  on one value row are summed within a workgroup first and
+ *                  the sums added with float32 atomic adds, so the rounding
+ *                  order (not the terms) varies from run to run.
  *   grad_offsets   device, [B, X Y, heads, L, P, 2] float32, 8-byte aligned,
  *                  or NULL.  Every element written once (zero for queries no
  *                  camera sees).
  *   grad_logits    device, [B, X Y, heads, L, P] float32, 4-byte aligned, or
- *                  NULL.  Every element written once.
+ *                  NULL.  Every element written (it holds an intermediate
+ *                  until the call's kernel ends).
  *   stream         hipStream_t; NULL means the default stream.
  *
  * At least one gradient must be requested; outputs must not overlap the
