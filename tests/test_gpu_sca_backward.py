@@ -160,6 +160,23 @@ def test_sca_backward_degenerate_inputs(fb, device):
     assert np.all(gpu["offsets"] == 0.0) and np.all(gpu["logits"] == 0.0)
 
 
+@pytest.mark.parametrize("case", ["spread", "crowded"])
+def test_sca_backward_row_merge_extremes(fb, device, case):
+    """The value gradient's row merge at its extremes.  `spread`: offsets
+    uniform over a 116 x 200 map, so nearly every in-range (point, slot, tap)
+    row of a tile's chunk is a distinct pixel: about as many keys as rows in
+    the table, with long probe runs.  `crowded`: one 4 x 4 map, so the rows of 32 queries x 8
+    points x 4 taps pile onto 16 pixels per head and the member lists run
+    long."""
+    if case == "spread":
+        inst = small(10, levels=((116, 200),), C=256, heads=8, P=8, Z=4, X=16, Y=16)
+        rng = np.random.default_rng(10)
+        inst.offsets[...] = rng.uniform(-150.0, 150.0, inst.offsets.shape).astype(np.float32)
+    else:
+        inst = small(11, levels=((4, 4),), C=256, heads=8, P=8, Z=4, X=16, Y=16)
+    check(fb, inst, device, what=f"row merge {case}")
+
+
 def test_sca_backward_bevformer_base(fb, device):
     """Table 7's setting, P = 8, every gradient element checked."""
     inst = synth.make_sca_workload(synth.sca_config("sca_base"))
