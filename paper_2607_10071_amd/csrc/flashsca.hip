@@ -610,6 +610,9 @@ sca_bwd(const ScaParams p)
         thead[h] = kMrgEnd;
     }
     if (tid == 0) *tcount = 0u;
+    // the walk's first element (u0, ch0) and step (du, dch) in (row, channel)
+    const int u0 = div_small(tid, D, p.rcp_d), ch0 = tid - u0 * D;
+    const int du = div_small(nthreads, D, p.rcp_d), dch = nthreads - du * D;
     __syncthreads();
 
     // Chunks of lph points (lane sub owns point c0 + sub), each over the
@@ -733,9 +736,9 @@ sca_bwd(const ScaParams p)
                 }
                 __syncthreads();
                 const int nel = (int)*tcount * D;
+                // element E = u D + ch, stepped by nthreads = du D + dch
+                int u = u0, ch = ch0;
                 for (int E = tid; E < nel; E += nthreads) {
-                    const int u = div_small(E, D, p.rcp_d);
-                    const int ch = E - u * D;
                     const uint32_t h = tuniq[u] & (uint32_t)(trows - 1);
                     const uint32_t key = tkey[h];
                     uint32_t R = thead[h];
@@ -760,6 +763,12 @@ sca_bwd(const ScaParams p)
                         }
                     }
                     if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
+                    u += du;
+                    ch += dch;
+                    if (ch >= D) {
+                        ch -= D;
+                        ++u;
+                    }
                 }
                 __syncthreads();
                 for (int h = tid; h < trows; h += nthreads) {
