@@ -8,30 +8,39 @@
 //     (a power of two); lane `sub` of a slot holds one LW-byte slice of the
 //     head's D channels, so every bilinear tap of the head is one coalesced
 //     run of D * elem bytes across the slot's lanes.  A wavefront holds
-//     64 / lph slots; a workgroup a tile of consecutive pairs of one batch
-//     element, in a blocked visiting order of the queries (query_of).
+//     64 / lph slots.  Queries are visited in blocks (query_of, Z order
+//     inside a block).  A forward tile holds consecutive (query, head)
+//     pairs of one batch element (the heads of a few queries); a backward
+//     tile holds waves * spw consecutive queries of one head.
 //   * Phase 1 (workgroup): every (query, camera) pair of the tile projects the
 //     query's Z anchors (float32 recipe, IEEE divisions), records the
 //     normalized reference points in LDS and sets the camera's bit in the
-//     query's hit mask (LDS atomic OR).
+//     query's hit mask and in the tile's union (LDS atomic OR).
 //   * Phase 2 (slot): softmax over the head's L * P logits, read once per
-//     query (not once per camera), kept in the slot's LDS area.
-//   * Phase 3 (slot, per hit camera): in chunks of lph points, lane `sub`
+//     query (not once per camera): the forward keeps the weights in LDS, the
+//     backward keeps the maximum and 1 / sum and recomputes a weight where
+//     it needs one.
+//   * Phase 3 (slot): in chunks of lph points, per hit camera, lane `sub`
 //     sets up point c + sub (anchor k mod Z, location (u W_l + dx) - 1/2,
 //     floor, four tap offsets and bilinear weights) and publishes it in LDS;
 //     then all lanes of the slot load the chunk's lph * 4 taps with raw buffer
-//     loads.  A tap outside the map gets an offset past the end of the
-//     camera's buffer, so its load returns zero without a memory access.
-//       - forward: each lane accumulates its channels in float32;
-//       - backward: each lane forms its channels' share of the tap rows'
+//     loads.  A tap outside the map is not loaded.
+//       - forward (cameras outside, chunks inside): each lane accumulates its
+//         channels in float32;
+//       - backward (chunks outside, cameras inside, uniform over the
+//         workgroup): each lane forms its channels' share of the tap rows'
 //         dot products with the output gradient; a reduction across the slot
 //         gives the point's gradients of attention weight and location, kept
-//         by the lane that owns the point; the value gradient is scattered
-//         with float atomic adds.
+//         in registers by the lane that owns the point.  For the value
+//         gradient the workgroup merges the chunk's rows in an LDS table by
+//         tap offset (all slots share the head, so equal offsets are the same
+//         value-gradient row), sums each key's members and scatters one
+//         float atomic add per distinct row and channel.
 //   * Forward: each output element is written once, no atomics on global
 //     memory, no workspace, one launch.  Backward: a fill kernel zeroes the
-//     value gradient, then one launch; offset and logit gradients are
-//     written once each.
+//     value gradient, then one launch; every offset and logit gradient is
+//     written (the logit gradient holds d a_j until the slot's softmax
+//     backward finishes it).
 // Coordinates follow the float32 recipe of the conventions in flashsca.h, so
 // mask and floor decisions match the CPU oracle bit for bit: the file is
 // compiled with -ffp-contract=off and uses IEEE division.
@@ -99,7 +108,8 @@ struct ScaParams {
     int32_t lph;             // lanes per slot (power of two)
     int32_t lph_shift;       // log2(lph)
     int32_t spw;             // slots per wavefront
-    int32_t tile_pairs;      // forward: (query, head) pairs per workgroup
+    int32_t tile_pairs;      // slots per workgroup: forward (query, head) pairs,
+                             // backward queries (of one head)
     int32_t mrg_shift;       // backward: 32 - log2(rows of the merge table)
     int32_t tiles_per_b;
     int32_t stripe;          // consecutive tiles an XCD takes in turn (about one block)
