@@ -193,23 +193,11 @@ def sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int
     """
     import torch
 
-    if features.dim() != 5:
-        raise ValueError("features must be [B, N, H, W, C]")
-    if not features.is_cuda or not lidar2img.is_cuda:
-        raise ValueError("features and lidar2img must be device tensors")
-    if not features.is_contiguous():
-        raise ValueError("features must be contiguous (channel-last NHWC)")
-    if lidar2img.dtype != torch.float32 or not lidar2img.is_contiguous():
-        raise ValueError("lidar2img must be a contiguous float32 tensor")
+    _check_forward(features, lidar2img, grid)
     B, N, H, W, C = features.shape
-    if tuple(lidar2img.shape) != (B, N, 4, 4):
-        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
     if out is None:
         out = torch.empty((B, C, grid.X, grid.Y), dtype=torch.float32, device=features.device)
-    else:
-        if out.dtype != torch.float32 or not out.is_contiguous() or \
-                tuple(out.shape) != (B, C, grid.X, grid.Y):
-            raise ValueError(f"out must be a contiguous float32 tensor [{B}, {C}, {grid.X}, {grid.Y}]")
+    _check_out(out, (B, C, grid.X, grid.Y), "out")
     z = _z_array(z_bins)
     f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
                         grid, z, reduce)
@@ -222,6 +210,52 @@ def sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int
     if rc != 0:
         raise FlashBevError(rc)
     return out
+
+
+def _check_forward(features, lidar2img, grid: BevGrid) -> None:
+    """The forward's tensor checks (sample_vt and prepare_sample_vt): the C
+    call reads these tensors as raw device memory of the stated shape."""
+    if features.dim() != 5:
+        raise ValueError("features must be [B, N, H, W, C]")
+    if not features.is_cuda or not lidar2img.is_cuda:
+        raise ValueError("features and lidar2img must be device tensors")
+    if not features.is_contiguous():
+        raise ValueError("features must be contiguous (channel-last NHWC)")
+    _dtype_code(features)
+    _check_matrices(lidar2img, features.shape[0], features.shape[1])
+
+
+def _check_matrices(lidar2img, B: int, N: int) -> None:
+    import torch
+
+    if lidar2img.dtype != torch.float32 or not lidar2img.is_contiguous():
+        raise ValueError("lidar2img must be a contiguous float32 tensor")
+    if tuple(lidar2img.shape) != (B, N, 4, 4):
+        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
+
+
+def _check_out(t, shape, name: str) -> None:
+    """A float32 contiguous device tensor of exactly ``shape``."""
+    import torch
+
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be a contiguous float32 tensor "
+                         f"[{', '.join(str(int(v)) for v in shape)}]")
+
+
+def _check_backward(grad_out, lidar2img, grid: BevGrid, features_shape):
+    """The backward's tensor checks (sample_vt_backward and
+    prepare_sample_vt_backward); returns (B, N, H, W, C)."""
+    if len(tuple(features_shape)) != 5:
+        raise ValueError("features_shape must be (B, N, H, W, C)")
+    B, N, H, W, C = (int(v) for v in features_shape)
+    if not grad_out.is_cuda or not lidar2img.is_cuda:
+        raise ValueError("grad_out and lidar2img must be device tensors")
+    _check_out(grad_out, (B, C, grid.X, grid.Y), "grad_out")
+    _check_matrices(lidar2img, B, N)
+    return B, N, H, W, C
 
 
 def _stream_handle(stream, device):
@@ -271,22 +305,10 @@ def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple
     """
     import torch
 
-    if not grad_out.is_cuda or not lidar2img.is_cuda:
-        raise ValueError("grad_out and lidar2img must be device tensors")
-    if grad_out.dtype != torch.float32 or not grad_out.is_contiguous():
-        raise ValueError("grad_out must be a contiguous float32 tensor")
-    if lidar2img.dtype != torch.float32 or not lidar2img.is_contiguous():
-        raise ValueError("lidar2img must be a contiguous float32 tensor")
-    B, N, H, W, C = (int(v) for v in features_shape)
-    if tuple(grad_out.shape) != (B, C, grid.X, grid.Y):
-        raise ValueError(f"grad_out must be [{B}, {C}, {grid.X}, {grid.Y}]")
-    if tuple(lidar2img.shape) != (B, N, 4, 4):
-        raise ValueError(f"lidar2img must be [{B}, {N}, 4, 4]")
+    B, N, H, W, C = _check_backward(grad_out, lidar2img, grid, features_shape)
     if grad_features is None:
         grad_features = torch.empty((B, N, H, W, C), dtype=torch.float32, device=grad_out.device)
-    elif grad_features.dtype != torch.float32 or not grad_features.is_contiguous() or \
-            tuple(grad_features.shape) != (B, N, H, W, C):
-        raise ValueError(f"grad_features must be a contiguous float32 tensor [{B}, {N}, {H}, {W}, {C}]")
+    _check_out(grad_features, (B, N, H, W, C), "grad_features")
     if not isinstance(features_dtype, str):
         features_dtype = {torch.float32: "f32", torch.float16: "f16",
                           torch.bfloat16: "bf16"}[features_dtype]
@@ -400,14 +422,9 @@ def prepare_sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw, out,
                       reduce: str = "mean", stream=None) -> _Prepared:
     """``sample_vt`` with every argument fixed: returns a callable that
     enqueues the same forward call again (same tensors, same stream)."""
-    import torch
-
+    _check_forward(features, lidar2img, grid)
     B, N, H, W, C = features.shape
-    if not (features.is_cuda and lidar2img.is_cuda and out.is_cuda):
-        raise ValueError("features, lidar2img and out must be device tensors")
-    if out.dtype != torch.float32 or not out.is_contiguous() or \
-            tuple(out.shape) != (B, C, grid.X, grid.Y):
-        raise ValueError(f"out must be a contiguous float32 tensor [{B}, {C}, {grid.X}, {grid.Y}]")
+    _check_out(out, (B, C, grid.X, grid.Y), "out")
     z = _z_array(z_bins)
     f, g, zb = _structs(features.shape, _dtype_code(features), features.data_ptr(), img_hw,
                         grid, z, reduce)
@@ -425,12 +442,8 @@ def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_h
     """``sample_vt_backward`` with every argument fixed (see prepare_sample_vt)."""
     import torch
 
-    B, N, H, W, C = (int(v) for v in features_shape)
-    if not (grad_out.is_cuda and lidar2img.is_cuda and grad_features.is_cuda):
-        raise ValueError("grad_out, lidar2img and grad_features must be device tensors")
-    if grad_features.dtype != torch.float32 or not grad_features.is_contiguous() or \
-            tuple(grad_features.shape) != (B, N, H, W, C):
-        raise ValueError(f"grad_features must be a contiguous float32 tensor [{B}, {N}, {H}, {W}, {C}]")
+    B, N, H, W, C = _check_backward(grad_out, lidar2img, grid, features_shape)
+    _check_out(grad_features, (B, N, H, W, C), "grad_features")
     if not isinstance(features_dtype, str):
         features_dtype = {torch.float32: "f32", torch.float16: "f16",
                           torch.bfloat16: "bf16"}[features_dtype]

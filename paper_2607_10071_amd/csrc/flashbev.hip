@@ -1113,11 +1113,14 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     const int es = (f->dtype == FLASHBEV_F32) ? 4 : 2;
     const uint64_t row = (uint64_t)f->C * es;
     if (row > FLASHBEV_ROW_BYTES_MAX) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t feat_bytes = (uint64_t)f->B * f->N * f->H * f->W * row;
+    // every size product saturates instead of wrapping (size_prod)
+    const uint64_t feat_bytes =
+        size_prod({(uint64_t)f->B, (uint64_t)f->N, (uint64_t)f->H, (uint64_t)f->W, row});
     if (feat_bytes > kFeatBytesMax) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t XY = (uint64_t)s->X * s->Y;
+    const uint64_t XY = size_prod({(uint64_t)s->X, (uint64_t)s->Y});
     if (XY > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t out_elems = (uint64_t)f->B * f->C * XY;
+    const uint64_t out_elems = size_prod({(uint64_t)f->B, (uint64_t)f->C, XY});
+    if (out_elems > kSizeCap / 4) return FLASHBEV_ERR_UNSUPPORTED;
     const bool empty = out_elems == 0;
     if (zb->Z > 0 && !zb->z) return FLASHBEV_ERR_NULLPTR;
     if (need_data && !empty) {
@@ -1163,7 +1166,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     // 1.44 -> 1.99 ms, where per-workgroup set-up dominates)
     int rounds = (kCellsPerWave + cpw - 1) / cpw;
     if ((cpw <= 2 || vpl >= 2) &&
-        (uint64_t)f->B * (uint64_t)s->X * (uint64_t)s->Y <= (uint64_t)waves * cpw * kOneRoundTilesMax)
+        size_prod({(uint64_t)f->B, XY}) <= (uint64_t)waves * cpw * kOneRoundTilesMax)
         rounds = 1;
     // heights per projection pass; a cell's list holds one pass's valid
     // samples (at most zc N <= 64), padded to whole gather iterations
@@ -1204,7 +1207,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.x_min = s->x_min; p.dx = s->dx; p.y_min = s->y_min; p.dy = s->dy;
     p.depth_eps = s->depth_eps;
     p.reduce = s->reduce;
-    p.bands = ((uint64_t)f->B * XY * (uint64_t)zb->Z * row <= kBandsWorkMax) ? 1 : 0;
+    p.bands = (size_prod({(uint64_t)f->B, XY, (uint64_t)zb->Z, row}) <= kBandsWorkMax) ? 1 : 0;
     p.row_bytes = (uint32_t)row;
     p.step_x = f->W >= 2 ? (uint32_t)row : 0u;
     p.step_y = f->H >= 2 ? (uint32_t)(row * f->W) : 0u;
@@ -1290,11 +1293,14 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
         return FLASHBEV_ERR_VALUE;
     const int es = (f->dtype == FLASHBEV_F32) ? 4 : 2;
     if ((uint64_t)f->C * es > FLASHBEV_ROW_BYTES_MAX) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t gelems = (uint64_t)f->B * f->N * f->H * f->W * f->C;
+    // every size product saturates instead of wrapping (size_prod)
+    const uint64_t gelems = size_prod(
+        {(uint64_t)f->B, (uint64_t)f->N, (uint64_t)f->H, (uint64_t)f->W, (uint64_t)f->C});
     if (gelems > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t XY = (uint64_t)s->X * s->Y;
+    const uint64_t XY = size_prod({(uint64_t)s->X, (uint64_t)s->Y});
     if (XY > 0x7FFFFFFFull) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t out_elems = (uint64_t)f->B * f->C * XY;
+    const uint64_t out_elems = size_prod({(uint64_t)f->B, (uint64_t)f->C, XY});
+    if (out_elems > kSizeCap / 4) return FLASHBEV_ERR_UNSUPPORTED;
     if (zb->Z > 0 && !zb->z) return FLASHBEV_ERR_NULLPTR;
     if (need_data && gelems > 0) {
         if (!gfeat) return FLASHBEV_ERR_NULLPTR;
@@ -1338,7 +1344,7 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     // table, the pass's sorted term list (sized for the pass's largest
     // possible number of terms) and as many per-pixel rows as the budget
     // leaves
-    const uint64_t npix = (uint64_t)f->N * f->H * f->W;
+    const uint64_t npix = size_prod({(uint64_t)f->N, (uint64_t)f->H, (uint64_t)f->W});
     bool tiled = false;
     int t_waves = 0, t_tx = 0, t_ty = 0, t_cap = 0, t_zc = 0;
     uint32_t t_mask = 0, l_slot = 0, l_tbl = 0, l_spix = 0, l_acc = 0, l_cnt = 0, l_total = 0;
@@ -1348,7 +1354,7 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     // rows up to kBwdTiledCMax channels (wider ones leave too few LDS rows);
     // grid sides that leave a tile's cell coordinates (side + tile side)
     // within int32
-    if (npix + 1 < (1u << kKeyBits) && f->C <= kBwdTiledCMax && f->N > 0 &&
+    if (npix < (1u << kKeyBits) - 1u && f->C <= kBwdTiledCMax && f->N > 0 &&
         (uint64_t)s->X + 2u * kWave < 0x7FFFFFFFull && (uint64_t)s->Y + 2u * kWave < 0x7FFFFFFFull) {
         t_waves = kBwdTileWaves;
         const int T = t_waves * cpw;

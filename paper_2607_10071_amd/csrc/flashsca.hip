@@ -904,10 +904,14 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
         return FLASHBEV_ERR_SHAPE;
     if (v->C % v->heads != 0 || P % zb->Z != 0) return FLASHBEV_ERR_SHAPE;
     if (v->L > FLASHSCA_LMAX) return FLASHBEV_ERR_UNSUPPORTED;
+    // every size product saturates instead of wrapping (size_prod); the
+    // level areas are each below 2^62, so their sum of at most
+    // FLASHSCA_LMAX terms is checked against the cap before it could wrap
     uint64_t S = 0;
-    for (int l = 0; l < v->L; ++l) {
+    for (int l = 0; l < v->L && l < FLASHSCA_LMAX; ++l) {
         if (v->level_h[l] < 1 || v->level_w[l] < 1) return FLASHBEV_ERR_SHAPE;
-        S += (uint64_t)v->level_h[l] * (uint64_t)v->level_w[l];
+        S += size_prod({(uint64_t)v->level_h[l], (uint64_t)v->level_w[l]});
+        if (S > kSizeCap) return FLASHBEV_ERR_UNSUPPORTED;
     }
     if (v->N > FLASHSCA_NMAX || zb->Z > FLASHSCA_ZMAX || (int64_t)v->L * P > FLASHSCA_LPMAX)
         return FLASHBEV_ERR_UNSUPPORTED;
@@ -922,16 +926,19 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     const uint64_t head_bytes = (uint64_t)D * es;
     const uint64_t row = (uint64_t)v->C * es;
     if (head_bytes > FLASHSCA_HEAD_BYTES_MAX) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t cam_bytes = S * row;
+    const uint64_t cam_bytes = size_prod({S, row});
     if (cam_bytes > kScaCamBytesMax) return FLASHBEV_ERR_UNSUPPORTED;
-    const uint64_t Q = (uint64_t)s->X * s->Y;
-    if (Q > 0x7FFFFFFFull || Q * (uint64_t)v->heads > 0x7FFFFFFFull)
+    const uint64_t Q = size_prod({(uint64_t)s->X, (uint64_t)s->Y});
+    if (Q > 0x7FFFFFFFull || size_prod({Q, (uint64_t)v->heads}) > 0x7FFFFFFFull)
         return FLASHBEV_ERR_UNSUPPORTED;
     const int LP = v->L * P;
-    const uint64_t out_elems = (uint64_t)v->B * Q * v->C;
-    const uint64_t value_elems = (uint64_t)v->B * v->N * S * v->C;
+    const uint64_t out_elems = size_prod({(uint64_t)v->B, Q, (uint64_t)v->C});
+    const uint64_t value_elems = size_prod({(uint64_t)v->B, (uint64_t)v->N, S, (uint64_t)v->C});
+    const uint64_t pts = size_prod({(uint64_t)v->B, Q, (uint64_t)v->heads, (uint64_t)LP});
+    // byte sizes below (x 8 at most) stay inside 64 bits
+    if (out_elems > kSizeCap / 8 || value_elems > kSizeCap / 8 || pts > kSizeCap / 8)
+        return FLASHBEV_ERR_UNSUPPORTED;
     const uint64_t value_bytes = value_elems * es;
-    const uint64_t pts = (uint64_t)v->B * Q * v->heads * LP;
     // forward: nothing to do without outputs; backward: a requested value
     // gradient is still zeroed
     const bool empty = out_elems == 0;

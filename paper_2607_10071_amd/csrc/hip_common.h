@@ -1,10 +1,13 @@
-// Device helpers shared by the library's kernels (flashbev.hip, flashsca.hip):
+// Helpers shared by the library's kernels (flashbev.hip, flashsca.hip):
 // 16/8/4/2-byte buffer loads, exact conversion of stored elements to
-// float32, wavefront-local LDS ordering and a small exact integer division.
+// float32, wavefront-local LDS ordering, a small exact integer division, and
+// on the host a size product that cannot wrap.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <initializer_list>
 
 #include "flashbev.h"
 
@@ -74,6 +77,27 @@ __device__ __forceinline__ int div_small(int a, int d, float rcp)
     q += (r >= d) ? 1 : 0;
     q -= (r < 0) ? 1 : 0;
     return q;
+}
+
+// ---------------------------------------------------------------------------
+// host: sizes
+// ---------------------------------------------------------------------------
+// Product of non-negative sizes that cannot wrap: the exact product while
+// every partial product stays at most kSizeCap (2^62), else kSizeOver, which
+// every size limit of the library rejects.  A zero factor gives zero.
+constexpr uint64_t kSizeCap = 1ull << 62;
+constexpr uint64_t kSizeOver = ~0ull;
+
+inline uint64_t size_prod(std::initializer_list<uint64_t> factors)
+{
+    for (const uint64_t v : factors)
+        if (v == 0) return 0;
+    uint64_t p = 1;
+    for (const uint64_t v : factors) {
+        if (p > kSizeCap / v) return kSizeOver;
+        p *= v;
+    }
+    return p;
 }
 
 }  // namespace

@@ -155,6 +155,26 @@ def test_argument_errors_before_any_hip_call(kw, status):
     assert call(**kw) == S[status]
 
 
+def test_size_products_do_not_wrap():
+    # B N H W C s = 2^15 * 2^20 * 2^20 * 512 wraps 64 bits to 0: the call must
+    # refuse it, not launch with an empty buffer and report success
+    assert call(shape=(2**15, 1, 2**20, 2**20, 128), X=1, Y=1) == S["ERR_UNSUPPORTED"]
+    # no features (N = 0) but B C X Y = 2^30 * 1024 * 2^30 output elements
+    assert call(shape=(2**30, 0, 1, 1, 1024), X=2**15, Y=2**15) == S["ERR_UNSUPPORTED"]
+    # the backward: B N H W C = 2^15 * 2^40 * 512 = 2^64 gradient elements
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32)
+    grid = fb.BevGrid(-50.0, 0.5, 1, -50.0, 0.5, 1)
+    rc = fb.sample_vt_backward_raw((2**15, 1, 2**20, 2**20, 512), "f32", L2I, z, grid,
+                                   (256, 704), OUT, FEAT)
+    assert rc == S["ERR_UNSUPPORTED"]
+    rc = fb.sample_vt_backward_raw((2**30, 0, 1, 1, 512), "f32", L2I, z,
+                                   fb.BevGrid(-50.0, 0.5, 2**15, -50.0, 0.5, 2**15),
+                                   (256, 704), OUT, FEAT)
+    assert rc == S["ERR_UNSUPPORTED"]
+    with pytest.raises(fb.FlashBevError):
+        fb.launch_info((2**15, 1, 2**20, 2**20, 128), "f32", z, grid, (256, 704))
+
+
 def test_empty_outputs_enqueue_nothing():
     # nothing to write: returns OK without touching HIP (this box has no GPU)
     assert call(X=0) == S["OK"]
@@ -210,6 +230,65 @@ def test_binding_rejects_host_tensors():
         fb.prepare_sample_vt_backward(torch.zeros(1, 4, 2, 2), m, [0.0],
                                       fb.BevGrid(-1, 1, 2, -1, 1, 2), (8, 8), (1, 1, 2, 2, 4),
                                       "f32", f)
+
+
+class _OnDevice:
+    """A host tensor that reports itself as a device tensor: the binding's
+    checks read only its shape, dtype, layout and device flag, and each case
+    below must be rejected by them before any pointer is taken."""
+
+    def __init__(self, t):
+        self._t = t
+        self.is_cuda = True
+        self.device = t.device
+
+    def __getattr__(self, name):
+        return getattr(self._t, name)
+
+    def data_ptr(self):
+        raise AssertionError("a malformed tensor reached the C call")
+
+
+def test_prepared_calls_reject_malformed_tensors():
+    import torch
+    D = _OnDevice
+    grid = fb.BevGrid(-1, 1, 2, -1, 1, 3)
+    feats = D(torch.zeros(1, 2, 4, 4, 8))
+    l2i = D(torch.zeros(1, 2, 4, 4))
+    out = D(torch.zeros(1, 8, 2, 3))
+    gout = D(torch.zeros(1, 8, 2, 3))
+    gfeat = D(torch.zeros(1, 2, 4, 4, 8))
+    bad_fwd = [
+        ("features", D(torch.zeros(1, 2, 4, 8, 4).transpose(3, 4))),   # strided
+        ("features", D(torch.zeros(1, 2, 4, 4, 8, dtype=torch.float64))),
+        ("lidar2img", D(torch.zeros(1, 2, 3, 4))),
+        ("lidar2img", D(torch.zeros(1, 2, 4, 4, dtype=torch.float64))),
+        ("lidar2img", D(torch.zeros(1, 2, 4, 4).transpose(2, 3))),
+        ("out", D(torch.zeros(1, 8, 3, 2))),
+        ("out", D(torch.zeros(1, 8, 3, 2).transpose(2, 3))),
+    ]
+    for name, t in bad_fwd:
+        kw = {"features": feats, "lidar2img": l2i, "out": out, name: t}
+        for fn in (fb.prepare_sample_vt, fb.sample_vt):
+            with pytest.raises((ValueError, TypeError)):
+                fn(kw["features"], kw["lidar2img"], [0.0], grid, (8, 8), out=kw["out"])
+    bad_bwd = [
+        ("grad_out", D(torch.zeros(1, 8, 3, 2))),
+        ("grad_out", D(torch.zeros(1, 8, 3, 2).transpose(2, 3))),
+        ("grad_out", D(torch.zeros(1, 8, 2, 3, dtype=torch.float16))),
+        ("lidar2img", D(torch.zeros(1, 2, 3, 4))),
+        ("lidar2img", D(torch.zeros(1, 2, 4, 4, dtype=torch.float64))),
+        ("grad_features", D(torch.zeros(1, 2, 4, 4, 4))),
+        ("grad_features", D(torch.zeros(1, 2, 4, 8, 4).transpose(3, 4))),
+    ]
+    for name, t in bad_bwd:
+        kw = {"grad_out": gout, "lidar2img": l2i, "grad_features": gfeat, name: t}
+        with pytest.raises(ValueError):
+            fb.prepare_sample_vt_backward(kw["grad_out"], kw["lidar2img"], [0.0], grid, (8, 8),
+                                          (1, 2, 4, 4, 8), "f32", kw["grad_features"])
+        with pytest.raises(ValueError):
+            fb.sample_vt_backward(kw["grad_out"], kw["lidar2img"], [0.0], grid, (8, 8),
+                                  (1, 2, 4, 4, 8), "f32", kw["grad_features"])
 
 
 def test_binding_requires_one_device_per_call():

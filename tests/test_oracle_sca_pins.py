@@ -381,3 +381,56 @@ def test_terms_count_in_range_taps():
     assert int(terms.sum()) == cnt["taps"] > 0
     wl = inst.wl
     assert terms.max() <= wl.N * wl.L * wl.P * 4
+
+
+@pytest.mark.parametrize("which", ["tiny", "small", "wide_z"])
+def test_reference_points_equal_the_dense_projection(which):
+    """The oracle's reference points (step 1: every anchor projected into
+    every camera, normalized by the image size) and their masks against the
+    dense path's float64 projection, independent code.  Masks and hit
+    cameras agree exactly on robust queries; the float32 coordinates agree
+    within their rounding bound, including the depth-clamped points of
+    anchors behind a camera (an invalid anchor of a hit camera still
+    samples)."""
+    inst = {"tiny": lambda: synth.make_sca_workload(synth.sca_config("sca_tiny")),
+            "small": lambda: small_sca(11),
+            "wide_z": lambda: small_sca(12, Z=4, P=8, z_lo=-9.0, z_hi=6.0)}[which]()
+    wl = inst.wl
+    un, vn, valid, hit = oracle.sca_reference_points(
+        inst.lidar2img, inst.z, wl.B, wl.N, (wl.img_h, wl.img_w), wl.X, wl.Y, wl.x_min, wl.dx,
+        wl.y_min, wl.dy, wl.depth_eps)
+    eps32 = float(np.float32(wl.depth_eps))
+    ref, dvalid, depth = anchors_in_cameras(inst.lidar2img, inst.z, wl.X, wl.Y, wl.x_min, wl.dx,
+                                            wl.y_min, wl.dy, (wl.img_h, wl.img_w), eps32)
+    # dense layout [B, N, Q, Z] -> the oracle's [B, Q, N, Z]
+    ref = ref.numpy().transpose(0, 2, 1, 3, 4)
+    dvalid = dvalid.numpy().transpose(0, 2, 1, 3)
+    depth = depth.numpy().transpose(0, 2, 1, 3)
+    keep = robust_queries(inst.lidar2img, inst.z, wl.X, wl.Y, wl.x_min, wl.dx, wl.y_min, wl.dy,
+                          (wl.img_h, wl.img_w), eps32)
+    assert keep.mean() > 0.9
+    assert np.array_equal(valid[keep], dvalid[keep])
+    assert np.array_equal(hit[keep], dvalid.any(axis=-1)[keep])
+    assert dvalid[keep].any() and not dvalid[keep].all() and (depth <= eps32).any()
+    # rounding bound of the float32 recipe on robust queries (no depth near
+    # the clamp): the cell centre carries 3 roundings and each of (u', v', d)
+    # 3 more of its term magnitudes; the divides and the normalization one
+    # each
+    # cell centres are formed in float32 as well, so their magnitude terms
+    # are |x_min| + (i + 1/2) |dx| (likewise y)
+    m = np.asarray(inst.lidar2img, np.float64)
+    xs = abs(wl.x_min) + (np.arange(wl.X) + 0.5) * abs(wl.dx)
+    ys = abs(wl.y_min) + (np.arange(wl.Y) + 0.5) * abs(wl.dy)
+    gx, gy = np.meshgrid(xs, ys, indexing="ij")
+    pts = np.stack([gx.reshape(-1, 1).repeat(wl.Z, 1), gy.reshape(-1, 1).repeat(wl.Z, 1),
+                    np.broadcast_to(np.asarray(inst.z, np.float64), (wl.X * wl.Y, wl.Z)),
+                    np.ones((wl.X * wl.Y, wl.Z))], axis=-1)            # [Q, Z, 4]
+    mag = np.einsum("bnrc,qzc->bqnzr", np.abs(m), np.abs(pts))          # [B, Q, N, Z, 4]
+    dd = np.maximum(depth, eps32)
+    e = 2.0 ** -24
+    for k, (got, size) in enumerate(((un, wl.img_w), (vn, wl.img_h))):
+        want = ref[..., k]
+        bound = (6 * e * (mag[..., k] + np.abs(want * size) * mag[..., 2]) / dd / size
+                 + 3 * e * np.abs(want))
+        err = np.abs(got.astype(np.float64) - want)[keep]
+        assert np.all(err <= bound[keep]), (which, k, float((err / bound[keep]).max()))

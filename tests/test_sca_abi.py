@@ -109,6 +109,15 @@ def test_argument_errors_before_any_hip_call(kw, status):
     assert call(**kw) == S[status], kw
 
 
+def test_size_products_do_not_wrap():
+    # B Q C = (2^31 - 1) * 10^8 * 256 output elements wraps 64 bits; with no
+    # cameras there is no value tensor to reject it first
+    assert call(B=2**31 - 1, N=0, X=10000, Y=10000) == S["ERR_UNSUPPORTED"]
+    # eight levels near 2^31 pixels each: their sum no longer fits a camera
+    big = tuple((46340, 46340) for _ in range(8))
+    assert call(levels=big, C=8, heads=1) == S["ERR_UNSUPPORTED"]
+
+
 def test_empty_outputs_enqueue_nothing():
     # B = 0 or an empty grid: OK without touching the (null) device pointers
     assert call(B=0, val=0, l2i=0, off=0, log=0, out=0) == S["OK"]
