@@ -177,10 +177,16 @@ def test_sca_backward_row_merge_extremes(fb, device, case):
     check(fb, inst, device, what=f"row merge {case}")
 
 
-def test_sca_backward_bevformer_base(fb, device):
-    """Table 7's setting, P = 8, every gradient element checked."""
-    inst = synth.make_sca_workload(synth.sca_config("sca_base"))
-    check(fb, inst, device, what="sca_base P=8")
+@pytest.mark.parametrize("name,P", [("sca_base", 8), ("sca_base", 16), ("sca_base", 32),
+                                    ("sca_base_bf16", 8)])
+def test_sca_backward_bevformer_base(fb, device, name, P):
+    """Table 7's setting at every P the bench times (the row merge's keys and
+    member lists grow with P), and the bfloat16 batch of two; every element
+    of all three gradients checked against the oracle."""
+    wl = synth.sca_config(name).with_(P=P)
+    print(f"[case] {name} P={P} B={wl.B} dtype={wl.dtype}", flush=True)
+    inst = synth.make_sca_workload(wl)
+    check(fb, inst, device, what=f"{name} P={P}")
 
 
 def test_sca_backward_adjoint_of_gpu_forward(fb, device):
