@@ -30,19 +30,27 @@ extern "C" {
 
 /*
  * Gather ceiling.
- *   buf         device buffer of buf_bytes bytes, 16-byte aligned.
- *   row_bytes   bytes per pixel row (multiple of 16, at most 1024).
- *   row_pitch   pixels per image row (the lower taps are row_pitch pixels
- *               further), at least 1.
- *   iters       samples gathered per cell (even).
- *   workgroups  workgroups of 256 threads to launch.
- *   sink        device float array of workgroups * 256 entries.
+ *   buf              device buffer of buf_bytes bytes, 16-byte aligned.
+ *   row_bytes        bytes per pixel row (multiple of 16, at most 1024).
+ *   row_pitch        pixels per image row (the lower taps are row_pitch
+ *                    pixels further), at least 1.
+ *   iters            samples gathered per cell (a multiple of
+ *                    loads_in_flight / 4).
+ *   loads_in_flight  16-byte loads a lane issues before it sums them: 8, 16
+ *                    or 32 (2, 4 or 8 samples of four taps).
+ *   lds_bytes        dynamic LDS per workgroup, 0..65536; it is not used,
+ *                    it only limits the workgroups resident per CU (the
+ *                    occupancy).
+ *   workgroups       workgroups of 256 threads to launch.
+ *   sink             device float array of workgroups * 256 entries.
+ * First-tap rows follow a linear congruential sequence per cell, masked to
+ * the largest power-of-two span that keeps all four taps inside buf.
  * Bytes moved: workgroups * 4 * cells_per_wave * iters * 4 * row_bytes,
  * where cells_per_wave = min(8, 64 / (row_bytes / 16)).
  */
 int flashbev_membench_gather(const void *buf, uint64_t buf_bytes, int32_t row_bytes,
-                             int32_t row_pitch, int32_t iters, int32_t workgroups, float *sink,
-                             void *stream);
+                             int32_t row_pitch, int32_t iters, int32_t loads_in_flight,
+                             int32_t lds_bytes, int32_t workgroups, float *sink, void *stream);
 
 /*
  * HBM read ceiling: reads all of buf (bytes, a multiple of 16 * 256) once

@@ -25,9 +25,20 @@ __device__ __forceinline__ uint32_t mix(uint32_t x)
     return x;
 }
 
+// One sample = four 16-byte loads per lane (two rows, two columns of a
+// pixel's bilinear support).  SPI samples are issued before any is summed,
+// so a lane keeps 4 SPI loads in flight.  Rows come from a per-cell linear
+// congruential sequence masked to a power-of-two span (one multiply-add, a
+// shift and an AND per sample), so address arithmetic stays far below the
+// loads' issue cost.  The launch's dynamic LDS (never accessed) limits the
+// workgroups resident per CU, which sets the occupancy.
+// The waves-per-SIMD hint lets the compiler keep all 4 SPI loads of a step
+// in registers (it would otherwise shorten the window to fit 8 waves).
+template <int SPI>
 __global__ void __launch_bounds__(kThreads)
-gather_kernel(const void *buf, uint32_t nrows, uint32_t row_bytes, uint32_t row_pitch,
-              int32_t iters, int32_t lpc, int32_t cpw, float *sink)
+__attribute__((amdgpu_waves_per_eu(1, SPI == 8 ? 2 : (SPI == 4 ? 4 : 8))))
+gather_kernel(const void *buf, uint32_t nrows, uint32_t span_mask, uint32_t row_bytes,
+              uint32_t row_pitch, int32_t iters, int32_t lpc, int32_t cpw, float *sink)
 {
     const int lane = threadIdx.x % 64;
     const int wave = (blockIdx.x * kThreads + threadIdx.x) / 64;
@@ -36,23 +47,22 @@ gather_kernel(const void *buf, uint32_t nrows, uint32_t row_bytes, uint32_t row_
     const bool active = m < cpw;
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<void *>(buf), (short)0, (int)(nrows * row_bytes), 0x00020000);
-    // first-tap rows r satisfy r + row_pitch + 1 < nrows
-    const uint32_t span = nrows - row_pitch - 1;
+    // first-tap rows r <= span_mask satisfy r + row_pitch + 1 < nrows
     const uint32_t sx = row_bytes, sy = row_bytes * row_pitch;
+    uint32_t state = mix((uint32_t)wave * 0x9e3779b9u + (uint32_t)m * 0x85ebca6bu);
+    const uint32_t lane_off = slot * 16u;
     float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
-    for (int it = 0; it < iters; it += 2) {
-        const uint32_t h0 = mix((uint32_t)wave * 0x9e3779b9u + (uint32_t)it * 0x85ebca6bu + m);
-        const uint32_t h1 = mix(h0 + 0x27d4eb2fu);
-        const uint32_t v0 = active ? (h0 % span) * row_bytes + slot * 16u : 0x80000000u;
-        const uint32_t v1 = active ? (h1 % span) * row_bytes + slot * 16u : 0x80000000u;
-        uint32_t t[8][4];
-        const uint32_t vo[2] = {v0, v1};
+    for (int it = 0; it < iters; it += SPI) {
+        uint32_t t[4 * SPI][4];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            auto a = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo[u], 0u, 0);
-            auto b = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo[u], sx, 0);
-            auto c = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo[u], sy, 0);
-            auto d = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo[u], sx + sy, 0);
+        for (int u = 0; u < SPI; ++u) {
+            state = state * 1664525u + 1013904223u;
+            const uint32_t vo = active ? ((state >> 8) & span_mask) * row_bytes + lane_off
+                                       : 0x80000000u;
+            auto a = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, 0u, 0);
+            auto b = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, sx, 0);
+            auto c = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, sy, 0);
+            auto d = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, sx + sy, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 t[4 * u + 0][e] = a[e];
@@ -62,7 +72,7 @@ gather_kernel(const void *buf, uint32_t nrows, uint32_t row_bytes, uint32_t row_
             }
         }
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+        for (int k = 0; k < 4 * SPI; ++k) {
             acc0 = fmaf(0.25f, __builtin_bit_cast(float, t[k][0]), acc0);
             acc1 = fmaf(0.25f, __builtin_bit_cast(float, t[k][1]), acc1);
             acc2 = fmaf(0.25f, __builtin_bit_cast(float, t[k][2]), acc2);
@@ -108,26 +118,35 @@ static int launch_status(const void *fn, int32_t workgroups, void **args, void *
 extern "C" {
 
 int flashbev_membench_gather(const void *buf, uint64_t buf_bytes, int32_t row_bytes,
-                             int32_t row_pitch, int32_t iters, int32_t workgroups, float *sink,
-                             void *stream)
+                             int32_t row_pitch, int32_t iters, int32_t loads_in_flight,
+                             int32_t lds_bytes, int32_t workgroups, float *sink, void *stream)
 {
     if (!buf || !sink) return -1;
-    if (row_bytes < 16 || row_bytes > 1024 || row_bytes % 16 || row_pitch < 1 || iters < 2 ||
-        iters % 2 ||
-        workgroups < 1 || ((uintptr_t)buf % 16))
+    const int spi = loads_in_flight / 4;
+    if (row_bytes < 16 || row_bytes > 1024 || row_bytes % 16 || row_pitch < 1 ||
+        (spi != 2 && spi != 4 && spi != 8) || iters < spi || iters % spi || workgroups < 1 ||
+        lds_bytes < 0 || lds_bytes > 65536 || ((uintptr_t)buf % 16))
         return -2;
     if (buf_bytes > 0x7FFFFFFFull) return -3;
     const uint64_t nrows = buf_bytes / (uint64_t)row_bytes;
     if (nrows < (uint64_t)row_pitch + 3) return -2;
+    // the largest power-of-two span of first-tap rows that keeps every tap
+    // inside the buffer
+    uint32_t span = 1;
+    while ((uint64_t)span * 2 + row_pitch + 1 < nrows) span *= 2;
     const int lpc = row_bytes / 16;
     int cpw = 64 / lpc;
     if (cpw > 8) cpw = 8;
     const void *a0 = buf;
-    uint32_t a1 = (uint32_t)nrows, a2 = (uint32_t)row_bytes, a3 = (uint32_t)row_pitch;
-    int32_t a4 = iters, a5 = lpc, a6 = cpw;
-    float *a7 = sink;
-    void *args[] = {&a0, &a1, &a2, &a3, &a4, &a5, &a6, &a7};
-    return launch_status(reinterpret_cast<const void *>(gather_kernel), workgroups, args, stream);
+    uint32_t a1 = (uint32_t)nrows, a2 = span - 1u, a3 = (uint32_t)row_bytes, a4 = (uint32_t)row_pitch;
+    int32_t a5 = iters, a6 = lpc, a7 = cpw;
+    float *a8 = sink;
+    void *args[] = {&a0, &a1, &a2, &a3, &a4, &a5, &a6, &a7, &a8};
+    const void *fn = spi == 2 ? reinterpret_cast<const void *>(gather_kernel<2>)
+                   : spi == 4 ? reinterpret_cast<const void *>(gather_kernel<4>)
+                              : reinterpret_cast<const void *>(gather_kernel<8>);
+    return hipLaunchKernel(fn, dim3((unsigned)workgroups), dim3(kThreads), args, (size_t)lds_bytes,
+                           (hipStream_t)stream) == hipSuccess ? 0 : -4;
 }
 
 int flashbev_membench_stream(const void *buf, uint64_t bytes, int32_t workgroups, float *sink,

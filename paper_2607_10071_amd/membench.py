@@ -22,7 +22,8 @@ def _lib():
         L = ctypes.CDLL(_LIB_PATH)
         L.flashbev_membench_gather.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
-                                               ctypes.c_void_p, ctypes.c_void_p]
+                                               ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                               ctypes.c_void_p]
         L.flashbev_membench_gather.restype = ctypes.c_int
         L.flashbev_membench_stream.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
                                                ctypes.c_void_p, ctypes.c_void_p]
@@ -42,10 +43,12 @@ def gather_bytes(workgroups: int, row_bytes: int, iters: int) -> int:
     return workgroups * 4 * cells_per_wave(row_bytes) * iters * 4 * row_bytes
 
 
-def gather(buf, row_bytes: int, row_pitch: int, iters: int, workgroups: int, sink, stream: int) -> None:
+def gather(buf, row_bytes: int, row_pitch: int, iters: int, workgroups: int, sink, stream: int,
+           loads_in_flight: int = 8, lds_bytes: int = 0) -> None:
     rc = _lib().flashbev_membench_gather(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
-                                         row_bytes, row_pitch, iters, workgroups,
-                                         ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream))
+                                         row_bytes, row_pitch, iters, loads_in_flight, lds_bytes,
+                                         workgroups, ctypes.c_void_p(sink.data_ptr()),
+                                         ctypes.c_void_p(stream))
     if rc:
         raise RuntimeError(f"flashbev_membench_gather failed: {rc}")
 
