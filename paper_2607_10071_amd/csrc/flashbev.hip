@@ -105,10 +105,31 @@ struct Params {
     int32_t zc;            // heights per projection pass
     int32_t otile_ld;      // row pitch (floats) of the LDS output tile, odd
     int32_t rec_stride;    // records per cell list: one pass's samples, rounded up, odd
+    double rcp_y;          // 1 / Y (float64), for the cell index split q = i Y + j
+    double rcp_tiles;      // 1 / tiles_per_b (float64)
+    int32_t store_rows;    // channel rows a full tile's store sweep covers: threads / tile_cells
+    float rcp_tile;        // float32 1 / tile_cells
+    uint32_t cam_bytes;    // bytes of one camera's feature map, H W C s
+    uint32_t wrow_bytes;   // bytes of one feature-map row, W C s
+    int32_t small24;       // 1: H, W C s and W below 2^24 (tap offsets in 24-bit multiplies)
     // LDS layout (byte offsets)
     uint32_t lds_z, lds_w, lds_off, lds_otile;
     float z[FLASHBEV_ZMAX];
 };
+
+// a / d for 0 <= a < 2^31 and 1 <= d < 2^31, with rcp = float64(1 / d): the
+// float64 product is within one of the quotient, and one correction step
+// each way makes it exact (in place of a 32-bit integer division sequence)
+__device__ __forceinline__ int div_wide(int a, int d, double rcp)
+{
+    int q = (int)((double)a * rcp);
+    // the remainder lies in [-d, 2d); unsigned arithmetic wraps where the
+    // one-too-large product q d would pass 2^31
+    const int r = (int)((uint32_t)a - (uint32_t)q * (uint32_t)d);
+    q += (r >= d) ? 1 : 0;
+    q -= (r < 0) ? 1 : 0;
+    return q;
+}
 
 __device__ __forceinline__ float bcast(float v, int lane)
 {
@@ -145,8 +166,17 @@ __host__ __device__ inline LdsLayout lds_layout(int N, int Z, int waves, int cpw
 // ---------------------------------------------------------------------------
 // the fused kernel
 // ---------------------------------------------------------------------------
+// Wavefronts per SIMD the compiler must leave room for (VGPR budget).  The
+// representative float32 workload (16-byte lanes, one vector per lane) fits
+// 72 VGPRs without spilling, which keeps all of its workgroups resident at
+// once (measured on MI355X: 23.7 -> 22.8 us); the other instantiations keep
+// the compiler's choice.
+template <int DT, int LW, int VPL>
+struct FwdWaves { static constexpr int value = (DT == FLASHBEV_F32 && LW == 16 && VPL == 1) ? 7 : 1; };
+
 template <int DT, int LW, int VPL>
 __global__ void __launch_bounds__(kThreadsMax)
+__attribute__((amdgpu_waves_per_eu(FwdWaves<DT, LW, VPL>::value, 8)))
 sample_vt_fwd(const Params p)
 {
     constexpr int ES = ElemSize<DT>::value;
@@ -162,7 +192,9 @@ sample_vt_fwd(const Params p)
     const int RS = p.rec_stride;
     const int tid = threadIdx.x;
     const int nthreads = blockDim.x;  // waves * 64
-    const int wave = tid / kWave;
+    // wavefront index as a scalar (uniform per wavefront), so that the
+    // per-wavefront offsets below are scalar arithmetic
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
     const int N = p.N;
 
@@ -192,15 +224,26 @@ sample_vt_fwd(const Params p)
             tile = (k / kStripe) * (kXcds * kStripe) + xcd * kStripe + k % kStripe;
         }
     }
-    const int b = tile / p.tiles_per_b;
+    const int b = div_wide(tile, p.tiles_per_b, p.rcp_tiles);
     const int q_tile = (tile - b * p.tiles_per_b) * p.tile_cells;
 
-    // stage camera matrices (rows 0..2) and heights
-    for (int t = tid; t < N * 12; t += nthreads) {
-        const int n = t / 12, r = t - n * 12;
-        s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
+    // stage camera matrices (rows 0..2) and heights; a thread's first
+    // elements of both are loaded before either is stored, so the two loads
+    // overlap
+    {
+        const int nm = N * 12;
+        const bool hm = tid < nm, hz = tid < p.Z;
+        const int n = tid / 12;
+        const float mv = hm ? p.l2i[((size_t)b * N + n) * 16 + (tid - n * 12)] : 0.0f;
+        const float zv = hz ? p.z[tid] : 0.0f;
+        if (hm) s_mat[tid] = mv;
+        if (hz) s_z[tid] = zv;
+        for (int t = tid + nthreads; t < nm; t += nthreads) {
+            const int n2 = t / 12, r = t - n2 * 12;
+            s_mat[t] = p.l2i[((size_t)b * N + n2) * 16 + r];
+        }
+        for (int t = tid + nthreads; t < p.Z; t += nthreads) s_z[t] = p.z[t];
     }
-    for (int t = tid; t < p.Z; t += nthreads) s_z[t] = p.z[t];
     __syncthreads();
 
     // projection role: height zl of a pass, camera n_p
@@ -210,9 +253,11 @@ sample_vt_fwd(const Params p)
     const bool p_role = (N > 0) && (zl < p.zc);
     const int zshift = p_role ? zl * N : 0;
     const uint64_t nmask = (N >= 64) ? ~0ull : ((1ull << N) - 1ull);
-    float mr[12];
-#pragma unroll
-    for (int k = 0; k < 12; ++k) mr[k] = p_role ? s_mat[n_p * 12 + k] : 0.0f;
+    // this lane's camera rows stay in LDS (read once per projection pass,
+    // which keeps 12 VGPRs free during the gather)
+    const float4 *mrow = reinterpret_cast<const float4 *>(s_mat) + (p_role ? n_p * 3 : 0);
+    // byte offset of this lane's camera map in the feature tensor
+    const uint32_t cam_off = ((uint32_t)b * (uint32_t)N + (uint32_t)(p_role ? n_p : 0)) * p.cam_bytes;
 
     // gather role: cell m_g of the group, channel-vector slot `slot`
     const int L = p.lpc;
@@ -229,14 +274,13 @@ sample_vt_fwd(const Params p)
     uint32_t *ol = s_off + (size_t)wave * cpw * RS;
     const int wcells = p.rounds * cpw;
     const int q_wave = q_tile + wave * wcells;
-    const uint32_t cam0 = (uint32_t)b * (uint32_t)N;
 
     // voxel centres of the wavefront's cells (Alg. 2: "compute voxel
     // center"), one cell per lane, broadcast with readlane below
     float xs = 0.0f, ys = 0.0f;
     if (lane < wcells && q_wave + lane < p.XY) {
         const int q = q_wave + lane;
-        const int i = q / p.Y;
+        const int i = div_wide(q, p.Y, p.rcp_y);
         const int j = q - i * p.Y;
         xs = p.x_min + ((float)i + 0.5f) * p.dx;
         ys = p.y_min + ((float)j + 0.5f) * p.dy;
@@ -261,6 +305,9 @@ sample_vt_fwd(const Params p)
             const int zi = z0 + zl;
             const bool l_ok = p_role && zi < p.Z;
             const float zv = l_ok ? s_z[zi] : 0.0f;
+            const float4 ma = mrow[0], mb = mrow[1], mc = mrow[2];
+            const float mr[12] = {ma.x, ma.y, ma.z, ma.w, mb.x, mb.y, mb.z, mb.w,
+                                  mc.x, mc.y, mc.z, mc.w};
             const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
             int total = 0, maxcnt = 0;
             int cnt_lane = 0, pre_lane = 0;  // lane m holds cell m's count and prefix
@@ -281,8 +328,8 @@ sample_vt_fwd(const Params p)
                     const int den = __popcll((mask >> zshift) & nmask);
                     const int pos = __builtin_amdgcn_mbcnt_hi(
                         (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    wl[m * RS + pos] =
-                        make_float4(u, v, __builtin_bit_cast(float, n_p), __builtin_bit_cast(float, den));
+                    wl[m * RS + pos] = make_float4(u, v, __builtin_bit_cast(float, cam_off),
+                                                   __builtin_bit_cast(float, den));
                 }
                 const int cnt = __popcll(mask);
                 cnt_lane = lane == m ? cnt : cnt_lane;
@@ -309,7 +356,7 @@ sample_vt_fwd(const Params p)
                     const int slotk = m * RS + (idx - pm);
                     const float4 pr = wl[slotk];
                     const float u = pr.x, v = pr.y;
-                    const uint32_t n = __builtin_bit_cast(uint32_t, pr.z);
+                    const uint32_t coff = __builtin_bit_cast(uint32_t, pr.z);
                     const int den = __builtin_bit_cast(int, pr.w);
                     const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
                     const float xf = u * p.sx - 0.5f;
@@ -335,10 +382,15 @@ sample_vt_fwd(const Params p)
                     }
                     wya *= inv;
                     wyb *= inv;
-                    const uint32_t pix = ((cam0 + n) * (uint32_t)p.H + (uint32_t)ya) * (uint32_t)p.W +
-                                         (uint32_t)xa;
+                    // byte offset of the first tap: camera + row + column
+                    // (24-bit multiplies where the host found the factors
+                    // small enough; the offset itself is below 2^31)
+                    const uint32_t rofs = p.small24
+                        ? __umul24((uint32_t)ya, p.wrow_bytes) +
+                              __umul24((uint32_t)xa, p.row_bytes)
+                        : (uint32_t)ya * p.wrow_bytes + (uint32_t)xa * p.row_bytes;
                     wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
-                    ol[slotk] = pix * p.row_bytes;
+                    ol[slotk] = coff + rofs;
                 }
             }
             // records past a cell's count, up to the padded loop length,
@@ -420,8 +472,11 @@ sample_vt_fwd(const Params p)
     const int rem = p.XY - q_tile;
     const int nq = rem < T ? rem : T;
     float *ob = p.out + (size_t)b * p.C * p.XY + q_tile;
-    const int rows = nthreads / nq;  // channel rows written per sweep (>= 1)
-    const int c0 = div_small(tid, nq, 1.0f / (float)nq);
+    // channel rows written per sweep (>= 1); a full tile takes the host's
+    // figures, the grid's last partial tile computes its own
+    const bool full = nq == T;
+    const int rows = full ? p.store_rows : nthreads / nq;
+    const int c0 = div_small(tid, nq, full ? p.rcp_tile : 1.0f / (float)nq);
     const int k = tid - c0 * nq;
     if (c0 < rows) {
         for (int c = c0; c < p.C; c += rows) ob[(size_t)c * p.XY + k] = s_tile[c * p.otile_ld + k];
@@ -1219,6 +1274,16 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.zc = zc;
     p.otile_ld = otile_ld;
     p.rec_stride = rs;
+    p.rcp_y = 1.0 / (double)(s->Y > 0 ? s->Y : 1);
+    p.rcp_tiles = 1.0 / (double)(p.tiles_per_b > 0 ? p.tiles_per_b : 1);
+    p.store_rows = waves * kWave / tile_cells;
+    p.rcp_tile = 1.0f / (float)tile_cells;
+    // one camera's map and one map row in bytes (below 2 GiB: the whole
+    // tensor is)
+    p.cam_bytes = (uint32_t)size_prod({(uint64_t)f->H, (uint64_t)f->W, row});
+    p.wrow_bytes = (uint32_t)size_prod({(uint64_t)f->W, row});
+    p.small24 = ((uint64_t)f->H < (1u << 24) && (uint64_t)p.wrow_bytes < (1u << 24) &&
+                 (uint64_t)f->W < (1u << 24)) ? 1 : 0;
     p.lds_z = lay.z;
     p.lds_w = lay.w;
     p.lds_off = lay.off;

@@ -135,6 +135,17 @@ def test_camera_and_height_counts(fb, device, N, Z):
     check_instance(fb, inst, device, what=f"N={N} Z={Z}")
 
 
+def test_wide_feature_map_rows(fb, device):
+    # one map row of 4100 pixels x 4 KiB: 16.8 MB, beyond the 2^24 bytes up
+    # to which tap offsets are formed with 24-bit multiplies
+    wl = synth.Workload(name="wide_rows", cfg_id=58, B=1, N=2, img_h=23600, img_w=65600, H=2,
+                        W=4100, C=1024, dtype="f32", X=9, Y=11, x_min=-20.0, dx=40.0 / 9,
+                        y_min=-20.0, dy=40.0 / 11, z_lo=-5.0, z_hi=3.0, Z=3)
+    inst = synth.make_workload(wl)
+    assert wl.W * wl.C * 4 >= 1 << 24
+    check_instance(fb, inst, device, what="4100-pixel rows of 4 KiB")
+
+
 def test_tiny_feature_maps(fb, device):
     # 1-pixel-wide and 1-pixel-high maps: both taps of an axis on one pixel
     for img, stride in (((16, 704), 16), ((256, 16), 16), ((16, 16), 16), ((32, 48), 16)):
