@@ -102,7 +102,7 @@ struct Params {
     int32_t lpc;           // lanes per cell
     int32_t cpw;           // cells per wavefront group
     float rcp_n, rcp_lpc;  // float32 1 / max(N, 1) and 1 / lpc
-    int32_t zc;            // heights per projection pass
+    int32_t zc;            // heights per per-cell projection pass
     int32_t otile_ld;      // row pitch (floats) of the LDS output tile, odd
     int32_t rec_stride;    // records per cell list: one pass's samples, rounded up, odd
     double rcp_y;          // 1 / Y (float64), for the cell index split q = i Y + j
@@ -112,8 +112,10 @@ struct Params {
     uint32_t cam_bytes;    // bytes of one camera's feature map, H W C s
     uint32_t wrow_bytes;   // bytes of one feature-map row, W C s
     int32_t small24;       // 1: H, W C s and W below 2^24 (tap offsets in 24-bit multiplies)
+    int32_t cull;          // packed phase: 1 to run the culling test (0: finite heights missing)
+    float zlo, zhi, zabs;  // lowest and highest height, max(|zlo|, |zhi|)
     // LDS layout (byte offsets)
-    uint32_t lds_z, lds_w, lds_off, lds_otile;
+    uint32_t lds_z, lds_w, lds_off, lds_otile, lds_cl;
     float z[FLASHBEV_ZMAX];
 };
 
@@ -129,6 +131,53 @@ __device__ __forceinline__ int div_wide(int a, int d, double rcp)
     q += (r >= d) ? 1 : 0;
     q -= (r < 0) ? 1 : 0;
     return q;
+}
+
+// the k lowest bits set (k in 0..64)
+__device__ __forceinline__ uint64_t lowmask64(int k)
+{
+    return k >= 64 ? ~0ull : ((1ull << k) - 1ull);
+}
+
+// Camera culling of one BEV column (the mask M_n of Sec. 3.1 decided for
+// every height at once).  Returns false only if every height z in
+// [zlo, zhi] certainly fails the mask, whatever the float32 rounding of the
+// projection recipe: along the column the homogeneous coordinates
+// (u', v', d) are linear in z, so each failure below holds at every height
+// once it holds at both ends with a margin.
+//   depth:   d <= depth_eps;
+//   left:    u' < 0 (then u = u'/d < 0; the magnitude guard keeps the
+//            quotient away from -0, which the mask would accept);
+//   right:   u' - img_w d > 0 (then u >= img_w where d > 0);
+//   top and bottom: the same with v' and img_h.
+// The margin, 2^-14 of the terms' magnitudes (|m0 x| + |m1 y| + |m2| zabs
+// + |m3| per row, zabs = max(|zlo|, |zhi|)), exceeds the rounding of the
+// recipe and of this test (a few 2^-24 of the same magnitudes) by far.  A
+// non-finite value fails every comparison, so such a column is kept.
+__device__ __forceinline__ bool column_may_project(const float (&mr)[12], float x, float y,
+                                                   float zlo, float zhi, float zabs,
+                                                   float img_w, float img_h, float eps)
+{
+    constexpr float k = 6.103515625e-05f;      // 2^-14
+    constexpr float tiny = 7.888609052e-31f;   // 2^-100
+    const float bu = mr[0] * x + mr[1] * y + mr[3];
+    const float bv = mr[4] * x + mr[5] * y + mr[7];
+    const float bd = mr[8] * x + mr[9] * y + mr[11];
+    const float Mu = fabsf(mr[0] * x) + fabsf(mr[1] * y) + fabsf(mr[2]) * zabs + fabsf(mr[3]);
+    const float Mv = fabsf(mr[4] * x) + fabsf(mr[5] * y) + fabsf(mr[6]) * zabs + fabsf(mr[7]);
+    const float Md = fabsf(mr[8] * x) + fabsf(mr[9] * y) + fabsf(mr[10]) * zabs + fabsf(mr[11]);
+    const float u0 = bu + mr[2] * zlo, u1 = bu + mr[2] * zhi;
+    const float v0 = bv + mr[6] * zlo, v1 = bv + mr[6] * zhi;
+    const float d0 = bd + mr[10] * zlo, d1 = bd + mr[10] * zhi;
+    const float td = eps - k * Md;
+    const bool behind = (d0 < td) & (d1 < td);
+    const float tu = k * Mu, tv = k * Mv;
+    const bool left = (u0 < -tu) & (u1 < -tu) & (Mu > tiny * Md);
+    const bool top = (v0 < -tv) & (v1 < -tv) & (Mv > tiny * Md);
+    const float tr = k * (Mu + img_w * Md), tb = k * (Mv + img_h * Md);
+    const bool right = (u0 - img_w * d0 > tr) & (u1 - img_w * d1 > tr);
+    const bool bottom = (v0 - img_h * d0 > tb) & (v1 - img_h * d1 > tb);
+    return !(behind | left | top | right | bottom);
 }
 
 __device__ __forceinline__ float bcast(float v, int lane)
@@ -171,12 +220,24 @@ __host__ __device__ inline LdsLayout lds_layout(int N, int Z, int waves, int cpw
 // 72 VGPRs without spilling, which keeps all of its workgroups resident at
 // once (measured on MI355X: 23.7 -> 22.8 us); the other instantiations keep
 // the compiler's choice.
-template <int DT, int LW, int VPL>
-struct FwdWaves { static constexpr int value = (DT == FLASHBEV_F32 && LW == 16 && VPL == 1) ? 7 : 1; };
+template <int DT, int LW, int VPL, bool CULL>
+struct FwdWaves {
+    static constexpr int value = (!CULL && DT == FLASHBEV_F32 && LW == 16 && VPL == 1) ? 7 : 1;
+};
 
-template <int DT, int LW, int VPL>
+// CULL selects the projection phase (chosen on the host, make_plan):
+//   false: per-cell passes.  The 64 lanes hold the (height, camera) pairs of
+//          one cell; a dense set-up pass then serves the group's valid
+//          samples.  Suits groups of few cells whose heights and cameras
+//          fill a pass.
+//   true:  a culling pass per group drops the cameras no cell of the group
+//          can see (column_may_project), then passes pack several cells'
+//          (height, visible camera) pairs and set up each valid sample
+//          where it is found.  Suits groups of many cells, or heights and
+//          cameras that would need several passes per cell.
+template <int DT, int LW, int VPL, bool CULL>
 __global__ void __launch_bounds__(kThreadsMax)
-__attribute__((amdgpu_waves_per_eu(FwdWaves<DT, LW, VPL>::value, 8)))
+__attribute__((amdgpu_waves_per_eu(FwdWaves<DT, LW, VPL, CULL>::value, 8)))
 sample_vt_fwd(const Params p)
 {
     constexpr int ES = ElemSize<DT>::value;
@@ -246,18 +307,11 @@ sample_vt_fwd(const Params p)
     }
     __syncthreads();
 
-    // projection role: height zl of a pass, camera n_p
+    // culling role: cell zl of a group, camera n_p
     const int Nd = N > 0 ? N : 1;
     const int zl = div_small(lane, Nd, p.rcp_n);
     const int n_p = lane - zl * Nd;
-    const bool p_role = (N > 0) && (zl < p.zc);
-    const int zshift = p_role ? zl * N : 0;
-    const uint64_t nmask = (N >= 64) ? ~0ull : ((1ull << N) - 1ull);
-    // this lane's camera rows stay in LDS (read once per projection pass,
-    // which keeps 12 VGPRs free during the gather)
-    const float4 *mrow = reinterpret_cast<const float4 *>(s_mat) + (p_role ? n_p * 3 : 0);
-    // byte offset of this lane's camera map in the feature tensor
-    const uint32_t cam_off = ((uint32_t)b * (uint32_t)N + (uint32_t)(p_role ? n_p : 0)) * p.cam_bytes;
+    const uint64_t nmask = lowmask64(N);
 
     // gather role: cell m_g of the group, channel-vector slot `slot`
     const int L = p.lpc;
@@ -272,6 +326,7 @@ sample_vt_fwd(const Params p)
 
     float4 *wl = s_w + (size_t)wave * cpw * RS;
     uint32_t *ol = s_off + (size_t)wave * cpw * RS;
+    uint32_t *cl = reinterpret_cast<uint32_t *>(smem + p.lds_cl) + wave * kWave;  // visible cameras
     const int wcells = p.rounds * cpw;
     const int q_wave = q_tile + wave * wcells;
 
@@ -286,6 +341,70 @@ sample_vt_fwd(const Params p)
         ys = p.y_min + ((float)j + 0.5f) * p.dy;
     }
 
+    // phase 2 of one group: gather-reduce over the compacted samples of the
+    // group's cells.  kUnroll samples per iteration keep 4*kUnroll tap
+    // loads in flight per lane.
+    auto gather = [&](float (&acc)[VPL][EPV], bool g_active, int maxpad) {
+        if (g_active) {
+            const float4 *wv = wl + m_lds * RS;
+            const uint32_t *ov = ol + m_lds * RS;
+            for (int k = 0; k < maxpad; k += kUnroll) {
+                float4 w[kUnroll];
+                uint32_t base[kUnroll];
+                // the samples' offsets, then their weights, both read from
+                // LDS before the tap loads are issued: the loads wait only
+                // for the offsets, and the weights arrive while they are in
+                // flight (the scheduling barrier keeps that order)
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) base[u] = ov[k + u];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) w[u] = wv[k + u];
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int v = 0; v < VPL; ++v) {
+                    const int vi = slot + L * v;
+                    if (VPL == 1 || vi < p.nvec) {
+                        Raw<LW> t[kUnroll][4];
+#pragma unroll
+                        for (int u = 0; u < kUnroll; ++u) {
+                            const uint32_t vo = base[u] + (uint32_t)vi * LW;
+                            t[u][0] = load_vec<LW>(rsrc, vo, 0u);
+                            t[u][1] = load_vec<LW>(rsrc, vo, p.step_x);
+                            t[u][2] = load_vec<LW>(rsrc, vo, p.step_y);
+                            t[u][3] = load_vec<LW>(rsrc, vo, p.step_x + p.step_y);
+                        }
+#pragma unroll
+                        for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+                            for (int e = 0; e < EPV; ++e) {
+                                float s = acc[v][e];
+                                s = fmaf(w[u].x, elem<DT, LW>(t[u][0], e), s);
+                                s = fmaf(w[u].y, elem<DT, LW>(t[u][1], e), s);
+                                s = fmaf(w[u].z, elem<DT, LW>(t[u][2], e), s);
+                                s = fmaf(w[u].w, elem<DT, LW>(t[u][3], e), s);
+                                acc[v][e] = s;
+                            }
+                        }
+                    }
+                }
+            }
+        }
+        wave_lds_sync();
+    };
+
+    // records past a cell's count, up to the padded loop length, carry zero
+    // weights and no tap
+    auto pad = [&](int ncell, int cnt_lane, int maxpad) {
+        for (int m = 0; m < ncell; ++m) {
+            const int c = __builtin_amdgcn_readlane(cnt_lane, m);
+            if (lane >= c && lane < maxpad) {
+                wl[m * RS + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                ol[m * RS + lane] = kNoTap;
+            }
+        }
+        wave_lds_sync();
+    };
+
     for (int r = 0; r < p.rounds; ++r) {
         const int q_grp = q_wave + r * cpw;
         // cells of this group inside the grid (<= 0 past the end of the last tile)
@@ -298,156 +417,247 @@ sample_vt_fwd(const Params p)
 #pragma unroll
             for (int e = 0; e < EPV; ++e) acc[v][e] = 0.0f;
 
-        for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
-            // ---- phase 1a: project every (height, camera) pair of each
-            // cell, apply the mask M_n, and compact the valid samples as
-            // (u, v, camera, den_z) in the cell's record list
-            const int zi = z0 + zl;
-            const bool l_ok = p_role && zi < p.Z;
-            const float zv = l_ok ? s_z[zi] : 0.0f;
-            const float4 ma = mrow[0], mb = mrow[1], mc = mrow[2];
-            const float mr[12] = {ma.x, ma.y, ma.z, ma.w, mb.x, mb.y, mb.z, mb.w,
-                                  mc.x, mc.y, mc.z, mc.w};
-            const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
-            int total = 0, maxcnt = 0;
-            int cnt_lane = 0, pre_lane = 0;  // lane m holds cell m's count and prefix
-            for (int m = 0; m < ncell; ++m) {
-                const float x = bcast(xs, r * cpw + m);
-                const float y = bcast(ys, r * cpw + m);
-                // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
-                const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
-                const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
-                const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
-                const float u = up / d;
-                const float v = vp / d;
-                // M_n: positive depth, inside the image (half-open box)
-                const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
-                                (v >= 0.0f) && (v < p.img_h);
-                const uint64_t mask = __ballot(ok);
-                if (ok) {
-                    const int den = __popcll((mask >> zshift) & nmask);
-                    const int pos = __builtin_amdgcn_mbcnt_hi(
-                        (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    wl[m * RS + pos] = make_float4(u, v, __builtin_bit_cast(float, cam_off),
-                                                   __builtin_bit_cast(float, den));
+        if constexpr (CULL) {
+            // ---- camera culling for the group: lane (cell zl, camera n_p)
+            // tests whether the camera can see the cell's column at any height;
+            // cameras no cell of the group can see are left out of the
+            // projection passes (their samples are all masked out anyway)
+            uint64_t cmask = ncell > 0 ? nmask : 0ull;
+            if (p.cull && ncell > 0) {
+                bool vis = false;
+                if (N > 0 && zl < ncell) {
+                    const float4 *crow = reinterpret_cast<const float4 *>(s_mat) + n_p * 3;
+                    const float4 ma = crow[0], mb = crow[1], mc = crow[2];
+                    const float mr[12] = {ma.x, ma.y, ma.z, ma.w, mb.x, mb.y, mb.z, mb.w,
+                                          mc.x, mc.y, mc.z, mc.w};
+                    vis = column_may_project(mr, __shfl(xs, r * cpw + zl), __shfl(ys, r * cpw + zl),
+                                             p.zlo, p.zhi, p.zabs, p.img_w, p.img_h, p.depth_eps);
                 }
-                const int cnt = __popcll(mask);
-                cnt_lane = lane == m ? cnt : cnt_lane;
-                pre_lane = lane == m ? total : pre_lane;
-                total += cnt;
-                maxcnt = cnt > maxcnt ? cnt : maxcnt;
+                const uint64_t vm = __ballot(vis);
+                cmask = 0ull;
+                for (int m = 0; m < ncell; ++m) cmask |= (vm >> (m * N)) & nmask;
             }
-            const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
-            wave_lds_sync();
+            const int Np = __popcll(cmask);
 
-            // ---- phase 1b: for all valid samples of the group at once,
-            // bilinear set-up: feature coordinates, tap weights with
-            // 1 / max(1, den_z) folded in, byte offset of the first tap
-            for (int base = 0; base < total; base += kWave) {
-                const int idx = base + lane;
-                int m = 0, pm = 0;  // cell of sample idx and that cell's first index
-                for (int mm = 1; mm < ncell; ++mm) {
-                    const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
-                    const bool ge = idx >= pf;
-                    m = ge ? mm : m;
-                    pm = ge ? pf : pm;
+            if (Np > 0) {
+                // the visible cameras in ascending order
+                if (lane < N && ((cmask >> lane) & 1ull))
+                    cl[__popcll(cmask & lowmask64(lane))] = lane;
+                wave_lds_sync();
+                // pass layout: lane = (cell lm, height lz, visible camera lc),
+                // camera fastest.  A pass holds zcp heights of cpp cells; when
+                // all heights fit one pass, several cells share it.
+                const int zcp = (kWave / Np) < p.Z ? (kWave / Np) : p.Z;
+                const int P = zcp * Np;
+                int cpp = 1;
+                if (zcp == p.Z) {
+                    cpp = kWave / P;
+                    if (cpp > ncell) cpp = ncell;
                 }
-                if (idx < total) {
-                    const int slotk = m * RS + (idx - pm);
-                    const float4 pr = wl[slotk];
-                    const float u = pr.x, v = pr.y;
-                    const uint32_t coff = __builtin_bit_cast(uint32_t, pr.z);
-                    const int den = __builtin_bit_cast(int, pr.w);
-                    const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
-                    const float xf = u * p.sx - 0.5f;
-                    const float yf = v * p.sy - 0.5f;
-                    const float x0f = floorf(xf), y0f = floorf(yf);
-                    const float ax = xf - x0f, ay = yf - y0f;
-                    int xa = (int)x0f, ya = (int)y0f;
-                    float wxa = 1.0f - ax, wxb = ax;
-                    float wya = 1.0f - ay, wyb = ay;
-                    // keep both taps of each axis on in-range pixels; an
-                    // out-of-range tap gets weight zero (zero padding)
-                    if (xa < 0) {
-                        xa = 0; wxa = ax; wxb = 0.0f;
-                    } else if (xa >= p.W - 1) {
-                        if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
-                        else { xa = 0; wxb = 0.0f; }
-                    }
-                    if (ya < 0) {
-                        ya = 0; wya = ay; wyb = 0.0f;
-                    } else if (ya >= p.H - 1) {
-                        if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
-                        else { ya = 0; wyb = 0.0f; }
-                    }
-                    wya *= inv;
-                    wyb *= inv;
-                    // byte offset of the first tap: camera + row + column
-                    // (24-bit multiplies where the host found the factors
-                    // small enough; the offset itself is below 2^31)
-                    const uint32_t rofs = p.small24
-                        ? __umul24((uint32_t)ya, p.wrow_bytes) +
-                              __umul24((uint32_t)xa, p.row_bytes)
-                        : (uint32_t)ya * p.wrow_bytes + (uint32_t)xa * p.row_bytes;
-                    wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
-                    ol[slotk] = coff + rofs;
-                }
-            }
-            // records past a cell's count, up to the padded loop length,
-            // carry zero weights and no tap
-            for (int m = 0; m < ncell; ++m) {
-                const int c = __builtin_amdgcn_readlane(cnt_lane, m);
-                if (lane >= c && lane < maxpad) {
-                    wl[m * RS + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                    ol[m * RS + lane] = kNoTap;
-                }
-            }
-            wave_lds_sync();
+                const float rcp_p = __builtin_amdgcn_rcpf((float)P);
+                const float rcp_np = __builtin_amdgcn_rcpf((float)Np);
 
-            // ---- phase 2: gather-reduce over the compacted samples.
-            // kUnroll samples per iteration keep 4*kUnroll tap loads in
-            // flight per lane.
-            if (g_active) {
-                const float4 *wv = wl + m_lds * RS;
-                const uint32_t *ov = ol + m_lds * RS;
-                for (int k = 0; k < maxpad; k += kUnroll) {
-                    float4 w[kUnroll];
-                    uint32_t base[kUnroll];
-#pragma unroll
-                    for (int u = 0; u < kUnroll; ++u) {
-                        w[u] = wv[k + u];
-                        base[u] = ov[k + u];
-                    }
-#pragma unroll
-                    for (int v = 0; v < VPL; ++v) {
-                        const int vi = slot + L * v;
-                        if (VPL == 1 || vi < p.nvec) {
-                            Raw<LW> t[kUnroll][4];
-#pragma unroll
-                            for (int u = 0; u < kUnroll; ++u) {
-                                const uint32_t vo = base[u] + (uint32_t)vi * LW;
-                                t[u][0] = load_vec<LW>(rsrc, vo, 0u);
-                                t[u][1] = load_vec<LW>(rsrc, vo, p.step_x);
-                                t[u][2] = load_vec<LW>(rsrc, vo, p.step_y);
-                                t[u][3] = load_vec<LW>(rsrc, vo, p.step_x + p.step_y);
+                for (int z0 = 0; z0 < p.Z; z0 += zcp) {
+                    // this lane's place in the pass, its camera's rows and map
+                    // offset (formed per height chunk: nothing of it stays live
+                    // through the gather)
+                    const int lm = div_small(lane, P, rcp_p);
+                    const int lr = lane - lm * P;
+                    const int lz = div_small(lr, Np, rcp_np);
+                    const int lc = lr - lz * Np;
+                    const bool l_in = lm < cpp;
+                    const int n = (int)cl[lc];
+                    const float4 *prow = reinterpret_cast<const float4 *>(s_mat) + n * 3;
+                    const uint32_t coff = ((uint32_t)b * (uint32_t)N + (uint32_t)n) * p.cam_bytes;
+                    // lanes of this lane's (cell, height) group (den_z) and the
+                    // lanes before its cell in the pass (compaction offset)
+                    const uint64_t gmask = lowmask64(Np) << (lane - lc);
+                    const uint64_t before_cell = lowmask64(lm * P);
+                    int cnt_lane = 0, maxcnt = 0;  // lane m holds cell m's count
+                    const int zi = z0 + lz;
+                    const bool z_ok = l_in && zi < p.Z;
+                    const float zv = z_ok ? s_z[zi] : 0.0f;
+                    for (int m0 = 0; m0 < ncell; m0 += cpp) {
+                        // ---- phase 1: project, mask, compact and set up every
+                        // (cell, height, visible camera) sample of the pass
+                        const float4 ma = prow[0], mb = prow[1], mc = prow[2];
+                        const float mr[12] = {ma.x, ma.y, ma.z, ma.w, mb.x, mb.y, mb.z, mb.w,
+                                              mc.x, mc.y, mc.z, mc.w};
+                        const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
+                        const int m = m0 + lm;
+                        const bool l_ok = z_ok && m < ncell;
+                        const float x = __shfl(xs, r * cpw + m);
+                        const float y = __shfl(ys, r * cpw + m);
+                        // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
+                        const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
+                        const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
+                        const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
+                        const float u = up / d;
+                        const float v = vp / d;
+                        // M_n: positive depth, inside the image (half-open box)
+                        const bool ok = l_ok & (d > p.depth_eps) & (u >= 0.0f) & (u < p.img_w) &
+                                        (v >= 0.0f) & (v < p.img_h);
+                        const uint64_t mask = __ballot(ok);
+                        if (ok) {
+                            // den_z: the valid cameras of this (cell, height)
+                            const int den = __popcll(mask & gmask);
+                            const int pos = __builtin_amdgcn_mbcnt_hi(
+                                                (uint32_t)(mask >> 32),
+                                                __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u)) -
+                                            __popcll(mask & before_cell);
+                            // bilinear set-up: feature coordinates, tap weights
+                            // with 1 / max(1, den_z) folded in, first tap's offset
+                            const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+                            const float xf = u * p.sx - 0.5f;
+                            const float yf = v * p.sy - 0.5f;
+                            const float x0f = floorf(xf), y0f = floorf(yf);
+                            const float ax = xf - x0f, ay = yf - y0f;
+                            int xa = (int)x0f, ya = (int)y0f;
+                            float wxa = 1.0f - ax, wxb = ax;
+                            float wya = 1.0f - ay, wyb = ay;
+                            // keep both taps of each axis on in-range pixels; an
+                            // out-of-range tap gets weight zero (zero padding)
+                            if (xa < 0) {
+                                xa = 0; wxa = ax; wxb = 0.0f;
+                            } else if (xa >= p.W - 1) {
+                                if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
+                                else { xa = 0; wxb = 0.0f; }
                             }
-#pragma unroll
-                            for (int u = 0; u < kUnroll; ++u) {
-#pragma unroll
-                                for (int e = 0; e < EPV; ++e) {
-                                    float s = acc[v][e];
-                                    s = fmaf(w[u].x, elem<DT, LW>(t[u][0], e), s);
-                                    s = fmaf(w[u].y, elem<DT, LW>(t[u][1], e), s);
-                                    s = fmaf(w[u].z, elem<DT, LW>(t[u][2], e), s);
-                                    s = fmaf(w[u].w, elem<DT, LW>(t[u][3], e), s);
-                                    acc[v][e] = s;
-                                }
+                            if (ya < 0) {
+                                ya = 0; wya = ay; wyb = 0.0f;
+                            } else if (ya >= p.H - 1) {
+                                if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
+                                else { ya = 0; wyb = 0.0f; }
                             }
+                            wya *= inv;
+                            wyb *= inv;
+                            // byte offset of the first tap: camera + row + column
+                            // (24-bit multiplies where the host found the
+                            // factors small enough; the offset is below 2^31)
+                            const uint32_t rofs = p.small24
+                                ? __umul24((uint32_t)ya, p.wrow_bytes) + __umul24((uint32_t)xa, p.row_bytes)
+                                : (uint32_t)ya * p.wrow_bytes + (uint32_t)xa * p.row_bytes;
+                            const int slotk = m * RS + pos;
+                            wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
+                            ol[slotk] = coff + rofs;
+                        }
+                        // the pass's valid samples per cell
+                        for (int mm = 0; mm < cpp && m0 + mm < ncell; ++mm) {
+                            const int c = __popcll(mask & (lowmask64(P) << (mm * P)));
+                            cnt_lane = lane == m0 + mm ? c : cnt_lane;
+                            maxcnt = c > maxcnt ? c : maxcnt;
                         }
                     }
+                    const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
+                    pad(ncell, cnt_lane, maxpad);
+                    gather(acc, g_active, maxpad);
                 }
             }
-            wave_lds_sync();
+        } else {
+            // projection role: height zl of a pass, camera n_p; the lane's
+            // camera rows stay in LDS (read once per pass)
+            const bool p_role = (N > 0) && (zl < p.zc);
+            const int zshift = p_role ? zl * N : 0;
+            const float4 *mrow = reinterpret_cast<const float4 *>(s_mat) + (p_role ? n_p * 3 : 0);
+            const uint32_t cam_off = ((uint32_t)b * (uint32_t)N + (uint32_t)(p_role ? n_p : 0)) * p.cam_bytes;
+            for (int z0 = 0; z0 < p.Z; z0 += p.zc) {
+                // ---- phase 1a: project every (height, camera) pair of each
+                // cell, apply the mask M_n, and compact the valid samples as
+                // (u, v, camera, den_z) in the cell's record list
+                const int zi = z0 + zl;
+                const bool l_ok = p_role && zi < p.Z;
+                const float zv = l_ok ? s_z[zi] : 0.0f;
+                const float4 ma = mrow[0], mb = mrow[1], mc = mrow[2];
+                const float mr[12] = {ma.x, ma.y, ma.z, ma.w, mb.x, mb.y, mb.z, mb.w,
+                                      mc.x, mc.y, mc.z, mc.w};
+                const float t2u = mr[2] * zv, t2v = mr[6] * zv, t2d = mr[10] * zv;
+                int total = 0, maxcnt = 0;
+                int cnt_lane = 0, pre_lane = 0;  // lane m holds cell m's count and prefix
+                for (int m = 0; m < ncell; ++m) {
+                    const float x = bcast(xs, r * cpw + m);
+                    const float y = bcast(ys, r * cpw + m);
+                    // (u', v', d) = P[b,n] (x, y, z, 1), left to right, no contraction
+                    const float up = ((mr[0] * x + mr[1] * y) + t2u) + mr[3];
+                    const float vp = ((mr[4] * x + mr[5] * y) + t2v) + mr[7];
+                    const float d = ((mr[8] * x + mr[9] * y) + t2d) + mr[11];
+                    const float u = up / d;
+                    const float v = vp / d;
+                    // M_n: positive depth, inside the image (half-open box)
+                    const bool ok = l_ok && (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
+                                    (v >= 0.0f) && (v < p.img_h);
+                    const uint64_t mask = __ballot(ok);
+                    if (ok) {
+                        const int den = __popcll((mask >> zshift) & nmask);
+                        const int pos = __builtin_amdgcn_mbcnt_hi(
+                            (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                        wl[m * RS + pos] = make_float4(u, v, __builtin_bit_cast(float, cam_off),
+                                                       __builtin_bit_cast(float, den));
+                    }
+                    const int cnt = __popcll(mask);
+                    cnt_lane = lane == m ? cnt : cnt_lane;
+                    pre_lane = lane == m ? total : pre_lane;
+                    total += cnt;
+                    maxcnt = cnt > maxcnt ? cnt : maxcnt;
+                }
+                const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
+                wave_lds_sync();
+
+                // ---- phase 1b: for all valid samples of the group at once,
+                // bilinear set-up: feature coordinates, tap weights with
+                // 1 / max(1, den_z) folded in, byte offset of the first tap
+                for (int base = 0; base < total; base += kWave) {
+                    const int idx = base + lane;
+                    int m = 0, pm = 0;  // cell of sample idx and that cell's first index
+                    for (int mm = 1; mm < ncell; ++mm) {
+                        const int pf = __builtin_amdgcn_readlane(pre_lane, mm);
+                        const bool ge = idx >= pf;
+                        m = ge ? mm : m;
+                        pm = ge ? pf : pm;
+                    }
+                    if (idx < total) {
+                        const int slotk = m * RS + (idx - pm);
+                        const float4 pr = wl[slotk];
+                        const float u = pr.x, v = pr.y;
+                        const uint32_t coff = __builtin_bit_cast(uint32_t, pr.z);
+                        const int den = __builtin_bit_cast(int, pr.w);
+                        const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+                        const float xf = u * p.sx - 0.5f;
+                        const float yf = v * p.sy - 0.5f;
+                        const float x0f = floorf(xf), y0f = floorf(yf);
+                        const float ax = xf - x0f, ay = yf - y0f;
+                        int xa = (int)x0f, ya = (int)y0f;
+                        float wxa = 1.0f - ax, wxb = ax;
+                        float wya = 1.0f - ay, wyb = ay;
+                        // keep both taps of each axis on in-range pixels; an
+                        // out-of-range tap gets weight zero (zero padding)
+                        if (xa < 0) {
+                            xa = 0; wxa = ax; wxb = 0.0f;
+                        } else if (xa >= p.W - 1) {
+                            if (p.W >= 2) { xa = p.W - 2; wxb = 1.0f - ax; wxa = 0.0f; }
+                            else { xa = 0; wxb = 0.0f; }
+                        }
+                        if (ya < 0) {
+                            ya = 0; wya = ay; wyb = 0.0f;
+                        } else if (ya >= p.H - 1) {
+                            if (p.H >= 2) { ya = p.H - 2; wyb = 1.0f - ay; wya = 0.0f; }
+                            else { ya = 0; wyb = 0.0f; }
+                        }
+                        wya *= inv;
+                        wyb *= inv;
+                        // byte offset of the first tap: camera + row + column
+                        // (24-bit multiplies where the host found the factors
+                        // small enough; the offset itself is below 2^31)
+                        const uint32_t rofs = p.small24
+                            ? __umul24((uint32_t)ya, p.wrow_bytes) +
+                                  __umul24((uint32_t)xa, p.row_bytes)
+                            : (uint32_t)ya * p.wrow_bytes + (uint32_t)xa * p.row_bytes;
+                        wl[slotk] = make_float4(wxa * wya, wxb * wya, wxa * wyb, wxb * wyb);
+                        ol[slotk] = coff + rofs;
+                    }
+                }
+                pad(ncell, cnt_lane, maxpad);
+                gather(acc, g_active, maxpad);
+            }
         }
 
         // stash this group's results in the output tile
@@ -1099,36 +1309,42 @@ __global__ void __launch_bounds__(256) zero_fill(float *dst, uint64_t n)
 // ---------------------------------------------------------------------------
 using KernelFn = void (*)(const Params);
 
-template <int DT, int LW>
+template <int DT, int LW, bool CULL>
 KernelFn pick_vpl(int vpl)
 {
     switch (vpl) {
-    case 1: return sample_vt_fwd<DT, LW, 1>;
-    case 2: return sample_vt_fwd<DT, LW, 2>;
-    default: return sample_vt_fwd<DT, LW, 4>;
+    case 1: return sample_vt_fwd<DT, LW, 1, CULL>;
+    case 2: return sample_vt_fwd<DT, LW, 2, CULL>;
+    default: return sample_vt_fwd<DT, LW, 4, CULL>;
     }
 }
 
-template <int DT>
+template <int DT, bool CULL>
 KernelFn pick_lw(int lw, int vpl)
 {
     switch (lw) {
-    case 16: return pick_vpl<DT, 16>(vpl);
-    case 8: return pick_vpl<DT, 8>(vpl);
-    case 4: return pick_vpl<DT, 4>(vpl);
+    case 16: return pick_vpl<DT, 16, CULL>(vpl);
+    case 8: return pick_vpl<DT, 8, CULL>(vpl);
+    case 4: return pick_vpl<DT, 4, CULL>(vpl);
     default:
         if constexpr (DT == FLASHBEV_F32) return nullptr;
-        else return pick_vpl<DT, 2>(vpl);
+        else return pick_vpl<DT, 2, CULL>(vpl);
     }
 }
 
-KernelFn pick_kernel(int dtype, int lw, int vpl)
+template <bool CULL>
+KernelFn pick_dtype(int dtype, int lw, int vpl)
 {
     switch (dtype) {
-    case FLASHBEV_F32: return pick_lw<FLASHBEV_F32>(lw, vpl);
-    case FLASHBEV_F16: return pick_lw<FLASHBEV_F16>(lw, vpl);
-    default: return pick_lw<FLASHBEV_BF16>(lw, vpl);
+    case FLASHBEV_F32: return pick_lw<FLASHBEV_F32, CULL>(lw, vpl);
+    case FLASHBEV_F16: return pick_lw<FLASHBEV_F16, CULL>(lw, vpl);
+    default: return pick_lw<FLASHBEV_BF16, CULL>(lw, vpl);
     }
+}
+
+KernelFn pick_kernel(int dtype, int lw, int vpl, bool cull)
+{
+    return cull ? pick_dtype<true>(dtype, lw, vpl) : pick_dtype<false>(dtype, lw, vpl);
 }
 
 struct Plan {
@@ -1137,6 +1353,7 @@ struct Plan {
     int threads;
     size_t lds;
     int lw, vpl;
+    bool cull_path;     // the culled, packed projection phase
     bool empty;
 };
 
@@ -1223,19 +1440,37 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     if ((cpw <= 2 || vpl >= 2) &&
         size_prod({(uint64_t)f->B, XY}) <= (uint64_t)waves * cpw * kOneRoundTilesMax)
         rounds = 1;
-    // heights per projection pass; a cell's list holds one pass's valid
-    // samples (at most zc N <= 64), padded to whole gather iterations
+    // Projection phase (measured on MI355X, per-cell -> culled: long_range
+    // 98.7 -> 72.5 us, z_sweep Z=8 206 -> 176, half_batch 73.3 -> 69.5; but
+    // rep 22.2 -> 23.4 and the paper's reference setting 31.3 -> 31.7, whose
+    // groups of 2-3 cells already fill one pass per cell): the culled,
+    // packed phase for groups of at least 4 cells or cells needing several
+    // per-cell passes, where the culling pass (one lane per cell and camera)
+    // fits a wavefront.
+    const uint64_t zn = size_prod({(uint64_t)zb->Z, (uint64_t)(f->N > 0 ? f->N : 1)});
+    const bool cull_path = f->N > 0 && zb->Z > 0 && cpw * f->N <= kWave &&
+                           (cpw >= 4 || zn > (uint64_t)kWave);
+    // heights per per-cell pass (at most 64 / N, so zc N <= 64)
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;
     if (zc < 1) zc = 1;
-    const int rec_cap = (zc * (f->N > 0 ? f->N : 1) + kUnroll - 1) / kUnroll * kUnroll;
+    // a cell's list holds the valid samples of one pass over its heights,
+    // padded to whole gather iterations: at most zc N (per-cell passes) or
+    // min(64, Z N) (packed passes of at most 64 lanes)
+    const int pass_cap = cull_path ? (zn < (uint64_t)kWave ? (int)zn : kWave)
+                                   : zc * (f->N > 0 ? f->N : 1);
+    const int rec_cap = (pass_cap + kUnroll - 1) / kUnroll * kUnroll;
     const int rs = rec_cap | 1;
     auto pitch = [&](int r) { return (waves * r * cpw) | 1; };
+    // after the shared layout: each wavefront's list of visible cameras
+    const uint32_t cl_bytes = (uint32_t)waves * kWave * 4u;
     LdsLayout lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds), rs);
-    while (lay.total > kLdsBudget && rounds > 1) {
+    while (lay.total + cl_bytes > kLdsBudget && rounds > 1) {
         --rounds;
         lay = lds_layout(f->N, zb->Z, waves, cpw, f->C, pitch(rounds), rs);
     }
+    const uint32_t lds_cl = lay.total;
+    lay.total += cl_bytes;
     if (lay.total > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
     // a wavefront's cells fit its lanes (centre precompute) and a tile fits
     // the workgroup's threads (output store)
@@ -1274,6 +1509,19 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.zc = zc;
     p.otile_ld = otile_ld;
     p.rec_stride = rs;
+    p.cull = cull_path ? 1 : 0;
+    if (zb->Z > 0) {
+        float lo = zb->z[0], hi = zb->z[0];
+        for (int k = 1; k < zb->Z; ++k) {
+            lo = zb->z[k] < lo ? zb->z[k] : lo;
+            hi = zb->z[k] > hi ? zb->z[k] : hi;
+        }
+        p.zlo = lo;
+        p.zhi = hi;
+        p.zabs = fabsf(lo) > fabsf(hi) ? fabsf(lo) : fabsf(hi);
+        // a non-finite height: no culling (the test's margins assume finite ends)
+        if (!finite(lo) || !finite(hi)) p.cull = 0;
+    }
     p.rcp_y = 1.0 / (double)(s->Y > 0 ? s->Y : 1);
     p.rcp_tiles = 1.0 / (double)(p.tiles_per_b > 0 ? p.tiles_per_b : 1);
     p.store_rows = waves * kWave / tile_cells;
@@ -1288,6 +1536,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.lds_w = lay.w;
     p.lds_off = lay.off;
     p.lds_otile = lay.otile;
+    p.lds_cl = lds_cl;
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
     pl->workgroups = empty ? 0 : (int64_t)f->B * p.tiles_per_b;
@@ -1296,6 +1545,7 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     pl->lds = lay.total;
     pl->lw = lw;
     pl->vpl = vpl;
+    pl->cull_path = cull_path;
     pl->empty = empty;
     return FLASHBEV_OK;
 }
@@ -1599,7 +1849,7 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
     const int rc = make_plan(features, lidar2img, spec, z_bins, out, true, &pl);
     if (rc) return rc;
     if (pl.empty) return FLASHBEV_OK;
-    const KernelFn fn = pick_kernel(features->dtype, pl.lw, pl.vpl);
+    const KernelFn fn = pick_kernel(features->dtype, pl.lw, pl.vpl, pl.cull_path);
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
     void *args[] = {&pl.prm};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),

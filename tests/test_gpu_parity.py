@@ -146,6 +146,29 @@ def test_wide_feature_map_rows(fb, device):
     check_instance(fb, inst, device, what="4100-pixel rows of 4 KiB")
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_arbitrary_camera_matrices(fb, device, seed):
+    """Cameras in any orientation and place, with focal lengths and principal
+    points far from the benchmark rig's, and heights in any order over
+    +-30 m: both projection phases (per-cell passes, and the packed passes
+    behind the camera culling test) against the oracle."""
+    from test_cull_soundness import random_matrices
+    rng = np.random.default_rng([8200, seed])
+    C, dtype = [(16, "f32"), (80, "f32"), (64, "bf16"), (8, "f16")][seed % 4]
+    img_h, img_w = (256, 704) if seed % 2 else (900, 1600)
+    B, N, Z = int(rng.integers(1, 3)), int(rng.integers(1, 9)), int(rng.integers(1, 40))
+    half = float(rng.uniform(5.0, 60.0))
+    X, Y = int(rng.integers(8, 40)), int(rng.integers(8, 40))
+    wl = synth.Workload(name="arbitrary", cfg_id=8200 + seed, B=B, N=N, img_h=img_h,
+                        img_w=img_w, H=img_h // 16, W=img_w // 16, C=C, dtype=dtype, X=X, Y=Y,
+                        x_min=-half, dx=2 * half / X, y_min=-half, dy=2 * half / Y,
+                        z_lo=-5.0, z_hi=3.0, Z=Z)
+    inst = synth.make_workload(wl)
+    inst.lidar2img = np.stack([random_matrices(rng, N, img_h, img_w) for _ in range(B)])
+    inst.z = rng.uniform(-30.0, 30.0, Z).astype(np.float32)
+    check_instance(fb, inst, device, what=f"arbitrary cameras {seed}")
+
+
 def test_tiny_feature_maps(fb, device):
     # 1-pixel-wide and 1-pixel-high maps: both taps of an axis on one pixel
     for img, stride in (((16, 704), 16), ((256, 16), 16), ((16, 16), 16), ((32, 48), 16)):
