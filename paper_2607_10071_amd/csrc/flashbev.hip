@@ -1436,10 +1436,6 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     // (measured on MI355X at the paper's reference setting, C=128 float32:
     // 200x200 41.8 -> 35.2 us, 800x800 432 -> 401 us; but 1600x1600
     // 1.44 -> 1.99 ms, where per-workgroup set-up dominates)
-    int rounds = (kCellsPerWave + cpw - 1) / cpw;
-    if ((cpw <= 2 || vpl >= 2) &&
-        size_prod({(uint64_t)f->B, XY}) <= (uint64_t)waves * cpw * kOneRoundTilesMax)
-        rounds = 1;
     // Projection phase (measured on MI355X, per-cell -> culled: long_range
     // 98.7 -> 72.5 us, z_sweep Z=8 206 -> 176, half_batch 73.3 -> 69.5; but
     // rep 22.2 -> 23.4 and the paper's reference setting 31.3 -> 31.7, whose
@@ -1450,6 +1446,13 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     const uint64_t zn = size_prod({(uint64_t)zb->Z, (uint64_t)(f->N > 0 ? f->N : 1)});
     const bool cull_path = f->N > 0 && zb->Z > 0 && cpw * f->N <= kWave &&
                            (cpw >= 4 || zn > (uint64_t)kWave);
+    // The packed phase also takes one round per tile (half_batch 68.9 ->
+    // 67.6 us; rep on the per-cell phase is fastest with two: one 24.9,
+    // three 25.0, two 22.1 us).
+    int rounds = (kCellsPerWave + cpw - 1) / cpw;
+    if ((cpw <= 2 || vpl >= 2 || cull_path) &&
+        size_prod({(uint64_t)f->B, XY}) <= (uint64_t)waves * cpw * kOneRoundTilesMax)
+        rounds = 1;
     // heights per per-cell pass (at most 64 / N, so zc N <= 64)
     int zc = f->N > 0 ? kWave / f->N : 1;
     if (zc > zb->Z && zb->Z > 0) zc = zb->Z;

@@ -195,12 +195,14 @@ def test_launch_info_geometry():
         assert info["threads"] == 64 * waves
         # a tile is `waves` wavefronts x `rounds` groups of cpw cells: at
         # least 6 cells per wavefront, except one round where a wavefront
-        # holds at most two cells or a lane several 16-byte vectors
+        # holds at most two cells or a lane several 16-byte vectors, or the
+        # packed projection phase runs (groups of 4+ cells; N = 6, Z = 8)
         tiles = {math.ceil(40000 / (waves * r * cpw)): r for r in range(1, 9)}
         assert info["workgroups"] in tiles
         r = tiles[info["workgroups"]]
         vpl = math.ceil(C * (4 if dtype == "f32" else 2) / 16 / lpc)
-        if (cpw <= 2 or vpl >= 2) and 40000 <= waves * cpw * 262144:
+        packed = cpw >= 4 and cpw * 6 <= 64
+        if (cpw <= 2 or vpl >= 2 or packed) and 40000 <= waves * cpw * 262144:
             assert r == 1, (dtype, C, info)
         else:
             assert r * cpw >= 6, (dtype, C, info)
