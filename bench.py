@@ -265,9 +265,11 @@ def make_call(wl, inst, device):
     return fn, feats, l2i, out, stream
 
 
-def make_backward_call(wl, inst, device):
-    """One call of the backward (gradient w.r.t. the features): the fill of
-    the float32 gradient and the scatter kernel, on the current stream."""
+def make_backward_call(wl, inst, device, method="gather"):
+    """One call of the backward (gradient w.r.t. the features) on the
+    current stream: in gather form the transpose/den_z kernel and the
+    pixel-group gather (workspace allocated once, here), in scatter form the
+    fill of the float32 gradient and the scatter kernel."""
     import numpy as np
     import torch
 
@@ -281,7 +283,7 @@ def make_backward_call(wl, inst, device):
     img = (wl.img_h, wl.img_w)
     stream = torch.cuda.current_stream(device)
     fn = fb.prepare_sample_vt_backward(gout, l2i, inst.z, grid, img, inst.features.shape,
-                                       wl.dtype, gfeat, stream=stream)
+                                       wl.dtype, gfeat, stream=stream, method=method)
     return fn, (gout, l2i, gfeat), stream
 
 
@@ -292,10 +294,11 @@ def backward_bytes(wl) -> int:
             + wl.B * wl.N * wl.H * wl.W * wl.C * 4)
 
 
-def measure_backward(wl, inst, device, steps, warmup, taps=None, keep_grad=None) -> dict:
+def measure_backward(wl, inst, device, steps, warmup, taps=None, keep_grad=None,
+                     method="gather") -> dict:
     """Times the backward; with ``keep_grad`` (a list) the gradient of the
     last timed call is appended to it as a host array, for the parity record."""
-    fn, keep, stream = make_backward_call(wl, inst, device)
+    fn, keep, stream = make_backward_call(wl, inst, device, method)
     t = time_gpu(fn, steps, warmup, stream, 0.1)
     if keep_grad is not None:
         keep_grad.append(keep[2].cpu().numpy())

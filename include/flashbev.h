@@ -174,6 +174,58 @@ int flashbev_sample_vt_backward(const flashbev_features *features, const float *
                                 float *grad_features, void *stream);
 
 /*
+ * The same gradient as flashbev_sample_vt_backward, in gather form: every
+ * element of grad_features is written exactly once, with no atomics, and
+ * the result is bitwise identical from run to run.  Two kernels run on
+ * `stream`:
+ *   1. the output gradient is transposed to cell-major rows
+ *      Gt[b, i Y + j, c] = grad_out[b, c, i, j] and den_z of every
+ *      (b, i, j, z) (the number of cameras whose mask M_n holds, Eq. 1) is
+ *      tabulated, both in `workspace`;
+ *   2. each wavefront takes a few consecutive pixels of one feature-map row
+ *      of camera n, finds the (cell, height) samples whose bilinear taps
+ *      reach them (a conservative float64 region per height, then the
+ *      forward's exact float32 projection, mask and floor for each
+ *      candidate), and sums w_t / max(1, den_z) times their Gt rows in a
+ *      fixed order.
+ *
+ *   features, lidar2img, spec, z_bins, grad_out, grad_features, stream
+ *                  as in flashbev_sample_vt_backward.
+ *   workspace      device memory of at least workspace_bytes bytes, 256-byte
+ *                  aligned, owned by the caller; it must not overlap
+ *                  grad_out, lidar2img or grad_features, and must not be
+ *                  used by other work until the call's kernels have run.
+ *                  Its contents on entry do not matter.  Layout: Gt
+ *                  (float32, B X Y C), then at the next 256-byte boundary
+ *                  den_z (uint8, B X Y Z).
+ *   workspace_bytes  its size; flashbev_backward_workspace_size gives the
+ *                  minimum.
+ *
+ * Errors (before any HIP call): those of flashbev_sample_vt_backward;
+ * FLASHBEV_ERR_NULLPTR if workspace is NULL, FLASHBEV_ERR_ALIGN if it is not
+ * 256-byte aligned, FLASHBEV_ERR_VALUE if workspace_bytes is too small,
+ * FLASHBEV_ERR_ALIAS if it overlaps another buffer, and
+ * FLASHBEV_ERR_UNSUPPORTED when B X Y C * 4 or B X Y Z reaches 2^31 or
+ * C * 4 exceeds FLASHBEV_ROW_BYTES_MAX (flashbev_sample_vt_backward serves
+ * those shapes).  Nothing is enqueued when B, N, H, W or C is zero.
+ */
+int flashbev_sample_vt_backward_ws(const flashbev_features *features, const float *lidar2img,
+                                   const flashbev_bev_grid_spec *spec,
+                                   const flashbev_z_bins *z_bins, const float *grad_out,
+                                   float *grad_features, void *workspace,
+                                   uint64_t workspace_bytes, void *stream);
+
+/*
+ * Workspace bytes flashbev_sample_vt_backward_ws needs for these arguments
+ * (written to *bytes; a multiple of 256).  Same shape checks, no device
+ * pointer needed, no HIP call; FLASHBEV_ERR_UNSUPPORTED for the shapes the
+ * gather form does not serve.
+ */
+int flashbev_backward_workspace_size(const flashbev_features *features,
+                                     const flashbev_bev_grid_spec *spec,
+                                     const flashbev_z_bins *z_bins, uint64_t *bytes);
+
+/*
  * Launch geometry of flashbev_sample_vt_backward for these arguments: the
  * scatter kernel's workgroup count (0 when only the fill runs), threads per
  * workgroup, dynamic LDS bytes per workgroup, the LDS rows (distinct feature

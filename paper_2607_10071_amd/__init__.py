@@ -121,6 +121,14 @@ def _lib():
                                                     P(ctypes.c_int32), P(ctypes.c_int32),
                                                     P(ctypes.c_int32)]
         L.flashbev_backward_launch_info.restype = ctypes.c_int
+        L.flashbev_backward_workspace_size.argtypes = [P(Features), P(GridSpec), P(ZBins),
+                                                       P(ctypes.c_uint64)]
+        L.flashbev_backward_workspace_size.restype = ctypes.c_int
+        L.flashbev_sample_vt_backward_ws.argtypes = [P(Features), ctypes.c_void_p, P(GridSpec),
+                                                     P(ZBins), ctypes.c_void_p, ctypes.c_void_p,
+                                                     ctypes.c_void_p, ctypes.c_uint64,
+                                                     ctypes.c_void_p]
+        L.flashbev_sample_vt_backward_ws.restype = ctypes.c_int
         L.flashsca_forward.argtypes = [P(ScaValue), ctypes.c_void_p, P(GridSpec), P(ZBins),
                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p]
@@ -290,9 +298,40 @@ def _on_device(device):
     return torch.cuda.device(device)
 
 
+BACKWARD_METHODS = ("gather", "scatter")
+
+
+def backward_workspace_size(features_shape, features_dtype, z_bins, grid: BevGrid, img_hw,
+                            reduce: str = "mean") -> int:
+    """Workspace bytes of the gather-form backward for these arguments, or
+    -1 when it does not serve them (the scatter form then does)."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(tuple(int(v) for v in features_shape), DTYPE_CODES[features_dtype], 0,
+                        img_hw, grid, z, reduce)
+    out = ctypes.c_uint64()
+    rc = _lib().flashbev_backward_workspace_size(ctypes.byref(f), ctypes.byref(g),
+                                                 ctypes.byref(zb), ctypes.byref(out))
+    if rc == STATUS["ERR_UNSUPPORTED"]:
+        # the scatter form's own checks decide whether any backward serves it
+        backward_launch_info(features_shape, features_dtype, z, grid, img_hw, reduce)
+        return -1
+    if rc != 0:
+        raise FlashBevError(rc, "flashbev_backward_workspace_size")
+    return int(out.value)
+
+
+def _dtype_name(features_dtype) -> str:
+    import torch
+
+    if isinstance(features_dtype, str):
+        return features_dtype
+    return {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[features_dtype]
+
+
 def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int],
                        features_shape, features_dtype="f32", grad_features=None,
-                       reduce: str = "mean", stream=None):
+                       reduce: str = "mean", stream=None, method: str = "gather",
+                       workspace=None):
     """Gradient of the fused Sampling-VT forward with respect to the features.
 
     grad_out        CUDA float32 tensor [B, C, X, Y] (gradient w.r.t. ``out``).
@@ -300,22 +339,49 @@ def sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple
     features_shape  (B, N, H, W, C) of the features of the forward call.
     features_dtype  their dtype ("f32", "f16", "bf16" or a torch dtype).
     grad_features   optional CUDA float32 tensor [B, N, H, W, C] to write.
+    method          "gather" (flashbev_sample_vt_backward_ws: every gradient
+                    row written once, no atomics, bitwise reproducible; it
+                    needs a device workspace, allocated here unless
+                    ``workspace`` is given) or "scatter"
+                    (flashbev_sample_vt_backward: float atomics, no
+                    workspace).  "gather" falls back to "scatter" for
+                    shapes it does not serve.
 
     Returns ``grad_features`` (float32, channel-last).  Asynchronous.
     """
     import torch
 
+    if method not in BACKWARD_METHODS:
+        raise ValueError(f"method must be one of {BACKWARD_METHODS}")
     B, N, H, W, C = _check_backward(grad_out, lidar2img, grid, features_shape)
     if grad_features is None:
         grad_features = torch.empty((B, N, H, W, C), dtype=torch.float32, device=grad_out.device)
     _check_out(grad_features, (B, N, H, W, C), "grad_features")
-    if not isinstance(features_dtype, str):
-        features_dtype = {torch.float32: "f32", torch.float16: "f16",
-                          torch.bfloat16: "bf16"}[features_dtype]
+    features_dtype = _dtype_name(features_dtype)
     z = _z_array(z_bins)
     f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
     dev = _one_device(grad_out, lidar2img, grad_features)
     s = _stream_handle(stream, dev)
+    if method == "gather":
+        need = backward_workspace_size((B, N, H, W, C), features_dtype, z, grid, img_hw, reduce)
+        if need < 0:
+            method = "scatter"
+        else:
+            if workspace is None:
+                workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=grad_out.device)
+            elif not workspace.is_cuda or workspace.numel() * workspace.element_size() < need:
+                raise ValueError(f"workspace must be a device tensor of at least {need} bytes")
+            with _on_device(dev):
+                rc = _lib().flashbev_sample_vt_backward_ws(
+                    ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+                    ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
+                    ctypes.c_void_p(grad_features.data_ptr()),
+                    ctypes.c_void_p(workspace.data_ptr()),
+                    ctypes.c_uint64(workspace.numel() * workspace.element_size()),
+                    ctypes.c_void_p(s))
+            if rc != 0:
+                raise FlashBevError(rc, "flashbev_sample_vt_backward_ws")
+            return grad_features
     with _on_device(dev):
         rc = _lib().flashbev_sample_vt_backward(
             ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
@@ -335,6 +401,21 @@ def sample_vt_backward_raw(shape, dtype: str, lidar2img_ptr: int, z_bins, grid: 
     return int(_lib().flashbev_sample_vt_backward(
         ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr), ctypes.byref(g), ctypes.byref(zb),
         ctypes.c_void_p(grad_out_ptr), ctypes.c_void_p(grad_features_ptr),
+        ctypes.c_void_p(stream)))
+
+
+def sample_vt_backward_ws_raw(shape, dtype: str, lidar2img_ptr: int, z_bins, grid: BevGrid,
+                              img_hw, grad_out_ptr: int, grad_features_ptr: int,
+                              workspace_ptr: int, workspace_bytes: int, reduce: str = "mean",
+                              stream: int = 0) -> int:
+    """The gather-form backward's C entry point with raw device addresses;
+    returns the status."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], 0, img_hw, grid, z, reduce)
+    return int(_lib().flashbev_sample_vt_backward_ws(
+        ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr), ctypes.byref(g), ctypes.byref(zb),
+        ctypes.c_void_p(grad_out_ptr), ctypes.c_void_p(grad_features_ptr),
+        ctypes.c_void_p(workspace_ptr), ctypes.c_uint64(workspace_bytes),
         ctypes.c_void_p(stream)))
 
 
@@ -438,19 +519,32 @@ def prepare_sample_vt(features, lidar2img, z_bins, grid: BevGrid, img_hw, out,
 
 def prepare_sample_vt_backward(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw,
                                features_shape, features_dtype, grad_features,
-                               reduce: str = "mean", stream=None) -> _Prepared:
-    """``sample_vt_backward`` with every argument fixed (see prepare_sample_vt)."""
+                               reduce: str = "mean", stream=None,
+                               method: str = "gather") -> _Prepared:
+    """``sample_vt_backward`` with every argument fixed (see prepare_sample_vt);
+    the gather form's workspace is allocated once, here."""
     import torch
 
+    if method not in BACKWARD_METHODS:
+        raise ValueError(f"method must be one of {BACKWARD_METHODS}")
     B, N, H, W, C = _check_backward(grad_out, lidar2img, grid, features_shape)
     _check_out(grad_features, (B, N, H, W, C), "grad_features")
-    if not isinstance(features_dtype, str):
-        features_dtype = {torch.float32: "f32", torch.float16: "f16",
-                          torch.bfloat16: "bf16"}[features_dtype]
+    features_dtype = _dtype_name(features_dtype)
     z = _z_array(z_bins)
     f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
     dev = _one_device(grad_out, lidar2img, grad_features)
     s = _stream_handle(stream, dev)
+    if method == "gather":
+        need = backward_workspace_size((B, N, H, W, C), features_dtype, z, grid, img_hw, reduce)
+        if need >= 0:
+            ws = torch.empty(max(need, 1), dtype=torch.uint8, device=grad_out.device)
+            args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+                    ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
+                    ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                    ctypes.c_uint64(ws.numel()), ctypes.c_void_p(s))
+            return _Prepared(_lib().flashbev_sample_vt_backward_ws, args,
+                             (grad_out, lidar2img, grad_features, ws, z, f, g, zb),
+                             "flashbev_sample_vt_backward_ws", dev)
     args = (ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
             ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
             ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(s))

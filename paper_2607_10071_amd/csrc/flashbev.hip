@@ -1287,6 +1287,551 @@ sample_vt_bwd(const BwdParams p)
     }
 }
 
+// ---------------------------------------------------------------------------
+// backward, gather form: one write per gradient element, no atomics
+// ---------------------------------------------------------------------------
+// The gradient with respect to the features is the transpose of Eq. 1's map.
+// In gather form each feature pixel (b, n, py, px) collects its own terms:
+// the valid samples (cell, z) of camera n whose bilinear support holds the
+// pixel, each adding w_t / max(1, den_z) times the cell's output-gradient
+// row.  Two kernels on the caller's stream and workspace:
+//   * sample_vt_bwd_prep: the output gradient transposed to cell-major rows
+//     Gt[b, cell, C] (so a term's row is one contiguous read), and den_z of
+//     every (b, cell, z) (the valid cameras of the point, Eq. 1's divisor).
+//   * sample_vt_bwd_gather: a wavefront per group of cpw consecutive pixels
+//     of one feature-map row.  For each height the cells that can reach the
+//     group's support lie in a convex region of that height's plane,
+//     bounded by five half-planes (depth above depth_eps; u and v inside
+//     the group's support and the image) with slack for float32 rounding.
+//     The region's rows give contiguous runs of candidate cells; each
+//     candidate is re-checked with the forward's exact float32 recipe
+//     (projection, mask, floor), so mask and tap decisions are the
+//     forward's.  The terms go to per-pixel LDS lists, and the lanes of a
+//     pixel sum their rows of Gt in registers, as the forward gathers
+//     feature rows.  Each gradient row is written once; the summation order
+//     is fixed, so results are bitwise identical run to run.
+struct BwdGatherParams {
+    const float *l2i;
+    const float *gout;       // [B, C, X, Y]
+    float *gfeat;            // [B, N, H, W, C]
+    float *gt;               // workspace: [B, X Y, C]
+    uint8_t *den;            // workspace: [B, X Y, Z]
+    uint32_t gt_bytes;       // bytes of gt (buffer size for the descriptor)
+    int32_t B, N, H, W, C, X, Y, Z;
+    int32_t XY;
+    float img_w, img_h;
+    float sx, sy;
+    float x_min, dx, y_min, dy, depth_eps;
+    int32_t reduce;
+    double dx_d, dy_d, x_min_d, y_min_d;  // float64 copies for the regions
+    double isx_d, isy_d;        // 1 / sx, 1 / sy in float64 (sx, sy the float32 scales)
+    double xmax_abs, ymax_abs;  // bounds on |x|, |y| of a cell centre and its float32 terms
+    // prep kernel
+    int32_t prep_tiles_per_b;   // 64-cell tiles per batch element
+    int32_t prep_cblocks;       // 64-channel blocks
+    // gather kernel
+    int32_t cpw;             // pixels per wavefront group
+    int32_t lpc;             // lanes per pixel
+    int32_t nvec;            // LW-byte vectors per gradient row
+    float rcp_lpc;
+    int32_t groups_per_row;  // pixel groups per feature-map row
+    int64_t groups;          // all pixel groups (B N H groups_per_row)
+    int32_t rec_stride;      // records per pixel list
+    uint32_t row_bytes;      // C * 4
+    uint32_t lds_wave;       // LDS bytes per wavefront
+    float z[FLASHBEV_ZMAX];
+};
+
+constexpr int kPrepCells = 64;      // cells per prep workgroup
+constexpr int kGatherRec = 128;     // records per pixel list (two candidate chunks)
+constexpr int kGatherUnroll = 8;    // terms per gather iteration (loads in flight)
+constexpr int kHeightBatch = 32;    // heights whose rows one pass packs together
+// LDS bytes per wavefront after its pixel lists (see the kernel's layout)
+constexpr uint32_t kGatherTail = 4u * kWave * 4u + (5u * 8u + 36u * 2u + kHeightBatch * 5u) * 8u +
+                                 4u * kHeightBatch * 4u;
+
+// Prep: Gt rows of 64 consecutive cells for 64 channels, and (in the
+// workgroups of the first channel block) den_z of those cells.  256
+// threads; each moves 16 values with its loads all in flight.
+__global__ void __launch_bounds__(256) sample_vt_bwd_prep(const BwdGatherParams p)
+{
+    __shared__ float s_mat[FLASHBEV_NMAX * 12];
+    __shared__ float s_t[kPrepCells][65];   // transpose tile, odd pitch
+    const int tid = threadIdx.x;
+    const int per_b = p.prep_tiles_per_b * p.prep_cblocks;
+    const int b = blockIdx.x / per_b;
+    const int rem = blockIdx.x - b * per_b;
+    const int cb = rem / p.prep_tiles_per_b;
+    const int q0 = (rem - cb * p.prep_tiles_per_b) * kPrepCells;
+    const int c0 = cb * 64;
+    const int ncell = (p.XY - q0) < kPrepCells ? (p.XY - q0) : kPrepCells;
+    const int nc = (p.C - c0) < 64 ? (p.C - c0) : 64;
+    // Gt[b, q, c] = gout[b, c, q]: reads along cells, writes along channels
+    const float *gb = p.gout + (size_t)b * p.C * p.XY;
+    float *tb = p.gt + (size_t)b * p.XY * p.C;
+    {
+        const int cl = tid & 63, cc0 = tid >> 6;
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int cc = cc0 + 4 * u;
+            v[u] = (cc < nc && cl < ncell) ? gb[(size_t)(c0 + cc) * p.XY + q0 + cl] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s_t[cl][cc0 + 4 * u] = v[u];
+    }
+    __syncthreads();
+    {
+        const int cc = tid & 63, cl0 = tid >> 6;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int cl = cl0 + 4 * u;
+            if (cc < nc && cl < ncell) tb[(size_t)(q0 + cl) * p.C + c0 + cc] = s_t[cl][cc];
+        }
+    }
+    if (cb != 0) return;   // block-uniform; no barrier follows in this branch
+    const int N = p.N;
+    for (int t = tid; t < N * 12; t += 256) {
+        const int n = t / 12, r = t - n * 12;
+        s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
+    }
+    __syncthreads();
+    // den_z: thread per (cell, height), cameras in a loop, the forward's recipe
+    for (int t = tid; t < ncell * p.Z; t += 256) {
+        const int c = t / p.Z, k = t - c * p.Z;
+        const int q = q0 + c;
+        const int i = q / p.Y, j = q - (q / p.Y) * p.Y;
+        const float x = p.x_min + ((float)i + 0.5f) * p.dx;
+        const float y = p.y_min + ((float)j + 0.5f) * p.dy;
+        const float zv = p.z[k];
+        int den = 0;
+        for (int n = 0; n < N; ++n) {
+            const float *mr = s_mat + n * 12;
+            const float up = ((mr[0] * x + mr[1] * y) + mr[2] * zv) + mr[3];
+            const float vp = ((mr[4] * x + mr[5] * y) + mr[6] * zv) + mr[7];
+            const float d = ((mr[8] * x + mr[9] * y) + mr[10] * zv) + mr[11];
+            const float u = up / d;
+            const float v = vp / d;
+            den += ((d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) && (v >= 0.0f) &&
+                    (v < p.img_h)) ? 1 : 0;
+        }
+        p.den[((size_t)b * p.XY + q) * p.Z + k] = (uint8_t)den;
+    }
+}
+
+template <int LW, int VPL>
+__global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParams p)
+{
+    constexpr int EPV = LW / 4;   // float32 gradient elements per vector
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int lane = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int RS = p.rec_stride;
+    const int cpw = p.cpw;
+    unsigned char *wbase = smem + (size_t)wave * p.lds_wave;
+    float *wl = reinterpret_cast<float *>(wbase);                         // [cpw][RS] weights
+    uint32_t *ol = reinterpret_cast<uint32_t *>(wbase + (size_t)cpw * RS * 4);  // [cpw][RS] Gt offsets
+    // after the lists: per candidate row (64) its cell prefix, first cell,
+    // height slot and grid row; the height-free plane terms (5 x 8); the
+    // pair slopes (36 x 2); per height of a batch its plane offsets (x 5),
+    // row prefix, first row, no-region flag and value
+    int *rpre = reinterpret_cast<int *>(wbase + (size_t)cpw * RS * 8);
+    int *rjlo = rpre + kWave;
+    int *rhs = rjlo + kWave;
+    int *rci = rhs + kWave;
+    double *ptab = reinterpret_cast<double *>(rci + kWave);
+    double *pairt = ptab + 5 * 8;
+    double *hg = pairt + 36 * 2;
+    int *hpre = reinterpret_cast<int *>(hg + kHeightBatch * 5);
+    int *hilo = hpre + kHeightBatch;
+    int *hwild = hilo + kHeightBatch;
+    float *hz = reinterpret_cast<float *>(hwild + kHeightBatch);
+
+    // pixel group of this wavefront; workgroups go to the 8 XCDs
+    // round-robin, and each XCD takes one contiguous band of groups (the
+    // cells a band reaches, hence its rows of Gt, stay in one L2)
+    const int64_t nwg = gridDim.x;
+    const int64_t per = nwg / kXcds;
+    int64_t wg = blockIdx.x;
+    if (wg < per * kXcds) wg = (wg % kXcds) * per + wg / kXcds;
+    const int64_t grp = wg * (blockDim.x / kWave) + wave;
+    if (grp >= p.groups) return;   // wavefront-uniform: no barrier follows
+    const int gpr = p.groups_per_row;
+    const int64_t row = grp / gpr;
+    const int px0 = (int)(grp - row * gpr) * cpw;
+    const int py = (int)(row % p.H);
+    const int64_t bn = row / p.H;
+    const int n = (int)(bn % p.N);
+    const int b = (int)(bn / p.N);
+    const int g = (p.W - px0) < cpw ? (p.W - px0) : cpw;
+
+    // gather role: pixel m_g of the group, vector slot `slot`
+    const int L = p.lpc;
+    const int m_g = div_small(lane, L, p.rcp_lpc);
+    const int slot = lane - m_g * L;
+    const bool g_active = m_g < g;
+    const int m_lds = m_g < cpw ? m_g : 0;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(p.gt, (short)0, (int)p.gt_bytes, 0x00020000);
+
+    float acc[VPL][EPV];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) acc[v][e] = 0.0f;
+
+    // camera rows (uniform)
+    const float *mg = p.l2i + ((size_t)b * p.N + n) * 16;
+    float mr[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) mr[k] = mg[k];
+
+    // the group's support in image coordinates: samples whose first tap is
+    // in column [px0 - 1, px0 + g - 1] and row py - 1 or py, inside the image
+    const double U0 = fmax(0.0, ((double)px0 - 0.5) * p.isx_d);
+    const double U1 = fmin((double)p.img_w, ((double)(px0 + g) + 0.5) * p.isx_d);
+    const double V0 = fmax(0.0, ((double)py - 0.5) * p.isy_d);
+    const double V1 = fmin((double)p.img_h, ((double)py + 1.5) * p.isy_d);
+    const uint32_t cam_gt = (uint32_t)b * (uint32_t)p.XY * p.row_bytes;
+    const uint8_t *denb = p.den + (size_t)b * p.XY * p.Z;
+
+    int cnt_lane = 0;   // lane m holds pixel m's record count
+    int maxcnt = 0;
+
+    auto flush = [&]() {
+        const int maxpad = (maxcnt + kGatherUnroll - 1) / kGatherUnroll * kGatherUnroll;
+        for (int m = 0; m < g; ++m) {
+            const int c = __builtin_amdgcn_readlane(cnt_lane, m);
+            for (int k = c + lane; k < maxpad; k += kWave) {
+                wl[m * RS + k] = 0.0f;
+                ol[m * RS + k] = kNoTap;
+            }
+        }
+        wave_lds_sync();
+        if (g_active) {
+            const float *wv = wl + m_lds * RS;
+            const uint32_t *ov = ol + m_lds * RS;
+            for (int k = 0; k < maxpad; k += kGatherUnroll) {
+                uint32_t base[kGatherUnroll];
+                float w[kGatherUnroll];
+#pragma unroll
+                for (int u = 0; u < kGatherUnroll; ++u) base[u] = ov[k + u];
+#pragma unroll
+                for (int u = 0; u < kGatherUnroll; ++u) w[u] = wv[k + u];
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int v = 0; v < VPL; ++v) {
+                    const int vi = slot + L * v;
+                    if (VPL == 1 || vi < p.nvec) {
+                        Raw<LW> t[kGatherUnroll];
+#pragma unroll
+                        for (int u = 0; u < kGatherUnroll; ++u)
+                            t[u] = load_vec<LW>(rsrc, base[u] + (uint32_t)vi * LW, 0u);
+#pragma unroll
+                        for (int u = 0; u < kGatherUnroll; ++u)
+#pragma unroll
+                            for (int e = 0; e < EPV; ++e)
+                                acc[v][e] = fmaf(w[u], __builtin_bit_cast(float, t[u].w[e]), acc[v][e]);
+                    }
+                }
+            }
+        }
+        wave_lds_sync();
+        cnt_lane = 0;
+        maxcnt = 0;
+    };
+
+    if (U0 < U1 && V0 < V1 && p.X > 0 && p.Y > 0) {
+        // slack bounds: magnitudes of the rows' terms over the grid
+        const double Mu0 = fabs((double)mr[0]) * p.xmax_abs + fabs((double)mr[1]) * p.ymax_abs +
+                           fabs((double)mr[3]);
+        const double Mv0 = fabs((double)mr[4]) * p.xmax_abs + fabs((double)mr[5]) * p.ymax_abs +
+                           fabs((double)mr[7]);
+        const double Md0 = fabs((double)mr[8]) * p.xmax_abs + fabs((double)mr[9]) * p.ymax_abs +
+                           fabs((double)mr[11]);
+        // slack: 2^-18 of the magnitudes, far above the float32 recipe's
+        // rounding of u', v', d, the quotient, the feature coordinate and
+        // the cell centre (a few 2^-24 of the same magnitudes)
+        const double e = 3.814697265625e-06;   // 2^-18
+        const double yc0 = p.y_min_d + 0.5 * p.dy_d;   // centre of column 0
+        const double xr0 = p.x_min_d + 0.5 * p.dx_d;   // centre of row 0
+        const double Yd = (double)p.Y, Xd = (double)p.X;
+        const double xspan = fabs(xr0) + fabs(p.dx_d) * Xd;   // bound on |x| terms of a row
+        // Half-plane q (0: depth above depth_eps, 1: u >= U0, 2: u <= U1,
+        // 3: v >= V0, 4: v <= V1) on the plane of height z reads
+        // pa_q x + pb_q y + pc_q(z) >= 0, and only pc_q depends on z.  On
+        // the grid row at x, in column-index form:
+        // pa_q x + gam_q(z) + beta_q j >= 0 with beta_q = pb_q dy, so its
+        // kind (the sign of beta_q: a lower bound, an upper bound or no
+        // column dependence) is the same at every height.  Lane q < 5
+        // tabulates the height-free terms of plane q.
+        if (lane < 5) {
+            const int q = lane;
+            const double ad = mr[8], bd = mr[9];
+            const double ra = q <= 2 ? (double)mr[0] : (double)mr[4];
+            const double rb = q <= 2 ? (double)mr[1] : (double)mr[5];
+            const double S = q == 1 ? U0 : (q == 2 ? U1 : (q == 3 ? V0 : V1));
+            const double sg = (q == 1 || q == 3) ? 1.0 : -1.0;
+            const double pa = q == 0 ? ad : sg * (ra - S * ad);
+            const double pb = q == 0 ? bd : sg * (rb - S * bd);
+            const double beta = pb * p.dy_d;
+            const int kind = beta > 1e-200 ? 1 : (beta < -1e-200 ? -1 : 0);
+            const double rho = kind != 0 ? 1.0 / beta : 0.0;
+            const double Bs = pa * p.dx_d;
+            ptab[q * 8 + 0] = pa;
+            ptab[q * 8 + 1] = pb;
+            ptab[q * 8 + 2] = rho;
+            ptab[q * 8 + 3] = fabs(beta) * Yd;              // slack of a kind-0 plane
+            ptab[q * 8 + 4] = (double)kind;
+            ptab[q * 8 + 5] = kind != 0 ? -Bs * rho : Bs;   // row slope T1
+        }
+        wave_lds_sync();
+        int kind[5];
+#pragma unroll
+        for (int q = 0; q < 5; ++q) kind[q] = __builtin_amdgcn_readfirstlane((int)ptab[q * 8 + 4]);
+        // pair (p, q) of 6 x 6 (index 5: the clamps Y and -1): the row slope
+        // of "upper bound p minus lower bound q" and its reciprocal
+        if (lane < 36) {
+            const int pp = lane / 6, qq = lane - pp * 6;
+            const double be = (pp == 5 ? 0.0 : ptab[pp * 8 + 5]) - (qq == 5 ? 0.0 : ptab[qq * 8 + 5]);
+            pairt[lane * 2 + 0] = be;
+            pairt[lane * 2 + 1] = be != 0.0 ? 1.0 / be : 0.0;
+        }
+        wave_lds_sync();
+        for (int k0 = 0; k0 < p.Z; k0 += kHeightBatch) {
+            const int nb = (p.Z - k0) < kHeightBatch ? (p.Z - k0) : kHeightBatch;
+            // lanes over the batch's heights: each height's offsets gam_q
+            // and the range of grid rows that can hold a candidate
+            float zv = 0.0f;
+            for (int h = 0; h < nb; ++h) {
+                const float zh = p.z[k0 + h];
+                zv = lane == h ? zh : zv;
+            }
+            int rows = 0;
+            if (lane < nb && __builtin_isfinite(zv)) {
+                // (a non-finite height makes u', v' and d non-finite or NaN:
+                // the forward's mask rejects every sample of it)
+                const double zd = (double)zv;
+                const double Mu = Mu0 + fabs((double)mr[2] * zd), Mv = Mv0 + fabs((double)mr[6] * zd),
+                             Md = Md0 + fabs((double)mr[10] * zd);
+                const double cu = (double)mr[2] * zd + (double)mr[3];
+                const double cv = (double)mr[6] * zd + (double)mr[7];
+                const double cd = (double)mr[10] * zd + (double)mr[11];
+                // rows that are non-finite, near float32 overflow or in its
+                // subnormal range get no region: every cell is a candidate
+                const bool tame = Mu < 1e36 && Mv < 1e36 && Md < 1e36 &&
+                                  (Mu == 0.0 || Mu > 1e-30) && (Mv == 0.0 || Mv > 1e-30) &&
+                                  (Md == 0.0 || Md > 1e-30);
+                const double pc[5] = {cd - (double)p.depth_eps + e * Md,
+                                      (cu - U0 * cd) + e * (Mu + U0 * Md),
+                                      -(cu - U1 * cd) + e * (Mu + U1 * Md),
+                                      (cv - V0 * cd) + e * (Mv + V0 * Md),
+                                      -(cv - V1 * cd) + e * (Mv + V1 * Md)};
+                // per plane: the column bound -(pa x + gam) rho (kind != 0)
+                // or the value pa x + gam + slack (kind 0) on row r is
+                // T0 + T1 r; TM bounds the magnitude of its terms
+                double T0[5], TM[5];
+#pragma unroll
+                for (int q = 0; q < 5; ++q) {
+                    const double pa = ptab[q * 8 + 0], rho = ptab[q * 8 + 2], sj = ptab[q * 8 + 3];
+                    const double gam = pc[q] + ptab[q * 8 + 1] * yc0;
+                    hg[lane * 5 + q] = gam;
+                    const double A = pa * xr0 + gam;
+                    const double Mq = fabs(pa) * xspan + fabs(gam);
+                    T0[q] = kind[q] != 0 ? -A * rho : A + sj;
+                    TM[q] = kind[q] != 0 ? Mq * fabs(rho) : Mq + sj;
+                }
+                // "upper bound p >= lower bound q" holds on a half-line of
+                // rows, as does a kind-0 plane; each bound is widened by a
+                // row, and a slope under 2^-40 of the terms' magnitude
+                // bounds nothing unless the pair fails on every row by more
+                int rlo = 0, rhi = p.X - 1;
+                bool none = false;
+                auto bound = [&](double al, double be, double rbe, double mm) {
+                    const double tiny = 9.094947017729282e-13 * mm;   // 2^-40
+                    if (fabs(be) > tiny) {
+                        const double b = fmin(fmax(-al * rbe, -4.0), Xd + 4.0);
+                        if (be > 0.0) rlo = max(rlo, (int)floor(b) - 1);
+                        else rhi = min(rhi, (int)ceil(b) + 1);
+                    } else {
+                        none = none || (al + fabs(be) * Xd < -tiny);
+                    }
+                };
+#pragma unroll
+                for (int pp = 0; pp < 6; ++pp) {
+#pragma unroll
+                    for (int qq = 0; qq < 6; ++qq) {
+                        const bool up = pp == 5 || kind[pp] < 0;
+                        const bool lw = qq == 5 || kind[qq] > 0;
+                        if (!up || !lw || (pp == 5 && qq == 5)) continue;   // uniform
+                        const double t0p = pp == 5 ? Yd : T0[pp], mp = pp == 5 ? Yd : TM[pp];
+                        const double t0q = qq == 5 ? -1.0 : T0[qq], mq = qq == 5 ? 1.0 : TM[qq];
+                        const int j = pp * 6 + qq;
+                        bound(t0p - t0q, pairt[j * 2], pairt[j * 2 + 1], mp + mq);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 5; ++q) {
+                    if (kind[q] != 0) continue;   // uniform
+                    const double be = ptab[q * 8 + 5];
+                    bound(T0[q], be, be != 0.0 ? 1.0 / be : 0.0, TM[q]);
+                }
+                if (!tame) { rlo = 0; rhi = p.X - 1; none = false; }
+                const int ilo = max(0, rlo), ihi = min(p.X - 1, rhi);
+                rows = (!none && ilo <= ihi) ? ihi - ilo + 1 : 0;
+                hilo[lane] = ilo;
+                hwild[lane] = tame ? 0 : 1;
+            }
+            if (lane < kHeightBatch) hz[lane] = zv;
+            int hincl = rows;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const int t = __shfl_up(hincl, d);
+                if (lane >= d) hincl += t;
+            }
+            const int R = __builtin_amdgcn_readlane(hincl, kWave - 1);
+            if (lane < kHeightBatch) hpre[lane] = hincl - rows;
+            wave_lds_sync();
+            for (int s0 = 0; s0 < R; s0 += kWave) {
+                // lanes over the batch's candidate rows, heights packed: the
+                // run of candidate cells of each
+                const int sl = s0 + lane;
+                int jlo = 1, jhi = 0, hs = 0, ri = 0;
+                if (sl < R) {
+                    // its height: the last with row prefix <= sl
+#pragma unroll
+                    for (int step = kHeightBatch / 2; step >= 1; step >>= 1)
+                        if (hpre[hs + step] <= sl) hs += step;
+                    ri = hilo[hs] + (sl - hpre[hs]);
+                    if (hwild[hs]) {
+                        jlo = 0;
+                        jhi = p.Y - 1;
+                    } else {
+                        const double x = p.x_min_d + ((double)ri + 0.5) * p.dx_d;
+                        double lo = -1.0, hi = Yd;
+                        bool empty = false;
+#pragma unroll
+                        for (int q = 0; q < 5; ++q) {
+                            const double v = ptab[q * 8 + 0] * x + hg[hs * 5 + q];
+                            if (kind[q] > 0) lo = fmax(lo, -v * ptab[q * 8 + 2]);
+                            else if (kind[q] < 0) hi = fmin(hi, -v * ptab[q * 8 + 2]);
+                            else empty = empty || (v + ptab[q * 8 + 3] < 0.0);
+                        }
+                        lo = fmin(lo, Yd);
+                        hi = fmax(hi, -1.0);
+                        if (!empty) {
+                            jlo = max(0, (int)ceil(lo));
+                            jhi = min(p.Y - 1, (int)floor(hi));
+                        }
+                    }
+                }
+                const int cn = jhi >= jlo ? jhi - jlo + 1 : 0;
+                // inclusive prefix over the lanes
+                int incl = cn;
+#pragma unroll
+                for (int d = 1; d < kWave; d <<= 1) {
+                    const int t = __shfl_up(incl, d);
+                    if (lane >= d) incl += t;
+                }
+                const int total = __builtin_amdgcn_readlane(incl, kWave - 1);
+                if (total == 0) continue;
+                rpre[lane] = incl - cn;
+                rjlo[lane] = jlo;
+                rhs[lane] = hs;
+                rci[lane] = ri;
+                wave_lds_sync();
+                for (int kb = 0; kb < total; kb += kWave) {
+                    // candidate kb + lane: its row is the last with prefix <= it
+                    const int kk = kb + lane;
+                    int lo = 0;
+#pragma unroll
+                    for (int step = 32; step >= 1; step >>= 1)
+                        if (lo + step < kWave && rpre[lo + step] <= kk) lo += step;
+                    const bool c_ok = kk < total;
+                    const int ci = rci[lo];
+                    const int cj = rjlo[lo] + (kk - rpre[lo]);
+                    const int hc = rhs[lo];
+                    const int k = k0 + hc;
+                    const float zc = hz[hc];
+                    const int q = ci * p.Y + cj;
+                    // den_z of the point, read ahead of the test that needs it
+                    const int den = c_ok ? (int)denb[(size_t)q * p.Z + k] : 0;
+                    // exact test: the forward's recipe for camera n
+                    bool t0 = false, t1 = false;
+                    float w0 = 0.0f, w1 = 0.0f;
+                    int x0 = 0;
+                    uint32_t goff = 0;
+                    if (c_ok) {
+                        const float x = p.x_min + ((float)ci + 0.5f) * p.dx;
+                        const float y = p.y_min + ((float)cj + 0.5f) * p.dy;
+                        const float up = ((mr[0] * x + mr[1] * y) + mr[2] * zc) + mr[3];
+                        const float vp = ((mr[4] * x + mr[5] * y) + mr[6] * zc) + mr[7];
+                        const float d = ((mr[8] * x + mr[9] * y) + mr[10] * zc) + mr[11];
+                        const float u = up / d;
+                        const float v = vp / d;
+                        const bool ok = (d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) &&
+                                        (v >= 0.0f) && (v < p.img_h);
+                        if (ok) {
+                            const float xf = u * p.sx - 0.5f;
+                            const float yf = v * p.sy - 0.5f;
+                            const float x0f = floorf(xf), y0f = floorf(yf);
+                            const float ax = xf - x0f, ay = yf - y0f;
+                            x0 = (int)x0f;
+                            const int y0 = (int)y0f;
+                            // the group's row py is this sample's row y0 + 1
+                            // (weight ay) or y0 (weight 1 - ay)
+                            const bool yrow = (y0 == py - 1) || (y0 == py);
+                            if (yrow) {
+                                const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
+                                const float wy = ((y0 == py) ? 1.0f - ay : ay) * inv;
+                                w0 = (1.0f - ax) * wy;   // tap column x0
+                                w1 = ax * wy;            // tap column x0 + 1
+                                t0 = x0 >= px0 && x0 < px0 + g;
+                                t1 = x0 + 1 >= px0 && x0 + 1 < px0 + g;
+                                goff = cam_gt + (uint32_t)q * p.row_bytes;
+                            }
+                        }
+                    }
+                    // append the terms to the pixels' lists (candidate order)
+                    for (int m = 0; m < g; ++m) {
+                        const bool mine = (t0 && x0 == px0 + m) || (t1 && x0 + 1 == px0 + m);
+                        const uint64_t mask = __ballot(mine);
+                        const int base = __builtin_amdgcn_readlane(cnt_lane, m);
+                        if (mine) {
+                            const int pos = base + __builtin_amdgcn_mbcnt_hi(
+                                                       (uint32_t)(mask >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                            wl[m * RS + pos] = (x0 == px0 + m) ? w0 : w1;
+                            ol[m * RS + pos] = goff;
+                        }
+                        const int c = base + __popcll(mask);
+                        cnt_lane = lane == m ? c : cnt_lane;
+                        maxcnt = c > maxcnt ? c : maxcnt;
+                    }
+                    // a list may take up to 64 more terms before the next flush
+                    if (maxcnt > RS - 1 - kWave - kGatherUnroll) flush();
+                }
+                wave_lds_sync();
+            }
+            wave_lds_sync();   // the height tables are rewritten by the next batch
+        }
+    }
+    if (maxcnt > 0) flush();
+
+    // single write of the group's gradient rows (NHWC, contiguous)
+    if (g_active) {
+        float *dst = p.gfeat + ((((size_t)b * p.N + n) * p.H + py) * p.W + px0 + m_g) * p.C;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+            const int vi = slot + L * v;
+            if (VPL == 1 || vi < p.nvec) {
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) dst[vi * EPV + e] = acc[v][e];
+            }
+        }
+    }
+}
+
 // Zero-fills n floats at dst (any 4-byte alignment): a 16-byte aligned body
 // with vector stores plus scalar head and tail.
 __global__ void __launch_bounds__(256) zero_fill(float *dst, uint64_t n)
@@ -1806,6 +2351,152 @@ int make_bwd_plan(const flashbev_features *f, const float *l2i, const flashbev_b
     return FLASHBEV_OK;
 }
 
+// Plan of the gather-form backward (sample_vt_bwd_prep, sample_vt_bwd_gather).
+struct BwdGatherPlan {
+    BwdGatherParams prm;
+    int64_t prep_wgs;      // prep workgroups (0: no cells)
+    int64_t gather_wgs;    // gather workgroups (0: no pixels)
+    size_t lds;            // gather dynamic LDS per workgroup
+    int lw, vpl;
+    uint64_t ws_bytes;     // workspace bytes needed
+};
+
+constexpr int kGatherWaves = 4;   // gather: wavefronts per workgroup
+
+using BwdGatherFn = void (*)(const BwdGatherParams);
+
+template <int LW>
+BwdGatherFn pick_gather_vpl(int vpl)
+{
+    switch (vpl) {
+    case 1: return sample_vt_bwd_gather<LW, 1>;
+    case 2: return sample_vt_bwd_gather<LW, 2>;
+    default: return sample_vt_bwd_gather<LW, 4>;
+    }
+}
+
+BwdGatherFn pick_gather(int lw, int vpl)
+{
+    switch (lw) {
+    case 16: return pick_gather_vpl<16>(vpl);
+    case 8: return pick_gather_vpl<8>(vpl);
+    default: return pick_gather_vpl<4>(vpl);
+    }
+}
+
+uint64_t align256(uint64_t v) { return (v + 255u) & ~(uint64_t)255u; }
+
+// All argument checks of the gather-form backward, the workspace's layout
+// and size.  `need_data` requires the device pointers (and the workspace).
+int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
+                         const flashbev_bev_grid_spec *s, const flashbev_z_bins *zb,
+                         const float *gout, const float *gfeat, const void *ws, uint64_t ws_bytes,
+                         bool need_data, BwdGatherPlan *pl)
+{
+    // the shape, value, pointer and alias checks of the scatter-form backward
+    BwdPlan bp;
+    const int rc = make_bwd_plan(f, l2i, s, zb, gout, gfeat, need_data, &bp);
+    if (rc) return rc;
+    const uint64_t XY = (uint64_t)s->X * (uint64_t)s->Y;
+    const uint64_t row = (uint64_t)f->C * 4u;   // float32 gradient rows
+    if (row > FLASHBEV_ROW_BYTES_MAX) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t gt_bytes = size_prod({(uint64_t)f->B, XY, row});
+    if (gt_bytes > kFeatBytesMax) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t den_bytes = size_prod({(uint64_t)f->B, XY, (uint64_t)zb->Z});
+    if (den_bytes > kFeatBytesMax) return FLASHBEV_ERR_UNSUPPORTED;
+    const uint64_t need = align256(gt_bytes) + align256(den_bytes);
+    memset(pl, 0, sizeof(*pl));
+    pl->ws_bytes = need;
+    const uint64_t gelems = bp.gfeat_elems;
+    const uint64_t pixels = size_prod({(uint64_t)f->B, (uint64_t)f->N, (uint64_t)f->H});
+    if (need_data && gelems > 0 && need > 0) {
+        if (!ws) return FLASHBEV_ERR_NULLPTR;
+        if ((uintptr_t)ws % 256u) return FLASHBEV_ERR_ALIGN;
+        if (ws_bytes < need) return FLASHBEV_ERR_VALUE;
+        // the workspace overlaps none of the call's buffers
+        if (overlaps(ws, need, gfeat, gelems * 4) ||
+            overlaps(ws, need, gout, size_prod({(uint64_t)f->B, (uint64_t)f->C, XY}) * 4) ||
+            overlaps(ws, need, l2i, (size_t)f->B * f->N * 64))
+            return FLASHBEV_ERR_ALIAS;
+    }
+    // lanes over a gradient row: the widest of 16/8/4-byte vectors, one to
+    // four per lane so that a wavefront holds at least two pixels (four from
+    // 1 KiB rows on), as the forward lays out its feature rows
+    int lw = 16;
+    while (lw > 4 && (row % lw) != 0) lw >>= 1;
+    const int nvec = (int)(row / lw);
+    int vpl = 1;
+    while (vpl < 4 && (nvec + vpl - 1) / vpl > kWave) vpl <<= 1;
+    const int min_cpw = row >= 1024 ? 4 : 2;
+    while (vpl < 4 && kWave / ((nvec + vpl - 1) / vpl) < min_cpw && nvec >= 2 * vpl) vpl <<= 1;
+    const int lpc = (nvec + vpl - 1) / vpl;
+    if (lpc > kWave) return FLASHBEV_ERR_UNSUPPORTED;
+    int cpw = kWave / lpc;
+    if (cpw > kCpwMax) cpw = kCpwMax;
+
+    BwdGatherParams &p = pl->prm;
+    p.l2i = l2i;
+    p.gout = gout;
+    p.gfeat = const_cast<float *>(gfeat);
+    p.gt = reinterpret_cast<float *>(const_cast<void *>(ws));
+    p.den = ws ? reinterpret_cast<uint8_t *>(const_cast<void *>(ws)) + align256(gt_bytes) : nullptr;
+    p.gt_bytes = (uint32_t)gt_bytes;
+    p.B = f->B; p.N = f->N; p.H = f->H; p.W = f->W; p.C = f->C;
+    p.X = s->X; p.Y = s->Y; p.Z = zb->Z;
+    p.XY = (int32_t)XY;
+    p.img_w = (float)f->img_w;
+    p.img_h = (float)f->img_h;
+    p.sx = (float)f->W / (float)f->img_w;
+    p.sy = (float)f->H / (float)f->img_h;
+    p.x_min = s->x_min; p.dx = s->dx; p.y_min = s->y_min; p.dy = s->dy;
+    p.depth_eps = s->depth_eps;
+    p.reduce = s->reduce;
+    p.dx_d = s->dx; p.dy_d = s->dy; p.x_min_d = s->x_min; p.y_min_d = s->y_min;
+    p.isx_d = 1.0 / (double)p.sx;
+    p.isy_d = 1.0 / (double)p.sy;
+    // a bound on |x| of every cell centre and on the terms that form it in
+    // float32 (x_min and (i + 1/2) dx), so that the rounding of a centre is
+    // a few 2^-24 of it
+    p.xmax_abs = fabs((double)s->x_min) + ((double)s->X + 1.0) * fabs((double)s->dx);
+    p.ymax_abs = fabs((double)s->y_min) + ((double)s->Y + 1.0) * fabs((double)s->dy);
+    p.prep_tiles_per_b = (int32_t)((XY + kPrepCells - 1) / kPrepCells);
+    p.prep_cblocks = (f->C + 63) / 64;
+    p.cpw = cpw;
+    p.lpc = lpc;
+    p.nvec = nvec;
+    p.rcp_lpc = 1.0f / (float)lpc;
+    p.groups_per_row = (f->W + cpw - 1) / cpw;
+    p.groups = (int64_t)pixels * p.groups_per_row;
+    p.rec_stride = kGatherRec | 1;
+    p.row_bytes = (uint32_t)row;
+    p.lds_wave = align16((uint32_t)cpw * (uint32_t)p.rec_stride * 8u + kGatherTail);
+    for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
+
+    pl->prep_wgs = (gelems > 0) ? (int64_t)f->B * p.prep_tiles_per_b * p.prep_cblocks : 0;
+    pl->gather_wgs = (gelems > 0) ? (p.groups + kGatherWaves - 1) / kGatherWaves : 0;
+    if (pl->prep_wgs > 0x7FFFFFFFll || pl->gather_wgs > 0x7FFFFFFFll) return FLASHBEV_ERR_UNSUPPORTED;
+    pl->lds = (size_t)p.lds_wave * kGatherWaves;
+    if (pl->lds > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
+    pl->lw = lw;
+    pl->vpl = vpl;
+    return FLASHBEV_OK;
+}
+
+int launch_bwd_gather(const BwdGatherPlan &pl, hipStream_t st)
+{
+    void *args[] = {const_cast<BwdGatherParams *>(&pl.prm)};
+    if (pl.prep_wgs > 0 &&
+        hipLaunchKernel(reinterpret_cast<const void *>(sample_vt_bwd_prep),
+                        dim3((unsigned)pl.prep_wgs), dim3(256), args, 0, st) != hipSuccess)
+        return FLASHBEV_ERR_HIP;
+    if (pl.gather_wgs > 0 &&
+        hipLaunchKernel(reinterpret_cast<const void *>(pick_gather(pl.lw, pl.vpl)),
+                        dim3((unsigned)pl.gather_wgs), dim3(kGatherWaves * kWave), args, pl.lds,
+                        st) != hipSuccess)
+        return FLASHBEV_ERR_HIP;
+    return FLASHBEV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1914,4 +2605,32 @@ extern "C" int flashbev_sample_vt_backward(const flashbev_features *features,
                                          dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
                                          pl.lds, st);
     return e == hipSuccess ? FLASHBEV_OK : FLASHBEV_ERR_HIP;
+}
+
+extern "C" int flashbev_backward_workspace_size(const flashbev_features *features,
+                                                const flashbev_bev_grid_spec *spec,
+                                                const flashbev_z_bins *z_bins, uint64_t *bytes)
+{
+    if (!bytes) return FLASHBEV_ERR_NULLPTR;
+    BwdGatherPlan pl;
+    const int rc = make_bwd_gather_plan(features, nullptr, spec, z_bins, nullptr, nullptr, nullptr,
+                                        0, false, &pl);
+    if (rc) return rc;
+    *bytes = pl.ws_bytes;
+    return FLASHBEV_OK;
+}
+
+extern "C" int flashbev_sample_vt_backward_ws(const flashbev_features *features,
+                                              const float *lidar2img,
+                                              const flashbev_bev_grid_spec *spec,
+                                              const flashbev_z_bins *z_bins,
+                                              const float *grad_out, float *grad_features,
+                                              void *workspace, uint64_t workspace_bytes,
+                                              void *stream)
+{
+    BwdGatherPlan pl;
+    const int rc = make_bwd_gather_plan(features, lidar2img, spec, z_bins, grad_out, grad_features,
+                                        workspace, workspace_bytes, true, &pl);
+    if (rc) return rc;
+    return launch_bwd_gather(pl, reinterpret_cast<hipStream_t>(stream));
 }

@@ -347,3 +347,73 @@ def test_backward_plan_on_extreme_grid_sides(X, Y):
         assert e.status != 0
         return
     assert 0 < info["workgroups"] <= 2**31 - 1
+
+
+WS = 0x7F3000000000  # fake workspace address
+
+
+def test_gather_backward_workspace_size():
+    """Gt (float32 B X Y C) then den_z (uint8 B X Y Z), each padded to 256
+    bytes; -1 (the scatter form serves it) where Gt would reach 2^31 bytes."""
+    grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32)
+    for B, C, Z in ((1, 80, 8), (4, 128, 8), (2, 64, 8), (1, 1, 1), (3, 7, 13)):
+        zz = np.linspace(-4, 2, Z).astype(np.float32)
+        got = fb.backward_workspace_size((B, 6, 32, 88, C), "f32", zz, grid, (256, 704))
+        gt = B * 200 * 200 * C * 4
+        den = B * 200 * 200 * Z
+        assert got == -(-gt // 256) * 256 + -(-den // 256) * 256, (B, C, Z)
+    big = fb.BevGrid(-50, .5, 4096, -50, .5, 4096)
+    assert fb.backward_workspace_size((1, 6, 32, 88, 64), "f32", z, big, (256, 704)) == -1
+    with pytest.raises(fb.FlashBevError):
+        fb.backward_workspace_size((1, 6, 32, 88, 80), "f32", np.zeros(300), grid, (256, 704))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ws=0), "ERR_NULLPTR"),
+    (dict(ws=WS + 16), "ERR_ALIGN"),
+    (dict(ws_bytes=-1), "ERR_VALUE"),
+    (dict(ws=OUT), "ERR_ALIAS"),
+    (dict(ws=FEAT - 256), "ERR_ALIAS"),
+    (dict(ws=L2I), "ERR_ALIAS"),
+    (dict(gout=0), "ERR_NULLPTR"),
+    (dict(gout=OUT + 2), "ERR_ALIGN"),
+    (dict(shape=(1, 6, 32, 88, 1025)), "ERR_UNSUPPORTED"),
+    (dict(X=4096, Y=4096), "ERR_UNSUPPORTED"),
+    (dict(reduce=2), "ERR_VALUE"),
+])
+def test_gather_backward_argument_errors(kw, status):
+    """Every check of flashbev_sample_vt_backward_ws precedes its first HIP
+    call; ws_bytes=-1 means one byte fewer than the workspace needs."""
+    shape = kw.get("shape", (1, 6, 32, 88, 80))
+    X, Y = kw.get("X", 200), kw.get("Y", 200)
+    grid = fb.BevGrid(-50, .5, X, -50, .5, Y)
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32)
+    reduce = kw.get("reduce", "mean")
+    try:
+        need = fb.backward_workspace_size(shape, "f32", z, grid, (256, 704))
+    except fb.FlashBevError:
+        need = 0
+    ws_bytes = kw.get("ws_bytes", need)
+    if ws_bytes == -1:
+        ws_bytes = need - 1
+    if reduce == 2:
+        f, g, zb = fb._structs(shape, 0, 0, (256, 704), grid, z, "mean")
+        g.reduce = 2
+        rc = fb._lib().flashbev_sample_vt_backward_ws(
+            ctypes.byref(f), ctypes.c_void_p(L2I), ctypes.byref(g), ctypes.byref(zb),
+            ctypes.c_void_p(OUT), ctypes.c_void_p(FEAT), ctypes.c_void_p(WS),
+            ctypes.c_uint64(need), ctypes.c_void_p(0))
+    else:
+        rc = fb.sample_vt_backward_ws_raw(shape, "f32", L2I, z, grid, (256, 704),
+                                          kw.get("gout", OUT), FEAT, kw.get("ws", WS),
+                                          max(ws_bytes, 0))
+    assert rc == S[status]
+
+
+def test_gather_backward_empty_shapes_enqueue_nothing():
+    grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32)
+    for shape in ((0, 6, 32, 88, 80), (1, 0, 32, 88, 80)):
+        assert fb.sample_vt_backward_ws_raw(shape, "f32", L2I, z, grid, (256, 704), OUT, FEAT,
+                                            0, 0) == S["OK"]
