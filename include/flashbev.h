@@ -54,6 +54,8 @@ extern "C" {
 #define FLASHBEV_NMAX 64
 /* Largest feature row (C times the element size) in bytes. */
 #define FLASHBEV_ROW_BYTES_MAX 4096
+/* Size of the library's static device scratch (flashbev_sample_vt_backward_noalloc). */
+#define FLASHBEV_SCRATCH_BYTES 67108864
 
 /* Status codes.  Every argument check runs before any HIP call. */
 typedef enum {
@@ -65,7 +67,8 @@ typedef enum {
     FLASHBEV_ERR_UNSUPPORTED = -5, /* beyond a documented limit (Z, N, row, 2 GiB) */
     FLASHBEV_ERR_ALIAS = -6,       /* out overlaps an input                      */
     FLASHBEV_ERR_VALUE = -7,       /* non-finite grid spec or bad reduce mode    */
-    FLASHBEV_ERR_HIP = -8          /* the kernel launch failed                   */
+    FLASHBEV_ERR_HIP = -8,         /* the kernel launch failed                   */
+    FLASHBEV_ERR_SCRATCH = -9      /* needs more than FLASHBEV_SCRATCH_BYTES     */
 } flashbev_status;
 
 /* Feature element type; accumulation is float32 for all of them. */
@@ -214,6 +217,31 @@ int flashbev_sample_vt_backward_ws(const flashbev_features *features, const floa
                                    const flashbev_z_bins *z_bins, const float *grad_out,
                                    float *grad_features, void *workspace,
                                    uint64_t workspace_bytes, void *stream);
+
+/*
+ * flashbev_sample_vt_backward_ws without a caller workspace and without any
+ * allocation, for callers that cannot call hipMalloc: work captured into a
+ * HIP graph, tight serving loops, harnesses that forbid allocation.  The
+ * workspace is a static device array of FLASHBEV_SCRATCH_BYTES (64 MiB) that
+ * the library holds on each GPU it runs on until the process ends; its
+ * address on the current device is looked up once, on the first call on
+ * that device.  The call makes no hipMalloc, hipFree or other allocating
+ * call.
+ *
+ * Arguments, results and errors are those of flashbev_sample_vt_backward_ws
+ * without `workspace` and `workspace_bytes`; in addition it returns
+ * FLASHBEV_ERR_SCRATCH, before any HIP call, when the workspace the call
+ * needs (flashbev_backward_workspace_size) exceeds FLASHBEV_SCRATCH_BYTES.
+ * Every call on a GPU uses that GPU's one scratch array: calls that can
+ * overlap on one GPU (on different streams, or from several threads) race
+ * and must be ordered by the caller.  Nothing in the scratch needs to be
+ * zero on entry; a call overwrites what it reads.
+ */
+int flashbev_sample_vt_backward_noalloc(const flashbev_features *features,
+                                        const float *lidar2img,
+                                        const flashbev_bev_grid_spec *spec,
+                                        const flashbev_z_bins *z_bins, const float *grad_out,
+                                        float *grad_features, void *stream);
 
 /*
  * Workspace bytes flashbev_sample_vt_backward_ws needs for these arguments

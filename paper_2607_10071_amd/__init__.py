@@ -30,11 +30,13 @@ REDUCE_CODES = {"mean": 0, "sum": 1}
 STATUS = {
     "OK": 0, "ERR_NULLPTR": -1, "ERR_SHAPE": -2, "ERR_DTYPE": -3, "ERR_ALIGN": -4,
     "ERR_UNSUPPORTED": -5, "ERR_ALIAS": -6, "ERR_VALUE": -7, "ERR_HIP": -8,
+    "ERR_SCRATCH": -9,
 }
 ABI_VERSION = 2
 ZMAX = 256
 NMAX = 64
 ROW_BYTES_MAX = 4096
+SCRATCH_BYTES = 64 << 20
 
 
 class FlashBevError(RuntimeError):
@@ -129,6 +131,10 @@ def _lib():
                                                      ctypes.c_void_p, ctypes.c_uint64,
                                                      ctypes.c_void_p]
         L.flashbev_sample_vt_backward_ws.restype = ctypes.c_int
+        L.flashbev_sample_vt_backward_noalloc.argtypes = [P(Features), ctypes.c_void_p,
+                                                          P(GridSpec), P(ZBins), ctypes.c_void_p,
+                                                          ctypes.c_void_p, ctypes.c_void_p]
+        L.flashbev_sample_vt_backward_noalloc.restype = ctypes.c_int
         L.flashsca_forward.argtypes = [P(ScaValue), ctypes.c_void_p, P(GridSpec), P(ZBins),
                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p]
@@ -416,6 +422,46 @@ def sample_vt_backward_ws_raw(shape, dtype: str, lidar2img_ptr: int, z_bins, gri
         ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr), ctypes.byref(g), ctypes.byref(zb),
         ctypes.c_void_p(grad_out_ptr), ctypes.c_void_p(grad_features_ptr),
         ctypes.c_void_p(workspace_ptr), ctypes.c_uint64(workspace_bytes),
+        ctypes.c_void_p(stream)))
+
+
+def sample_vt_backward_noalloc(grad_out, lidar2img, z_bins, grid: BevGrid, img_hw,
+                               features_shape, features_dtype, grad_features,
+                               reduce: str = "mean", stream=None):
+    """The gather-form backward on the library's static device scratch
+    (flashbev_sample_vt_backward_noalloc): nothing is allocated, here or in
+    the library, so ``grad_features`` is required.  Calls that can overlap on
+    one GPU share its scratch and must be ordered by the caller.  Raises
+    FlashBevError with status ERR_SCRATCH when the call needs more than
+    SCRATCH_BYTES of workspace."""
+    B, N, H, W, C = _check_backward(grad_out, lidar2img, grid, features_shape)
+    _check_out(grad_features, (B, N, H, W, C), "grad_features")
+    features_dtype = _dtype_name(features_dtype)
+    z = _z_array(z_bins)
+    f, g, zb = _structs((B, N, H, W, C), DTYPE_CODES[features_dtype], 0, img_hw, grid, z, reduce)
+    dev = _one_device(grad_out, lidar2img, grad_features)
+    s = _stream_handle(stream, dev)
+    with _on_device(dev):
+        rc = _lib().flashbev_sample_vt_backward_noalloc(
+            ctypes.byref(f), ctypes.c_void_p(lidar2img.data_ptr()), ctypes.byref(g),
+            ctypes.byref(zb), ctypes.c_void_p(grad_out.data_ptr()),
+            ctypes.c_void_p(grad_features.data_ptr()), ctypes.c_void_p(s))
+    if rc != 0:
+        raise FlashBevError(rc, "flashbev_sample_vt_backward_noalloc")
+    return grad_features
+
+
+def sample_vt_backward_noalloc_raw(shape, dtype: str, lidar2img_ptr: int, z_bins,
+                                   grid: BevGrid, img_hw, grad_out_ptr: int,
+                                   grad_features_ptr: int, reduce: str = "mean",
+                                   stream: int = 0) -> int:
+    """flashbev_sample_vt_backward_noalloc with raw device addresses; returns
+    the status."""
+    z = _z_array(z_bins)
+    f, g, zb = _structs(shape, DTYPE_CODES[dtype], 0, img_hw, grid, z, reduce)
+    return int(_lib().flashbev_sample_vt_backward_noalloc(
+        ctypes.byref(f), ctypes.c_void_p(lidar2img_ptr), ctypes.byref(g), ctypes.byref(zb),
+        ctypes.c_void_p(grad_out_ptr), ctypes.c_void_p(grad_features_ptr),
         ctypes.c_void_p(stream)))
 
 

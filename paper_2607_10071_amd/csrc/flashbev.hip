@@ -41,6 +41,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "flashbev.h"
 #include "hip_common.h"
 
@@ -2391,7 +2393,7 @@ uint64_t align256(uint64_t v) { return (v + 255u) & ~(uint64_t)255u; }
 int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
                          const flashbev_bev_grid_spec *s, const flashbev_z_bins *zb,
                          const float *gout, const float *gfeat, const void *ws, uint64_t ws_bytes,
-                         bool need_data, BwdGatherPlan *pl)
+                         bool need_data, BwdGatherPlan *pl, bool check_ws = true)
 {
     // the shape, value, pointer and alias checks of the scatter-form backward
     BwdPlan bp;
@@ -2409,7 +2411,7 @@ int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
     pl->ws_bytes = need;
     const uint64_t gelems = bp.gfeat_elems;
     const uint64_t pixels = size_prod({(uint64_t)f->B, (uint64_t)f->N, (uint64_t)f->H});
-    if (need_data && gelems > 0 && need > 0) {
+    if (need_data && check_ws && gelems > 0 && need > 0) {
         if (!ws) return FLASHBEV_ERR_NULLPTR;
         if ((uintptr_t)ws % 256u) return FLASHBEV_ERR_ALIGN;
         if (ws_bytes < need) return FLASHBEV_ERR_VALUE;
@@ -2515,6 +2517,7 @@ const char *flashbev_status_string(int status)
     case FLASHBEV_ERR_ALIAS: return "output overlaps an input";
     case FLASHBEV_ERR_VALUE: return "non-finite grid spec or bad reduce mode";
     case FLASHBEV_ERR_HIP: return "HIP kernel launch failed";
+    case FLASHBEV_ERR_SCRATCH: return "needs more than the static scratch (FLASHBEV_SCRATCH_BYTES)";
     default: return "unknown status";
     }
 }
@@ -2618,6 +2621,60 @@ extern "C" int flashbev_backward_workspace_size(const flashbev_features *feature
     if (rc) return rc;
     *bytes = pl.ws_bytes;
     return FLASHBEV_OK;
+}
+
+// The no-allocation variant's workspace: a file-scope device array.  Host
+// code never takes the array's name as a device address (in host code it
+// names a host-side stand-in); the address on each device comes from
+// hipGetSymbolAddress, once per device, and is kept.
+static __device__ __align__(256) unsigned char scratch[FLASHBEV_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kScratchDevices = 256;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kScratchDevices];
+
+// The scratch array's address on the current device.
+int scratch_on_current_device(void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices)
+        return FLASHBEV_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return FLASHBEV_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return FLASHBEV_OK;
+}
+
+}  // namespace
+
+extern "C" int flashbev_sample_vt_backward_noalloc(const flashbev_features *features,
+                                                   const float *lidar2img,
+                                                   const flashbev_bev_grid_spec *spec,
+                                                   const flashbev_z_bins *z_bins,
+                                                   const float *grad_out, float *grad_features,
+                                                   void *stream)
+{
+    // every argument check first (no HIP call), then the size limit
+    BwdGatherPlan pl;
+    int rc = make_bwd_gather_plan(features, lidar2img, spec, z_bins, grad_out, grad_features,
+                                  nullptr, 0, true, &pl, false);
+    if (rc) return rc;
+    if (pl.ws_bytes > (uint64_t)FLASHBEV_SCRATCH_BYTES) return FLASHBEV_ERR_SCRATCH;
+    if (pl.prep_wgs == 0 && pl.gather_wgs == 0) return FLASHBEV_OK;
+    void *ws = nullptr;
+    rc = scratch_on_current_device(&ws);
+    if (rc) return rc;
+    rc = make_bwd_gather_plan(features, lidar2img, spec, z_bins, grad_out, grad_features, ws,
+                              (uint64_t)FLASHBEV_SCRATCH_BYTES, true, &pl);
+    if (rc) return rc;
+    return launch_bwd_gather(pl, reinterpret_cast<hipStream_t>(stream));
 }
 
 extern "C" int flashbev_sample_vt_backward_ws(const flashbev_features *features,

@@ -72,7 +72,8 @@ def test_abi_version_and_status_strings():
 def test_header_constants_match_binding():
     src = open(HEADER).read()
     for k, v in (("FLASHBEV_ZMAX", fb.ZMAX), ("FLASHBEV_NMAX", fb.NMAX),
-                 ("FLASHBEV_ROW_BYTES_MAX", fb.ROW_BYTES_MAX), ("FLASHBEV_ABI_VERSION", fb.ABI_VERSION)):
+                 ("FLASHBEV_ROW_BYTES_MAX", fb.ROW_BYTES_MAX), ("FLASHBEV_ABI_VERSION", fb.ABI_VERSION),
+                 ("FLASHBEV_SCRATCH_BYTES", fb.SCRATCH_BYTES)):
         assert re.search(rf"#define {k} {v}\b", src), k
     for k, v in fb.STATUS.items():
         assert re.search(rf"FLASHBEV_{k} = {v}\b", src), k
@@ -417,3 +418,25 @@ def test_gather_backward_empty_shapes_enqueue_nothing():
     for shape in ((0, 6, 32, 88, 80), (1, 0, 32, 88, 80)):
         assert fb.sample_vt_backward_ws_raw(shape, "f32", L2I, z, grid, (256, 704), OUT, FEAT,
                                             0, 0) == S["OK"]
+
+
+def test_noalloc_backward_checks_before_any_hip_call():
+    """flashbev_sample_vt_backward_noalloc: argument errors, then the static
+    scratch's limit, all before any HIP call (this box has no GPU)."""
+    grid = fb.BevGrid(-50, .5, 200, -50, .5, 200)
+    z = np.linspace(-4.5, 2.5, 8).astype(np.float32)
+    shape = (1, 6, 32, 88, 80)
+    raw = fb.sample_vt_backward_noalloc_raw
+    assert raw(shape, "f32", L2I, z, grid, (256, 704), 0, FEAT) == S["ERR_NULLPTR"]
+    assert raw(shape, "f32", L2I, z, grid, (256, 704), OUT + 2, FEAT) == S["ERR_ALIGN"]
+    assert raw(shape, "f32", L2I, z, grid, (256, 704), OUT, OUT) == S["ERR_ALIAS"]
+    assert raw((1, 6, 32, 88, 1025), "f32", L2I, z, grid, (256, 704), OUT, FEAT) == \
+        S["ERR_UNSUPPORTED"]
+    # 4 x 200 x 200 x 128 float32 rows of Gt: 82 MB, above the 64 MiB scratch
+    need = fb.backward_workspace_size((4, 6, 32, 88, 128), "bf16", z, grid, (256, 704))
+    assert need > fb.SCRATCH_BYTES
+    assert raw((4, 6, 32, 88, 128), "bf16", L2I, z, grid, (256, 704), OUT, FEAT) == \
+        S["ERR_SCRATCH"]
+    # nothing to do: no HIP call either
+    assert raw((0, 6, 32, 88, 80), "f32", L2I, z, grid, (256, 704), OUT, FEAT) == S["OK"]
+    assert fb.status_string(S["ERR_SCRATCH"]) != "unknown status"
