@@ -1352,9 +1352,10 @@ constexpr int kHeightBatch = 32;    // heights whose rows one pass packs togethe
 constexpr uint32_t kGatherTail = 4u * kWave * 4u + (5u * 8u + 36u * 2u + kHeightBatch * 5u) * 8u +
                                  4u * kHeightBatch * 4u;
 
-// Prep: Gt rows of 64 consecutive cells for 64 channels, and (in the
-// workgroups of the first channel block) den_z of those cells.  256
-// threads; each moves 16 values with its loads all in flight.
+// Prep: Gt rows of 64 consecutive cells for 64 channels, and a share of
+// den_z of those cells (the tile's (cell, height) pairs are split over its
+// channel blocks).  256 threads; each moves 16 values with its loads all in
+// flight.
 __global__ void __launch_bounds__(256) sample_vt_bwd_prep(const BwdGatherParams p)
 {
     __shared__ float s_mat[FLASHBEV_NMAX * 12];
@@ -1391,15 +1392,19 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_prep(const BwdGatherParams 
             if (cc < nc && cl < ncell) tb[(size_t)(q0 + cl) * p.C + c0 + cc] = s_t[cl][cc];
         }
     }
-    if (cb != 0) return;   // block-uniform; no barrier follows in this branch
     const int N = p.N;
     for (int t = tid; t < N * 12; t += 256) {
         const int n = t / 12, r = t - n * 12;
         s_mat[t] = p.l2i[((size_t)b * N + n) * 16 + r];
     }
     __syncthreads();
-    // den_z: thread per (cell, height), cameras in a loop, the forward's recipe
-    for (int t = tid; t < ncell * p.Z; t += 256) {
+    // den_z: thread per (cell, height), cameras in a loop, the forward's
+    // recipe (a quotient is formed only where the tests before it pass,
+    // which leaves every decision as the forward takes it)
+    const int items = ncell * p.Z;
+    const int share = (items + p.prep_cblocks - 1) / p.prep_cblocks;
+    const int t_end = min(items, (cb + 1) * share);
+    for (int t = cb * share + tid; t < t_end; t += 256) {
         const int c = t / p.Z, k = t - c * p.Z;
         const int q = q0 + c;
         const int i = q / p.Y, j = q - (q / p.Y) * p.Y;
@@ -1412,10 +1417,13 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_prep(const BwdGatherParams 
             const float up = ((mr[0] * x + mr[1] * y) + mr[2] * zv) + mr[3];
             const float vp = ((mr[4] * x + mr[5] * y) + mr[6] * zv) + mr[7];
             const float d = ((mr[8] * x + mr[9] * y) + mr[10] * zv) + mr[11];
-            const float u = up / d;
-            const float v = vp / d;
-            den += ((d > p.depth_eps) && (u >= 0.0f) && (u < p.img_w) && (v >= 0.0f) &&
-                    (v < p.img_h)) ? 1 : 0;
+            if (d > p.depth_eps) {
+                const float u = up / d;
+                if (u >= 0.0f && u < p.img_w) {
+                    const float v = vp / d;
+                    den += (v >= 0.0f && v < p.img_h) ? 1 : 0;
+                }
+            }
         }
         p.den[((size_t)b * p.XY + q) * p.Z + k] = (uint8_t)den;
     }
@@ -2363,7 +2371,7 @@ struct BwdGatherPlan {
     uint64_t ws_bytes;     // workspace bytes needed
 };
 
-constexpr int kGatherWaves = 4;   // gather: wavefronts per workgroup
+constexpr int kGatherWaves = 1;   // gather: wavefronts per workgroup (one: finest balance)
 
 using BwdGatherFn = void (*)(const BwdGatherParams);
 
