@@ -303,16 +303,20 @@ def measure_backward(wl, inst, device, steps, warmup, taps=None, keep_grad=None,
     if keep_grad is not None:
         keep_grad.append(keep[2].cpu().numpy())
     sec = t["ms_per_step"] * 1e-3
-    rec = {**step_stats(t),
+    rec = {"method": method, **step_stats(t),
            "gsamples_per_s": round(wl.samples / sec / 1e9, 3),
            "hbm_bytes_per_call": backward_bytes(wl),
            "hbm_frac": round(backward_bytes(wl) / sec / 1e9 / HBM_PEAK_GBS, 5)}
     if taps is not None:
-        # every in-range tap contributes C float32 terms; a plain scatter adds
-        # each with a float atomic, so terms/s over the measured atomic ceiling
-        # says how far the tiled reduction goes beyond that design
+        # every in-range tap contributes C float32 terms
         rec["terms_per_call"] = taps * wl.C
         rec["terms_G_per_s"] = round(taps * wl.C / sec / 1e9, 1)
+        if method == "gather":
+            # the gather form reads one float32 row of the transposed output
+            # gradient per in-range tap: its gather traffic over the whole
+            # call (transpose and gather kernels)
+            rec["gt_gather_bytes_per_call"] = taps * wl.C * 4
+            rec["gt_gather_GB_per_s"] = round(taps * wl.C * 4 / sec / 1e9, 1)
     del fn, keep
     return rec
 
@@ -705,6 +709,8 @@ def main(argv=None) -> int:
                          "paper's reference setting (one JSON line)")
     ap.add_argument("--backward-only", action="store_true",
                     help="time only the backward (gradient w.r.t. the features) on the workload")
+    ap.add_argument("--backward-method", default="gather", choices=("gather", "scatter"),
+                    help="the backward's form for --backward-only")
     ap.add_argument("--sca-only", action="store_true",
                     help="time only the FlashSCA forward at BEVFormer-base defaults")
     ap.add_argument("--sca-points", default="8,16,32",
@@ -751,7 +757,8 @@ def main(argv=None) -> int:
     inst = synth.make_workload(wl)
     if args.backward_only:
         rec = {"pass": "backward", "workload": wl.name,
-               **measure_backward(wl, inst, device, args.steps, args.warmup)}
+               **measure_backward(wl, inst, device, args.steps, args.warmup,
+                                  method=args.backward_method)}
         print(json.dumps(rec), flush=True)
         return 0
     fn, feats, l2i, out, stream = make_call(wl, inst, device)
@@ -859,11 +866,16 @@ def main(argv=None) -> int:
         # the paper's reference setting, whose backward the paper times
         taps = rec.get("gather_roofline", {}).get("taps")
         grads = []
-        bwd = {wl.name: measure_backward(wl, inst, device, max(20, args.steps // 2), args.warmup,
-                                         taps, grads)}
+        bsteps = max(20, args.steps // 2)
+        # the gather form (the default) and, beside it, the scatter form
+        bwd = {wl.name: measure_backward(wl, inst, device, bsteps, args.warmup, taps, grads),
+               f"{wl.name}_scatter": measure_backward(wl, inst, device, bsteps, args.warmup, taps,
+                                                      method="scatter")}
         w3 = synth.config("paper_ref")
-        bwd["paper_ref"] = measure_backward(w3, synth.make_workload(w3), device,
-                                            max(20, args.steps // 2), args.warmup)
+        i3 = synth.make_workload(w3)
+        bwd["paper_ref"] = measure_backward(w3, i3, device, bsteps, args.warmup)
+        bwd["paper_ref_scatter"] = measure_backward(w3, i3, device, bsteps, args.warmup,
+                                                    method="scatter")
         bwd["paper_context"] = {"flashbev_a6000_backward_ms": 3.27,
                                 "tensorized_a6000_backward_ms": 17.90}
         if not args.no_cpu_baseline:
@@ -872,10 +884,22 @@ def main(argv=None) -> int:
             # (the columns of the paper's Table 2, backward row)
             bwd[wl.name]["parity"] = parity_stats(grads[0], cb.pop("ref"), cb.pop("scale"))
             bwd[wl.name]["cpu_baseline"] = cb
+        # the scatter form adds every term with a float atomic unless its
+        # tile holds the pixel: terms/s over the measured atomic ceiling says
+        # how far its tiled reduction goes beyond a plain atomic scatter
         ceil = rec.get("ceilings_GBs", {}).get("float_atomic_Gops")
-        if ceil and "terms_G_per_s" in bwd[wl.name]:
-            bwd[wl.name]["float_atomic_ceiling_Gops"] = ceil
-            bwd[wl.name]["terms_over_atomic_ceiling"] = round(bwd[wl.name]["terms_G_per_s"] / ceil, 3)
+        sc = bwd[f"{wl.name}_scatter"]
+        if ceil and "terms_G_per_s" in sc:
+            sc["float_atomic_ceiling_Gops"] = ceil
+            sc["terms_over_atomic_ceiling"] = round(sc["terms_G_per_s"] / ceil, 3)
+        # the gather form's Gt rows against the measured gather ceiling,
+        # measured at the forward's row size: the same size when the
+        # features are float32
+        gl2 = rec.get("ceilings_GBs", {}).get("gather_l2")
+        g = bwd[wl.name]
+        if gl2 and "gt_gather_GB_per_s" in g and wl.dtype == "f32":
+            g["gather_ceiling_GBs"] = gl2
+            g["gt_gather_frac_of_ceiling"] = round(g["gt_gather_GB_per_s"] / gl2, 4)
         rec["backward"] = bwd
         # FlashSCA (Sec. 4.5, Table 7) at BEVFormer-base defaults
         rec["sca"] = measure_sca(device, max(20, args.steps // 4), args.warmup,
