@@ -60,6 +60,13 @@ namespace {
 constexpr int kScaWave = 64;
 constexpr int kScaWavesMax = 4;
 constexpr int kScaThreads = kScaWave * kScaWavesMax;
+// The backward takes tiles of up to 8 wavefronts (64 queries of a head at
+// D = 32 float32: an 8 x 8 patch of the visiting order, whose taps share
+// more pixels in the row merge) within a larger LDS budget (measured on
+// MI355X at BEVFormer-base: P = 8 1.52 -> 1.48 ms, P = 32 4.77 -> 4.64 ms).
+constexpr int kScaBwdWavesMax = 8;
+constexpr int kScaBwdThreads = kScaWave * kScaBwdWavesMax;
+constexpr uint32_t kScaBwdLdsBudget = 80u * 1024u;
 constexpr int kScaXcds = 8;      // MI355X: workgroups are dispatched to 8 XCDs round-robin
 constexpr int kScaBlock = 16;    // queries are visited in blocks of 16 x 16 BEV cells
 // Offset of a tap that is not loaded: one camera's value is smaller than
@@ -563,7 +570,7 @@ sca_fwd(const ScaParams p)
 
 // Backward: gradients of value (scatter), offsets and logits.
 template <int DT, int LW>
-__global__ void __launch_bounds__(kScaThreads)
+__global__ void __launch_bounds__(kScaBwdThreads)
 sca_bwd(const ScaParams p)
 {
     constexpr int ES = ElemSize<DT>::value;
@@ -1006,7 +1013,8 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     const int spw = kScaWave / lph;
     const int slot_stride = lph * (backward ? kRecBwd : kRecFwd) + kSlotPad;
 
-    int waves = kScaWavesMax;
+    int waves = backward ? kScaBwdWavesMax : kScaWavesMax;
+    const uint32_t budget = backward ? kScaBwdLdsBudget : kScaLdsBudget;
     int nq_max = 0;
     ScaLds lay{};
     for (;;) {
@@ -1015,7 +1023,7 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
         nq_max = backward ? tp : (tp - 1) / v->heads + 2;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
         lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, D, slot_stride, backward);
-        if (lay.total <= kScaLdsBudget || waves == 1) break;
+        if (lay.total <= budget || waves == 1) break;
         waves >>= 1;
     }
     // many points per head: one wavefront per workgroup, with more LDS

@@ -216,23 +216,24 @@ def test_backward_launch_geometry():
              grid=fb.BevGrid(-51.2, 0.512, 200, -51.2, 0.512, 200), img_hw=(900, 1600), P=8)
     f = fb.sca_launch_info(**d)
     b = fb.sca_launch_info(**d, backward=True)
-    # same lanes and launch size; a backward tile holds 32 queries (4
-    # wavefronts of 8) of one head, and the backward keeps output-gradient
-    # rows, wider chunk records and a row-merge table in LDS
-    assert (b["workgroups"], b["lanes_per_head"], b["lane_bytes"], b["threads"]) == \
-        (f["workgroups"], f["lanes_per_head"], f["lane_bytes"], f["threads"])
-    assert b["workgroups"] == (200 * 200 // 32) * 8
-    assert b["lds_bytes"] > f["lds_bytes"]
+    # same lanes; a backward tile holds 64 queries (8 wavefronts of 8) of one
+    # head, twice the forward's workgroup, and the backward keeps
+    # output-gradient rows, wider chunk records and a row-merge table in LDS
+    # (within 80 KiB)
+    assert (b["lanes_per_head"], b["lane_bytes"]) == (f["lanes_per_head"], f["lane_bytes"])
+    assert (b["threads"], f["threads"]) == (512, 256)
+    assert b["workgroups"] == (200 * 200 // 64) * 8
+    assert f["lds_bytes"] < b["lds_bytes"] <= 80 * 1024
     # the backward keeps no per-point state in LDS: its size does not grow
     # with L * P, while the forward's attention weights do
     d2 = dict(d, shape=(1, 6, 30825, 32), heads=4, P=128)
     b2 = fb.sca_launch_info(**d2, backward=True)
     assert b2["lds_bytes"] == fb.sca_launch_info(**dict(d2, P=8), backward=True)["lds_bytes"]
-    assert b2["threads"] == 256 and b2["lds_bytes"] <= 64 * 1024
+    assert b2["threads"] == 512 and b2["lds_bytes"] <= 80 * 1024
     # the backward takes 8 lanes per head where it can: D = 8 float32 in
-    # 4-byte lanes, 8 queries per wavefront, 32 per tile: Q / 32 tiles per head
+    # 4-byte lanes, 8 queries per wavefront, 64 per tile: Q / 64 tiles per head
     assert (b2["lanes_per_head"], b2["lane_bytes"]) == (8, 4)
-    assert b2["workgroups"] == 200 * 200 // 32 * 4
+    assert b2["workgroups"] == 200 * 200 // 64 * 4
     # bfloat16 BEVFormer-base: 8-byte lanes in the backward, 16-byte ones in
     # the forward
     bb = fb.sca_launch_info(**dict(d, dtype="bf16"), backward=True)
@@ -243,7 +244,7 @@ def test_backward_launch_geometry():
     # weights leave room for one wavefront within the 64 KiB budget
     f2 = fb.sca_launch_info(**d2)
     assert f2["threads"] == 64 and 32 * 1024 < f2["lds_bytes"] <= 64 * 1024
-    # one head: still four wavefronts, of 4 queries each (D = 32 float32,
-    # 8-byte lanes), one head per tile
+    # one head: still eight wavefronts, of 64 / lanes_per_head queries each,
+    # one head per tile
     b3 = fb.sca_launch_info(**dict(d, shape=(1, 6, 30825, 32), heads=1), backward=True)
-    assert b3["threads"] == 256 and b3["workgroups"] == -(-200 * 200 // (4 * 64 // b3["lanes_per_head"]))
+    assert b3["threads"] == 512 and b3["workgroups"] == -(-200 * 200 // (8 * 64 // b3["lanes_per_head"]))
