@@ -1,0 +1,47 @@
+/*
+ * flashbev_phases.h -- phase clock of the fused Sampling-VT forward
+ * (measurement tool, MI355X / gfx950).
+ *
+ * libflashbev_phases.so is the operator library of include/flashbev.h and
+ * include/flashsca.h built once more with the forward's phase clock compiled
+ * in; it is not the operator's library (libflashbev.so has no clock).  In
+ * it, lane 0 of every wavefront of the forward kernel records the 100 MHz
+ * real-time counter (s_memrealtime) at its start, after it has staged the
+ * camera matrices and heights (and the workgroup barrier), after the
+ * workgroup barrier that precedes the output stores, and at its end, and
+ * the counter ticks it spent in each phase of the Sec. 3.3 / Alg. 2 path:
+ * projection and masking (with the culling test and, where the packed pass
+ * does both at once, the bilinear set-up), set-up, padding of the sample
+ * lists, the gather, and the stash of the group's results in the output
+ * tile.  The operator's results are unchanged; the clock costs a few
+ * instructions and registers per wavefront.
+ *
+ * Slots of a wavefront's 16 (unsigned 64-bit): 0 start, 1 staged, 2
+ * projection, 3 set-up, 4 padding, 5 gather, 6 stash (2..6 are tick sums),
+ * 7 barrier, 8 end, 9 rounds (groups of cells), 10 projection passes,
+ * 11..15 zero.
+ */
+#ifndef FLASHBEV_PHASES_H
+#define FLASHBEV_PHASES_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Where the forward writes the clocks: device memory of at least
+ * workgroups * (threads_per_workgroup / 64) * 16 unsigned 64-bit words
+ * (flashbev_launch_info gives both figures), written at
+ * [(workgroup * waves + wave) * 16 + slot]; NULL stops the recording.  The
+ * pointer is kept in a device variable of the current device and applies
+ * to every later forward launch there; the caller keeps the memory until
+ * it passes NULL.  Returns 0, or -1 if the copy to the device variable
+ * fails.
+ */
+int flashbev_phase_log(void *log);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHBEV_PHASES_H */

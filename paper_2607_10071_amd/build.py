@@ -6,13 +6,17 @@ Produces ``paper_2607_10071_amd/libflashbev.so`` (the fused Sampling-VT
 forward and backward behind the C ABI of ``include/flashbev.h``, and FlashSCA
 behind ``include/flashsca.h``) and
 ``libflashbev_membench.so`` (the memory-ceiling micro-benchmarks of
-``include/flashbev_membench.h`` that bench.py uses).
+``include/flashbev_membench.h`` that bench.py uses) and
+``libflashbev_phases.so`` (the same operator library with the forward's
+phase clock compiled in, ``include/flashbev_phases.h``, for
+``python -m paper_2607_10071_amd.phases``).  The three compile in parallel.
 """
 from __future__ import annotations
 
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -23,6 +27,8 @@ LIB = os.path.join(HERE, "libflashbev.so")
 # memory-ceiling micro-benchmarks used by bench.py (not part of the operator)
 MEMBENCH_SRC = os.path.join(HERE, "csrc", "membench.hip")
 MEMBENCH_LIB = os.path.join(HERE, "libflashbev_membench.so")
+# the operator library with the forward's phase clock (measurement tool)
+PHASES_LIB = os.path.join(HERE, "libflashbev_phases.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -45,9 +51,9 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def _compile(srcs, lib: str, verbose: bool) -> str:
+def _compile(srcs, lib: str, verbose: bool, extra=()) -> str:
     tmp = lib + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{INCLUDE}", *srcs, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, f"-I{INCLUDE}", *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -81,8 +87,14 @@ def _build_c_abi_program(verbose: bool) -> str:
 def build(verbose: bool = False) -> str:
     """Compile the operator library, the micro-benchmark library and the
     C-ABI test program."""
-    _compile([MEMBENCH_SRC], MEMBENCH_LIB, verbose)
-    lib = _compile([SRC, SCA_SRC], LIB, verbose)
+    with ThreadPoolExecutor(max_workers=3) as ex:
+        jobs = [ex.submit(_compile, [MEMBENCH_SRC], MEMBENCH_LIB, verbose),
+                ex.submit(_compile, [SRC, SCA_SRC], LIB, verbose),
+                ex.submit(_compile, [SRC, SCA_SRC], PHASES_LIB, verbose,
+                          ("-DFLASHBEV_PHASE_CLOCK",))]
+        lib = jobs[1].result()
+        for j in jobs:
+            j.result()
     _build_c_abi_program(verbose)
     return lib
 

@@ -222,6 +222,51 @@ __host__ __device__ inline LdsLayout lds_layout(int N, int Z, int waves, int cpw
 // 72 VGPRs without spilling, which keeps all of its workgroups resident at
 // once (measured on MI355X: 23.7 -> 22.8 us); the other instantiations keep
 // the compiler's choice.
+// Phase clock of the forward, compiled in only with FLASHBEV_PHASE_CLOCK
+// (the instrumented library libflashbev_phases.so; the operator's library
+// has none of it).  Lane 0 of each wavefront keeps the real-time counter
+// (100 MHz) at its start, after staging, after the final barrier and at its
+// end, and the time it spent in each phase, and writes them to
+// phase_log[(workgroup * waves + wave) * kPhaseSlots + slot] at its end.
+#ifdef FLASHBEV_PHASE_CLOCK
+__device__ unsigned long long *phase_log;
+constexpr int kPhaseSlots = 16;
+enum PhaseSlot {
+    kPhStart = 0, kPhStaged = 1, kPhProject = 2, kPhSetup = 3, kPhPad = 4, kPhGather = 5,
+    kPhStash = 6, kPhBarrier = 7, kPhEnd = 8, kPhRounds = 9, kPhPasses = 10
+};
+#define PH_DECL                                                              \
+    unsigned long long ph_t = __builtin_amdgcn_s_memrealtime();              \
+    unsigned long long ph_s[kPhaseSlots] = {};                               \
+    ph_s[kPhStart] = ph_t
+#define PH_AT(slot)                                                          \
+    do {                                                                     \
+        ph_t = __builtin_amdgcn_s_memrealtime();                             \
+        ph_s[slot] = ph_t;                                                   \
+    } while (0)
+#define PH_ADD(slot)                                                         \
+    do {                                                                     \
+        const unsigned long long ph_n = __builtin_amdgcn_s_memrealtime();    \
+        ph_s[slot] += ph_n - ph_t;                                           \
+        ph_t = ph_n;                                                         \
+    } while (0)
+#define PH_COUNT(slot) (ph_s[slot] += 1)
+#define PH_WRITE(lane)                                                       \
+    do {                                                                     \
+        if (phase_log && (lane) == 0) {                                      \
+            unsigned long long *ph_o = phase_log +                           \
+                ((size_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) * kPhaseSlots; \
+            for (int k = 0; k < kPhaseSlots; ++k) ph_o[k] = ph_s[k];         \
+        }                                                                    \
+    } while (0)
+#else
+#define PH_DECL
+#define PH_AT(slot) ((void)0)
+#define PH_ADD(slot) ((void)0)
+#define PH_COUNT(slot) ((void)0)
+#define PH_WRITE(lane) ((void)0)
+#endif
+
 template <int DT, int LW, int VPL, bool CULL>
 struct FwdWaves {
     static constexpr int value = (!CULL && DT == FLASHBEV_F32 && LW == 16 && VPL == 1) ? 7 : 1;
@@ -251,6 +296,7 @@ sample_vt_fwd(const Params p)
     uint32_t *s_off = reinterpret_cast<uint32_t *>(smem + p.lds_off);
     float *s_tile = reinterpret_cast<float *>(smem + p.lds_otile);
 
+    PH_DECL;
     const int cpw = p.cpw;
     const int RS = p.rec_stride;
     const int tid = threadIdx.x;
@@ -308,6 +354,7 @@ sample_vt_fwd(const Params p)
         for (int t = tid + nthreads; t < p.Z; t += nthreads) s_z[t] = p.z[t];
     }
     __syncthreads();
+    PH_AT(kPhStaged);
 
     // culling role: cell zl of a group, camera n_p
     const int Nd = N > 0 ? N : 1;
@@ -408,6 +455,7 @@ sample_vt_fwd(const Params p)
     };
 
     for (int r = 0; r < p.rounds; ++r) {
+        PH_COUNT(kPhRounds);
         const int q_grp = q_wave + r * cpw;
         // cells of this group inside the grid (<= 0 past the end of the last tile)
         const int ncell = (p.XY - q_grp) < cpw ? (p.XY - q_grp) : cpw;
@@ -440,6 +488,7 @@ sample_vt_fwd(const Params p)
                 for (int m = 0; m < ncell; ++m) cmask |= (vm >> (m * N)) & nmask;
             }
             const int Np = __popcll(cmask);
+            PH_ADD(kPhProject);
 
             if (Np > 0) {
                 // the visible cameras in ascending order
@@ -550,9 +599,13 @@ sample_vt_fwd(const Params p)
                             maxcnt = c > maxcnt ? c : maxcnt;
                         }
                     }
+                    PH_ADD(kPhProject);
+                    PH_COUNT(kPhPasses);
                     const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
                     pad(ncell, cnt_lane, maxpad);
+                    PH_ADD(kPhPad);
                     gather(acc, g_active, maxpad);
+                    PH_ADD(kPhGather);
                 }
             }
         } else {
@@ -603,6 +656,8 @@ sample_vt_fwd(const Params p)
                 }
                 const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
                 wave_lds_sync();
+                PH_ADD(kPhProject);
+                PH_COUNT(kPhPasses);
 
                 // ---- phase 1b: for all valid samples of the group at once,
                 // bilinear set-up: feature coordinates, tap weights with
@@ -657,8 +712,11 @@ sample_vt_fwd(const Params p)
                         ol[slotk] = coff + rofs;
                     }
                 }
+                PH_ADD(kPhSetup);
                 pad(ncell, cnt_lane, maxpad);
+                PH_ADD(kPhPad);
                 gather(acc, g_active, maxpad);
+                PH_ADD(kPhGather);
             }
         }
 
@@ -675,8 +733,10 @@ sample_vt_fwd(const Params p)
                 }
             }
         }
+        PH_ADD(kPhStash);
     }
     __syncthreads();
+    PH_AT(kPhBarrier);
 
     // ---- single write of out[b, c, tile cells] (Alg. 2: write once):
     // consecutive threads write consecutive cells of one channel plane
@@ -693,6 +753,8 @@ sample_vt_fwd(const Params p)
     if (c0 < rows) {
         for (int c = c0; c < p.C; c += rows) ob[(size_t)c * p.XY + k] = s_tile[c * p.otile_ld + k];
     }
+    PH_AT(kPhEnd);
+    PH_WRITE(lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -2699,3 +2761,13 @@ extern "C" int flashbev_sample_vt_backward_ws(const flashbev_features *features,
     if (rc) return rc;
     return launch_bwd_gather(pl, reinterpret_cast<hipStream_t>(stream));
 }
+
+#ifdef FLASHBEV_PHASE_CLOCK
+// Instrumented builds only: where the forward's wavefronts write their phase
+// clocks (NULL: nowhere).  Returns 0, or -1 if the copy to the device
+// variable fails.
+extern "C" int flashbev_phase_log(void *log)
+{
+    return hipMemcpyToSymbol(HIP_SYMBOL(phase_log), &log, sizeof(log)) == hipSuccess ? 0 : -1;
+}
+#endif
