@@ -88,8 +88,8 @@ constexpr int kSlotPad = 4;
 // slot, tap) rows per wavefront.  Per wavefront's 256 rows: an open-addressing
 // table of keys (tap offsets) with the head of each key's member list, and per
 // row its factor (mean * a * w) and a link word (offset of its slot's
-// output-gradient row << 16 | next member); the keys in use (halfwords) and
-// their number.
+// output-gradient row << 16 | next member) side by side, read as one 8-byte
+// word; the keys in use (halfwords) and their number.
 constexpr int kMrgRows = 4 * kScaWave;
 constexpr int kMrgWaveBytes = kMrgRows * 18;
 constexpr uint32_t kMrgEmpty = 0xFFFFFFFFu;   // no key (tap offsets are below 2^31)
@@ -621,9 +621,8 @@ sca_bwd(const ScaParams p)
     const int trows = (nthreads / kScaWave) * kMrgRows;
     uint32_t *tkey = m.mrg;
     uint32_t *thead = tkey + trows;
-    float *rcoef = reinterpret_cast<float *>(thead + trows);
-    uint32_t *rlink = reinterpret_cast<uint32_t *>(rcoef + trows);
-    uint16_t *tuniq = reinterpret_cast<uint16_t *>(rlink + trows);
+    uint2 *rrow = reinterpret_cast<uint2 *>(thead + trows);   // (factor bits, link) per row
+    uint16_t *tuniq = reinterpret_cast<uint16_t *>(rrow + trows);
     uint32_t *tcount = reinterpret_cast<uint32_t *>(tuniq + trows);
     for (int h = tid; h < trows; h += nthreads) {
         tkey[h] = kMrgEmpty;
@@ -739,9 +738,10 @@ sca_bwd(const ScaParams p)
                         const float fy = __builtin_bit_cast(float, rr[5]);
                         const float wr = (r & 2) ? fy : 1.0f - fy;
                         const float wc = (r & 1) ? fx : 1.0f - fx;
-                        rcoef[R] = __builtin_bit_cast(float, rr[6]) * (wr * wc);
-                        rlink[R] = ((uint32_t)(sl * D) << 16) |
-                                   (atomicExch(&thead[h], R) & kMrgEnd16);
+                        const float cf = __builtin_bit_cast(float, rr[6]) * (wr * wc);
+                        rrow[R] = make_uint2(__builtin_bit_cast(uint32_t, cf),
+                                             ((uint32_t)(sl * D) << 16) |
+                                                 (atomicExch(&thead[h], R) & kMrgEnd16));
                     } else {
                         // unreachable (the table holds every row of a chunk);
                         // the row is then scattered alone
@@ -764,22 +764,20 @@ sca_bwd(const ScaParams p)
                     uint32_t R = thead[h];
                     float val = 0.0f;
                     if (R < (uint32_t)trows) {
-                        // the next member's link and factor are read while
-                        // this member's output-gradient element is
-                        uint32_t lk = rlink[R];
-                        float c = rcoef[R];
+                        // the next member's factor and link (one 8-byte read)
+                        // are read while this member's output-gradient
+                        // element is
+                        uint2 e = rrow[R];
                         for (int k = 0; k < trows; ++k) {
+                            const uint32_t lk = e.y;
                             const float g = m.gst[(lk >> 16) + ch];
                             const uint32_t nx = lk & kMrgEnd16;
                             const bool more = nx < (uint32_t)trows;
-                            const uint32_t Rn = more ? nx : R;
-                            const uint32_t lkn = rlink[Rn];
-                            const float cn = rcoef[Rn];
-                            val = fmaf(c, g, val);
+                            const uint2 en = rrow[more ? nx : R];
+                            val = fmaf(__builtin_bit_cast(float, e.x), g, val);
                             if (!more) break;
-                            R = Rn;
-                            lk = lkn;
-                            c = cn;
+                            R = nx;
+                            e = en;
                         }
                     }
                     if (key < p.cam_bytes) unsafeAtomicAdd(gv + key / ES + ch, val);
