@@ -681,16 +681,18 @@ sca_bwd(const ScaParams p)
                     d2 = fmaf(elem<DT, LW>(v2, e), gs[e], d2);
                     d3 = fmaf(elem<DT, LW>(v3, e), gs[e], d3);
                 }
-                for (int x = lph >> 1; x >= 1; x >>= 1) {
-                    d0 += __shfl_xor(d0, x);
-                    d1 += __shfl_xor(d1, x);
-                    d2 += __shfl_xor(d2, x);
-                    d3 += __shfl_xor(d3, x);
-                }
+                // the point's gradients are linear in the four dot products
+                // with weights shared by the slot's lanes: each lane forms
+                // its share, and three sums cross the slot in place of four
                 const float tax = tf.x, tay = tf.y;
-                const float da = ((tw.x * d0 + tw.y * d1) + tw.z * d2) + tw.w * d3;
-                const float dx = (1.0f - tay) * (d1 - d0) + tay * (d3 - d2);
-                const float dy = (1.0f - tax) * (d2 - d0) + tax * (d3 - d1);
+                float da = ((tw.x * d0 + tw.y * d1) + tw.z * d2) + tw.w * d3;
+                float dx = (1.0f - tay) * (d1 - d0) + tay * (d3 - d2);
+                float dy = (1.0f - tax) * (d2 - d0) + tax * (d3 - d1);
+                for (int x = lph >> 1; x >= 1; x >>= 1) {
+                    da += __shfl_xor(da, x);
+                    dx += __shfl_xor(dx, x);
+                    dy += __shfl_xor(dy, x);
+                }
                 const bool owner = s.sub == t;
                 my_da += owner ? da : 0.0f;
                 my_dx += owner ? dx : 0.0f;
