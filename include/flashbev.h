@@ -186,7 +186,8 @@ int flashbev_sample_vt_backward(const flashbev_features *features, const float *
  *      (b, i, j, z) (the number of cameras whose mask M_n holds, Eq. 1) is
  *      tabulated, both in `workspace`;
  *   2. each wavefront takes a few consecutive pixels of one feature-map row
- *      of camera n, finds the (cell, height) samples whose bilinear taps
+ *      of camera n (of two rows where the rows are wide: at most two pixels
+ *      per row), finds the (cell, height) samples whose bilinear taps
  *      reach them (a conservative float64 region per height, then the
  *      forward's exact float32 projection, mask and floor for each
  *      candidate), and sums w_t / max(1, den_z) times their Gt rows in a

@@ -1362,16 +1362,19 @@ sample_vt_bwd(const BwdParams p)
 //   * sample_vt_bwd_prep: the output gradient transposed to cell-major rows
 //     Gt[b, cell, C] (so a term's row is one contiguous read), and den_z of
 //     every (b, cell, z) (the valid cameras of the point, Eq. 1's divisor).
-//   * sample_vt_bwd_gather: a wavefront per group of cpw consecutive pixels
-//     of one feature-map row.  For each height the cells that can reach the
-//     group's support lie in a convex region of that height's plane,
+//   * sample_vt_bwd_gather: a wavefront per group of cpw consecutive columns
+//     of two feature-map rows (a sample's taps span two rows, so most of its
+//     terms in the group share one load of its gradient row).  For each
+//     height the cells that can reach the group's support lie in a convex
+//     region of that height's plane,
 //     bounded by five half-planes (depth above depth_eps; u and v inside
 //     the group's support and the image) with slack for float32 rounding.
 //     The region's rows give contiguous runs of candidate cells; each
 //     candidate is re-checked with the forward's exact float32 recipe
 //     (projection, mask, floor), so mask and tap decisions are the
-//     forward's.  The terms go to per-pixel LDS lists, and the lanes of a
-//     pixel sum their rows of Gt in registers, as the forward gathers
+//     forward's.  The terms go to per-column LDS lists (a row of Gt with its
+//     weights for the group's two pixels of that column), and the lanes of a
+//     column sum them into both pixels' registers, as the forward gathers
 //     feature rows.  Each gradient row is written once; the summation order
 //     is fixed, so results are bitwise identical run to run.
 struct BwdGatherParams {
@@ -1398,8 +1401,9 @@ struct BwdGatherParams {
     int32_t lpc;             // lanes per pixel
     int32_t nvec;            // LW-byte vectors per gradient row
     float rcp_lpc;
-    int32_t groups_per_row;  // pixel groups per feature-map row
-    int64_t groups;          // all pixel groups (B N H groups_per_row)
+    int32_t groups_per_row;  // pixel groups per group of rows
+    int32_t row_groups;      // groups of rows per map: H / rows, rounded up
+    int64_t groups;          // all pixel groups (B N row_groups groups_per_row)
     int32_t rec_stride;      // records per pixel list
     uint32_t row_bytes;      // C * 4
     uint32_t lds_wave;       // LDS bytes per wavefront
@@ -1491,23 +1495,51 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_prep(const BwdGatherParams 
     }
 }
 
-template <int LW, int VPL>
-__global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParams p)
+// List entry weights: one float per entry for one-row groups, the two rows'
+// weights for two-row groups.
+template <int ROWS> struct GatherW { using type = float; };
+template <> struct GatherW<2> { using type = float2; };
+__device__ __forceinline__ float gw_row0(float w) { return w; }
+__device__ __forceinline__ float gw_row0(float2 w) { return w.x; }
+__device__ __forceinline__ float gw_row1(float) { return 0.0f; }
+__device__ __forceinline__ float gw_row1(float2 w) { return w.y; }
+
+// ROWS: feature-map rows per group (two where a group has at most two
+// columns: its per-group set-up and regions then serve twice the pixels, and
+// one load of a sample's gradient row serves both rows' terms; one where it
+// has more, whose lists would carry many single-row terms).
+// Wavefronts per SIMD the compiler must leave room for: four (128 VGPRs),
+// which the second row's accumulators would otherwise push to three
+// (measured: paper_ref 67 -> 64 us, half_batch 160 -> 150 us); the
+// compiler's choice where that would spill (two-row groups of 16-byte lanes
+// with several vectors per lane).
+template <int LW, int VPL, int ROWS>
+struct GatherWaves {
+    static constexpr int value = (ROWS == 2 && LW == 16 && VPL >= 2) ? 1 : 4;
+};
+
+template <int LW, int VPL, int ROWS>
+__global__ void __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(GatherWaves<LW, VPL, ROWS>::value, 8)))
+sample_vt_bwd_gather(const BwdGatherParams p)
 {
     constexpr int EPV = LW / 4;   // float32 gradient elements per vector
+    using WT = typename GatherW<ROWS>::type;
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int RS = p.rec_stride;
     const int cpw = p.cpw;
     unsigned char *wbase = smem + (size_t)wave * p.lds_wave;
-    float *wl = reinterpret_cast<float *>(wbase);                         // [cpw][RS] weights
-    uint32_t *ol = reinterpret_cast<uint32_t *>(wbase + (size_t)cpw * RS * 4);  // [cpw][RS] Gt offsets
-    // after the lists: per candidate row (64) its cell prefix, first cell,
-    // height slot and grid row; the height-free plane terms (5 x 8); the
-    // pair slopes (36 x 2); per height of a batch its plane offsets (x 5),
-    // row prefix, first row, no-region flag and value
-    int *rpre = reinterpret_cast<int *>(wbase + (size_t)cpw * RS * 8);
+    // per column list: the weights for the group's rows, and the Gt row
+    WT *wl = reinterpret_cast<WT *>(wbase);                                          // [cpw][RS]
+    uint32_t *ol = reinterpret_cast<uint32_t *>(wbase + (size_t)cpw * RS * sizeof(WT));  // [cpw][RS]
+    // after the lists (16-byte aligned): per candidate row (64) its cell
+    // prefix, first cell, height slot and grid row; the height-free plane
+    // terms (5 x 8); the pair slopes (36 x 2); per height of a batch its
+    // plane offsets (x 5), row prefix, first row, no-region flag and value
+    const uint32_t tail = ((uint32_t)cpw * (uint32_t)RS * (uint32_t)(sizeof(WT) + 4) + 15u) & ~15u;
+    int *rpre = reinterpret_cast<int *>(wbase + tail);
     int *rjlo = rpre + kWave;
     int *rhs = rjlo + kWave;
     int *rci = rhs + kWave;
@@ -1531,8 +1563,9 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
     const int gpr = p.groups_per_row;
     const int64_t row = grp / gpr;
     const int px0 = (int)(grp - row * gpr) * cpw;
-    const int py = (int)(row % p.H);
-    const int64_t bn = row / p.H;
+    const int py = ROWS * (int)(row % p.row_groups);   // the group's rows: py .. py + nrows - 1
+    const int nrows = (ROWS == 1) ? 1 : ((p.H - py) < 2 ? (p.H - py) : 2);
+    const int64_t bn = row / p.row_groups;
     const int n = (int)(bn % p.N);
     const int b = (int)(bn / p.N);
     const int g = (p.W - px0) < cpw ? (p.W - px0) : cpw;
@@ -1546,11 +1579,14 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc(p.gt, (short)0, (int)p.gt_bytes, 0x00020000);
 
-    float acc[VPL][EPV];
+    float acc[VPL][EPV], acc1[VPL][EPV];   // rows py and py + 1
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) acc[v][e] = 0.0f;
+        for (int e = 0; e < EPV; ++e) {
+            acc[v][e] = 0.0f;
+            acc1[v][e] = 0.0f;
+        }
 
     // camera rows (uniform)
     const float *mg = p.l2i + ((size_t)b * p.N + n) * 16;
@@ -1559,15 +1595,16 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
     for (int k = 0; k < 12; ++k) mr[k] = mg[k];
 
     // the group's support in image coordinates: samples whose first tap is
-    // in column [px0 - 1, px0 + g - 1] and row py - 1 or py, inside the image
+    // in column [px0 - 1, px0 + g - 1] and row [py - 1, py + nrows - 1],
+    // inside the image
     const double U0 = fmax(0.0, ((double)px0 - 0.5) * p.isx_d);
     const double U1 = fmin((double)p.img_w, ((double)(px0 + g) + 0.5) * p.isx_d);
     const double V0 = fmax(0.0, ((double)py - 0.5) * p.isy_d);
-    const double V1 = fmin((double)p.img_h, ((double)py + 1.5) * p.isy_d);
+    const double V1 = fmin((double)p.img_h, ((double)(py + nrows) + 0.5) * p.isy_d);
     const uint32_t cam_gt = (uint32_t)b * (uint32_t)p.XY * p.row_bytes;
     const uint8_t *denb = p.den + (size_t)b * p.XY * p.Z;
 
-    int cnt_lane = 0;   // lane m holds pixel m's record count
+    int cnt_lane = 0;   // lane m holds column m's record count
     int maxcnt = 0;
 
     auto flush = [&]() {
@@ -1575,17 +1612,17 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
         for (int m = 0; m < g; ++m) {
             const int c = __builtin_amdgcn_readlane(cnt_lane, m);
             for (int k = c + lane; k < maxpad; k += kWave) {
-                wl[m * RS + k] = 0.0f;
+                wl[m * RS + k] = WT{};
                 ol[m * RS + k] = kNoTap;
             }
         }
         wave_lds_sync();
         if (g_active) {
-            const float *wv = wl + m_lds * RS;
+            const WT *wv = wl + m_lds * RS;
             const uint32_t *ov = ol + m_lds * RS;
             for (int k = 0; k < maxpad; k += kGatherUnroll) {
                 uint32_t base[kGatherUnroll];
-                float w[kGatherUnroll];
+                WT w[kGatherUnroll];
 #pragma unroll
                 for (int u = 0; u < kGatherUnroll; ++u) base[u] = ov[k + u];
 #pragma unroll
@@ -1602,8 +1639,12 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
 #pragma unroll
                         for (int u = 0; u < kGatherUnroll; ++u)
 #pragma unroll
-                            for (int e = 0; e < EPV; ++e)
-                                acc[v][e] = fmaf(w[u], __builtin_bit_cast(float, t[u].w[e]), acc[v][e]);
+                            for (int e = 0; e < EPV; ++e) {
+                                const float gv = __builtin_bit_cast(float, t[u].w[e]);
+                                acc[v][e] = fmaf(gw_row0(w[u]), gv, acc[v][e]);
+                                if constexpr (ROWS == 2)
+                                    acc1[v][e] = fmaf(gw_row1(w[u]), gv, acc1[v][e]);
+                            }
                     }
                 }
             }
@@ -1830,7 +1871,7 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
                     const int den = c_ok ? (int)denb[(size_t)q * p.Z + k] : 0;
                     // exact test: the forward's recipe for camera n
                     bool t0 = false, t1 = false;
-                    float w0 = 0.0f, w1 = 0.0f;
+                    WT w0{}, w1{};
                     int x0 = 0;
                     uint32_t goff = 0;
                     if (c_ok) {
@@ -1850,21 +1891,30 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
                             const float ax = xf - x0f, ay = yf - y0f;
                             x0 = (int)x0f;
                             const int y0 = (int)y0f;
-                            // the group's row py is this sample's row y0 + 1
-                            // (weight ay) or y0 (weight 1 - ay)
-                            const bool yrow = (y0 == py - 1) || (y0 == py);
+                            // the sample's rows y0 (weight 1 - ay) and y0 + 1
+                            // (weight ay) meet the group's rows py and py + 1
+                            const bool yrow = (y0 >= py - 1) && (y0 <= py + nrows - 1);
                             if (yrow) {
                                 const float inv = (p.reduce == 0) ? __builtin_amdgcn_rcpf((float)den) : 1.0f;
-                                const float wy = ((y0 == py) ? 1.0f - ay : ay) * inv;
-                                w0 = (1.0f - ax) * wy;   // tap column x0
-                                w1 = ax * wy;            // tap column x0 + 1
+                                const float wy0 = ((y0 == py) ? 1.0f - ay : ((y0 == py - 1) ? ay : 0.0f)) * inv;
+                                // tap column x0 (1 - ax) and x0 + 1 (ax)
+                                if constexpr (ROWS == 2) {
+                                    const float wy1 = (nrows == 2)
+                                        ? ((y0 == py + 1) ? 1.0f - ay : ((y0 == py) ? ay : 0.0f)) * inv
+                                        : 0.0f;
+                                    w0 = make_float2((1.0f - ax) * wy0, (1.0f - ax) * wy1);
+                                    w1 = make_float2(ax * wy0, ax * wy1);
+                                } else {
+                                    w0 = (1.0f - ax) * wy0;
+                                    w1 = ax * wy0;
+                                }
                                 t0 = x0 >= px0 && x0 < px0 + g;
                                 t1 = x0 + 1 >= px0 && x0 + 1 < px0 + g;
                                 goff = cam_gt + (uint32_t)q * p.row_bytes;
                             }
                         }
                     }
-                    // append the terms to the pixels' lists (candidate order)
+                    // append the terms to the columns' lists (candidate order)
                     for (int m = 0; m < g; ++m) {
                         const bool mine = (t0 && x0 == px0 + m) || (t1 && x0 + 1 == px0 + m);
                         const uint64_t mask = __ballot(mine);
@@ -1893,12 +1943,17 @@ __global__ void __launch_bounds__(256) sample_vt_bwd_gather(const BwdGatherParam
     // single write of the group's gradient rows (NHWC, contiguous)
     if (g_active) {
         float *dst = p.gfeat + ((((size_t)b * p.N + n) * p.H + py) * p.W + px0 + m_g) * p.C;
+        float *dst1 = dst + (size_t)p.W * p.C;   // row py + 1
 #pragma unroll
         for (int v = 0; v < VPL; ++v) {
             const int vi = slot + L * v;
             if (VPL == 1 || vi < p.nvec) {
 #pragma unroll
                 for (int e = 0; e < EPV; ++e) dst[vi * EPV + e] = acc[v][e];
+                if (ROWS == 2 && nrows == 2) {
+#pragma unroll
+                    for (int e = 0; e < EPV; ++e) dst1[vi * EPV + e] = acc1[v][e];
+                }
             }
         }
     }
@@ -2430,6 +2485,7 @@ struct BwdGatherPlan {
     int64_t gather_wgs;    // gather workgroups (0: no pixels)
     size_t lds;            // gather dynamic LDS per workgroup
     int lw, vpl;
+    int rows;              // feature-map rows per gather group
     uint64_t ws_bytes;     // workspace bytes needed
 };
 
@@ -2437,23 +2493,29 @@ constexpr int kGatherWaves = 1;   // gather: wavefronts per workgroup (one: fine
 
 using BwdGatherFn = void (*)(const BwdGatherParams);
 
-template <int LW>
+template <int LW, int ROWS>
 BwdGatherFn pick_gather_vpl(int vpl)
 {
     switch (vpl) {
-    case 1: return sample_vt_bwd_gather<LW, 1>;
-    case 2: return sample_vt_bwd_gather<LW, 2>;
-    default: return sample_vt_bwd_gather<LW, 4>;
+    case 1: return sample_vt_bwd_gather<LW, 1, ROWS>;
+    case 2: return sample_vt_bwd_gather<LW, 2, ROWS>;
+    default: return sample_vt_bwd_gather<LW, 4, ROWS>;
     }
 }
 
-BwdGatherFn pick_gather(int lw, int vpl)
+template <int ROWS>
+BwdGatherFn pick_gather_lw(int lw, int vpl)
 {
     switch (lw) {
-    case 16: return pick_gather_vpl<16>(vpl);
-    case 8: return pick_gather_vpl<8>(vpl);
-    default: return pick_gather_vpl<4>(vpl);
+    case 16: return pick_gather_vpl<16, ROWS>(vpl);
+    case 8: return pick_gather_vpl<8, ROWS>(vpl);
+    default: return pick_gather_vpl<4, ROWS>(vpl);
     }
+}
+
+BwdGatherFn pick_gather(int lw, int vpl, int rows)
+{
+    return rows == 2 ? pick_gather_lw<2>(lw, vpl) : pick_gather_lw<1>(lw, vpl);
 }
 
 uint64_t align256(uint64_t v) { return (v + 255u) & ~(uint64_t)255u; }
@@ -2480,7 +2542,6 @@ int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
     memset(pl, 0, sizeof(*pl));
     pl->ws_bytes = need;
     const uint64_t gelems = bp.gfeat_elems;
-    const uint64_t pixels = size_prod({(uint64_t)f->B, (uint64_t)f->N, (uint64_t)f->H});
     if (need_data && check_ws && gelems > 0 && need > 0) {
         if (!ws) return FLASHBEV_ERR_NULLPTR;
         if ((uintptr_t)ws % 256u) return FLASHBEV_ERR_ALIGN;
@@ -2538,10 +2599,16 @@ int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
     p.nvec = nvec;
     p.rcp_lpc = 1.0f / (float)lpc;
     p.groups_per_row = (f->W + cpw - 1) / cpw;
-    p.groups = (int64_t)pixels * p.groups_per_row;
+    // two rows per group where a group has at most two columns (measured on
+    // MI355X: paper_ref 73 -> 64 us, half_batch 168 -> 150 us; with three or
+    // four columns two rows were slower: rep 67 -> 76 us, z_sweep 621 -> 719)
+    const int rows = cpw <= 2 ? 2 : 1;
+    p.row_groups = (f->H + rows - 1) / rows;
+    p.groups = (int64_t)f->B * f->N * p.row_groups * p.groups_per_row;
     p.rec_stride = kGatherRec | 1;
     p.row_bytes = (uint32_t)row;
-    p.lds_wave = align16((uint32_t)cpw * (uint32_t)p.rec_stride * 8u + kGatherTail);
+    p.lds_wave = align16(align16((uint32_t)cpw * (uint32_t)p.rec_stride * (rows == 2 ? 12u : 8u)) +
+                         kGatherTail);
     for (int k = 0; k < zb->Z; ++k) p.z[k] = zb->z[k];
 
     pl->prep_wgs = (gelems > 0) ? (int64_t)f->B * p.prep_tiles_per_b * p.prep_cblocks : 0;
@@ -2551,6 +2618,7 @@ int make_bwd_gather_plan(const flashbev_features *f, const float *l2i,
     if (pl->lds > kLdsBudget) return FLASHBEV_ERR_UNSUPPORTED;
     pl->lw = lw;
     pl->vpl = vpl;
+    pl->rows = rows;
     return FLASHBEV_OK;
 }
 
@@ -2562,7 +2630,7 @@ int launch_bwd_gather(const BwdGatherPlan &pl, hipStream_t st)
                         dim3((unsigned)pl.prep_wgs), dim3(256), args, 0, st) != hipSuccess)
         return FLASHBEV_ERR_HIP;
     if (pl.gather_wgs > 0 &&
-        hipLaunchKernel(reinterpret_cast<const void *>(pick_gather(pl.lw, pl.vpl)),
+        hipLaunchKernel(reinterpret_cast<const void *>(pick_gather(pl.lw, pl.vpl, pl.rows)),
                         dim3((unsigned)pl.gather_wgs), dim3(kGatherWaves * kWave), args, pl.lds,
                         st) != hipSuccess)
         return FLASHBEV_ERR_HIP;

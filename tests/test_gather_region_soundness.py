@@ -1,8 +1,9 @@
 """Soundness of the gather-form backward's candidate regions (CPU).
 
 The gather form of the backward (flashbev_sample_vt_backward_ws) takes the
-feature-map pixels a few at a time (a group: g consecutive pixels of row py)
-and, for each height, enumerates only the BEV cells inside a region of that
+feature-map pixels a few at a time (a group: g consecutive columns of one
+row py, or of rows py and py + 1 (py even) where g is at most 2) and, for
+each height, enumerates only the BEV cells inside a region of that
 height's plane: five half-planes in float64 (depth above depth_eps; u and v
 inside the group's tap support and the image), each loosened by 2^-18 of
 the magnitudes of its terms, cut into row intervals over a range of rows
@@ -28,10 +29,10 @@ F = np.float32
 E = 2.0 ** -18
 
 
-def region_has(m12, zk, i, j, py, px0, g, grid, img_hw, feat_hw, eps):
-    """Whether cell (i, j) is a candidate of the group (py, px0 .. px0+g-1)
-    at height zk for a camera with rows m12 [..., 12] (float32); every
-    argument broadcasts."""
+def region_has(m12, zk, i, j, py, nrows, px0, g, grid, img_hw, feat_hw, eps):
+    """Whether cell (i, j) is a candidate of the group (rows py .. py+nrows-1,
+    columns px0 .. px0+g-1) at height zk for a camera with rows m12 [..., 12]
+    (float32); every argument broadcasts."""
     x_min, dx, X, y_min, dy, Y = grid
     img_h, img_w = img_hw
     H, W = feat_hw
@@ -47,7 +48,7 @@ def region_has(m12, zk, i, j, py, px0, g, grid, img_hw, feat_hw, eps):
         U0 = np.maximum(0.0, (px0 - 0.5) * isx)
         U1 = np.minimum(float(img_w), ((px0 + g) + 0.5) * isx)
         V0 = np.maximum(0.0, (py - 0.5) * isy)
-        V1 = np.minimum(float(img_h), (py + 1.5) * isy)
+        V1 = np.minimum(float(img_h), ((py + nrows) + 0.5) * isy)
         support = (U0 < U1) & (V0 < V1)
         zd = np.asarray(zk, F).astype(np.float64)
         Mu0 = (np.abs(m[0]) * xmax + np.abs(m[1]) * ymax) + np.abs(m[3])
@@ -162,7 +163,10 @@ def check(l2i, z, grid, img_hw, feat_hw, cpws=(1, 3, 8), eps=1e-5):
                     continue
                 px0 = (px[sel] // cpw) * cpw
                 g = np.minimum(W - px0, cpw)
-                has = region_has(m12[sel], zk[sel], i[sel], j[sel], py[sel], px0, g, grid,
+                R = 2 if cpw <= 2 else 1          # rows per group
+                gy = (py[sel] // R) * R           # the group's first row
+                nrows = np.minimum(H - gy, R)
+                has = region_has(m12[sel], zk[sel], i[sel], j[sel], gy, nrows, px0, g, grid,
                                  img_hw, feat_hw, eps)
                 assert has.all(), (cpw, np.argwhere(~has)[:5].ravel(), b[sel][~has][:5],
                                    i[sel][~has][:5], j[sel][~has][:5], k[sel][~has][:5],
