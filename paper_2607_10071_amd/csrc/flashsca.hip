@@ -69,6 +69,7 @@ constexpr int kScaBwdThreads = kScaWave * kScaBwdWavesMax;
 constexpr uint32_t kScaBwdLdsBudget = 80u * 1024u;
 constexpr int kScaXcds = 8;      // MI355X: workgroups are dispatched to 8 XCDs round-robin
 constexpr int kScaBlock = 16;    // queries are visited in blocks of 16 x 16 BEV cells
+constexpr int kScaHeadChunks = 8;   // head-to-XCD order: chunks of the query groups
 // Offset of a tap that is not loaded: one camera's value is smaller than
 // 2 GiB and a lane adds less than 1 KiB, so the load is past the buffer's end
 // and returns zero without touching memory.
@@ -115,8 +116,8 @@ struct ScaParams {
     int32_t lph;             // lanes per slot (power of two)
     int32_t lph_shift;       // log2(lph)
     int32_t spw;             // slots per wavefront
-    int32_t tile_pairs;      // slots per workgroup: forward (query, head) pairs,
-                             // backward queries (of one head)
+    int32_t tile_pairs;      // slots per workgroup: queries of one head
+    int32_t head_xcd;        // head-to-XCD order: its chunks of the query groups (0: bands)
     int32_t mrg_shift;       // backward: 32 - log2(rows of the merge table)
     int32_t tiles_per_b;
     int32_t stripe;          // consecutive tiles an XCD takes in turn (about one block)
@@ -224,20 +225,52 @@ __device__ __forceinline__ ScaSmem sca_smem(const ScaParams &p, unsigned char *s
     return m;
 }
 
-// XCD-aware tile order.  Queries are visited block by block (query_of), so
-// consecutive tiles cover a compact patch of the BEV whose samples land on
-// overlapping pixels (measured on MI355X at BEVFormer-base, P = 32: 16 x 16
-// blocks 0.927 ms, 32 x 32 0.953 ms, 64 x 64 slower still).  The k-th
-// workgroup on XCD x takes tile (k / S) * 8S + x * S + k % S with S =
-// p.stripe, one eighth of the tiles: each XCD works through one contiguous
-// band of blocks, whose samples come from few cameras and share pixels in
-// its L2 (against stripes of one block interleaved over the grid: P = 8
-// 0.282 -> 0.268 ms, P = 32 0.927 -> 0.900 ms, bfloat16 0.487 -> 0.467 ms,
-// backward 4.37 -> 4.31 ms).  The few tiles past 8 S are split the same way
-// with shorter stripes.
-__device__ __forceinline__ int sca_tile(const ScaParams &p)
+// XCD-aware tile order.  A tile holds waves * spw consecutive queries (ranks
+// of query_of) of one head.  Queries are visited block by block (query_of),
+// so consecutive tiles cover a compact patch of the BEV whose samples land
+// on overlapping pixels (measured on MI355X at BEVFormer-base, P = 32:
+// 16 x 16 blocks 0.927 ms, 32 x 32 0.953 ms, 64 x 64 slower still).
+// Workgroups go to the 8 XCDs round-robin, and the k-th workgroup on XCD x
+// takes:
+//  * with heads a multiple of 8 (p.head_xcd = K chunks): batch element b,
+//    head group hh and query group qg, k running over (b, hh, qg) with qg
+//    fastest, and head 8 hh + (x + c) mod 8 on the c-th of K equal chunks of
+//    the query groups.  At any time each XCD then reads a single head's
+//    slice of the value rows (whole 128-byte lines for float32 D = 32), so
+//    its L2 holds the rows of 8 times as many queries as when every XCD
+//    reads every head, and over the K chunks every XCD takes every head once,
+//    which evens out heads whose points fall outside the maps more often
+//    (measured on MI355X at BEVFormer-base, forward, against the band order
+//    below: P = 8 0.258 -> 0.254 ms, P = 32 0.784 -> 0.765 ms with fabric
+//    fetches 2.10 -> 1.14 GB; one head per XCD throughout (K = 1) fetched
+//    1.09 GB but took 0.784 ms, its XCDs unequally loaded by up to 17%);
+//  * otherwise tile (k / S) * 8S + x * S + k % S with S = p.stripe, one
+//    eighth of the tiles (query groups major, heads minor): each XCD works
+//    through one contiguous band of blocks, whose samples come from few
+//    cameras and share pixels in its L2 (against stripes of one block
+//    interleaved over the grid: P = 8 0.282 -> 0.268 ms, P = 32 0.927 ->
+//    0.900 ms, bfloat16 0.487 -> 0.467 ms, backward 4.37 -> 4.31 ms).  The
+//    few tiles past 8 S are split the same way with shorter stripes.
+struct ScaTile {
+    int b, head, qg;
+};
+
+__device__ __forceinline__ ScaTile sca_tile(const ScaParams &p)
 {
     const int g = blockIdx.x;
+    const int nqg = p.tiles_per_b / p.heads;   // query groups per batch element
+    ScaTile t;
+    if (p.head_xcd) {
+        const int x = g % kScaXcds, k = g / kScaXcds;
+        const int per_b = (p.heads / kScaXcds) * nqg;
+        t.b = k / per_b;
+        const int r = k - t.b * per_b;
+        const int hh = r / nqg;
+        t.qg = r - hh * nqg;
+        const int c = (int)(((int64_t)t.qg * p.head_xcd) / nqg);
+        t.head = hh * kScaXcds + ((x + c) & (kScaXcds - 1));
+        return t;
+    }
     const int S8 = kScaXcds * p.stripe;
     const int full = (int)(gridDim.x / S8) * S8;
     int tile = g;
@@ -252,7 +285,11 @@ __device__ __forceinline__ int sca_tile(const ScaParams &p)
             tile = full + xcd * s2 + k;
         }
     }
-    return tile;
+    t.b = tile / p.tiles_per_b;
+    const int tb = tile - t.b * p.tiles_per_b;
+    t.qg = tb / p.heads;
+    t.head = tb - t.qg * p.heads;
+    return t;
 }
 
 // Stage matrices, level table and anchors; phase 1: reference points and
@@ -322,36 +359,15 @@ struct ScaSlot {
     size_t pt0;           // first (level, point) element of the pair
 };
 
-__device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m, int b,
-                                            int64_t pair0, int r_first, int wave, int lane)
-{
-    ScaSlot s;
-    s.sub = lane & (p.lph - 1);
-    s.slot = lane >> p.lph_shift;
-    const int64_t pair = pair0 + (int64_t)wave * p.spw + s.slot;
-    s.active = pair < (int64_t)p.Q * p.heads;
-    const int rank = s.active ? (int)(pair / p.heads) : r_first;
-    s.mh = s.active ? (int)(pair - (int64_t)rank * p.heads) : 0;
-    s.qi = rank - r_first;
-    int qx, qy;
-    query_of(rank, p.X, p.Y, qx, qy);
-    s.q = qx * p.Y + qy;
-    s.hits = s.active ? m.hit[s.qi] : 0u;
-    const int count = __popc(s.hits);
-    s.inv = (p.reduce == FLASHBEV_REDUCE_VALID_MEAN && count > 1) ? 1.0f / (float)count : 1.0f;
-    s.pt0 = (((size_t)b * p.Q + s.q) * p.heads + s.mh) * (size_t)p.LP;
-    return s;
-}
-
-// A slot of the backward.  A backward tile holds waves * spw consecutive
-// queries (ranks r_first ..., in the Z order of query_of) of one head, slot s
-// of wavefront w being query r_first + w spw + s.  All slots of the tile then
-// share their head and cover a compact patch of cells, so their taps on one
+// A slot of a tile.  A tile holds waves * spw consecutive queries (ranks
+// r_first ..., in the Z order of query_of) of one head, slot s of wavefront w
+// being query r_first + w spw + s.  All slots of the tile then share their
+// head and cover a compact patch of cells: in the backward their taps on one
 // pixel are the same value-gradient row and are merged before the scatter
 // (BEVFormer-base, P = 8, per chunk of 8 points: 1.83x fewer rows for 1 x 8
 // strips of queries, 2.05x for 2 x 4 patches, 2.85x for 4 x 4, 3.85x for
 // 4 x 8).
-__device__ __forceinline__ ScaSlot sca_slot_bwd(const ScaParams &p, const ScaSmem &m, int b,
+__device__ __forceinline__ ScaSlot sca_slot(const ScaParams &p, const ScaSmem &m, int b,
                                                 int r_first, int head, int wave, int lane)
 {
     ScaSlot s;
@@ -491,13 +507,12 @@ sca_fwd(const ScaParams p)
     const int wave = threadIdx.x / kScaWave;
     const int lane = threadIdx.x % kScaWave;
 
-    const int tile = sca_tile(p);
-    const int b = tile / p.tiles_per_b;
-    const int64_t pair0 = (int64_t)(tile - b * p.tiles_per_b) * p.tile_pairs;
-    const int r_first = (int)(pair0 / p.heads);   // first query rank of the tile
+    const ScaTile tl = sca_tile(p);
+    const int b = tl.b;
+    const int r_first = tl.qg * p.tile_pairs;   // first query rank of the tile
     sca_project_tile(p, m, b, r_first);
 
-    const ScaSlot s = sca_slot(p, m, b, pair0, r_first, wave, lane);
+    const ScaSlot s = sca_slot(p, m, b, r_first, tl.head, wave, lane);
     const int lph = p.lph, LP = p.LP;
     float *att = m.att + (size_t)(wave * p.spw + s.slot) * LP;
     // attention weights with the mean over hit cameras folded in
@@ -582,15 +597,12 @@ sca_bwd(const ScaParams p)
     const int tid = threadIdx.x;
     const int nthreads = blockDim.x;
 
-    // tiles: (query group, head), the heads of a query group consecutive
-    const int tile = sca_tile(p);
-    const int b = tile / p.tiles_per_b;
-    const int tb = tile - b * p.tiles_per_b;
-    const int qg = tb / p.heads;
-    const int r_first = qg * (nthreads / kScaWave) * p.spw;
+    const ScaTile tl = sca_tile(p);
+    const int b = tl.b;
+    const int r_first = tl.qg * p.tile_pairs;   // first query rank of the tile
     sca_project_tile(p, m, b, r_first);
 
-    const ScaSlot s = sca_slot_bwd(p, m, b, r_first, tb - qg * p.heads, wave, lane);
+    const ScaSlot s = sca_slot(p, m, b, r_first, tl.head, wave, lane);
     const int lph = p.lph, LP = p.LP;
     const int slot_id = wave * p.spw + s.slot;
     // softmax a_j = expf(logit_j - mx) * rcp, recomputed where needed
@@ -1019,8 +1031,8 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     ScaLds lay{};
     for (;;) {
         const int tp = waves * spw;
-        // forward: tp consecutive (query, head) pairs; backward: tp queries
-        nq_max = backward ? tp : (tp - 1) / v->heads + 2;
+        // tp consecutive queries of one head
+        nq_max = tp;
         if ((uint64_t)nq_max > Q) nq_max = (int)(Q > 0 ? Q : 1);
         lay = sca_lds_layout(v->N, zb->Z, nq_max, waves, spw, LP, D, slot_stride, backward);
         if (lay.total <= budget || waves == 1) break;
@@ -1054,11 +1066,14 @@ int make_sca_plan(const flashsca_value *v, const flashbev_bev_grid_spec *s,
     p.lph_shift = lph_shift;
     p.spw = spw;
     p.tile_pairs = tile_pairs;
-    const uint64_t pairs_b = Q * (uint64_t)v->heads;
-    // forward: tile_pairs consecutive pairs; backward: tile_pairs queries of
-    // one head (at most Q heads tiles, within 2^31 - 1)
-    p.tiles_per_b = backward ? (int32_t)(((Q + tile_pairs - 1) / tile_pairs) * (uint64_t)v->heads)
-                             : (int32_t)((pairs_b + tile_pairs - 1) / tile_pairs);
+    // tiles of tile_pairs queries of one head (at most Q heads tiles, within
+    // 2^31 - 1)
+    p.tiles_per_b = (int32_t)(((Q + tile_pairs - 1) / tile_pairs) * (uint64_t)v->heads);
+    // head-to-XCD order (sca_tile) for the forward; the backward, whose time
+    // at few points goes to the row merge and its atomics, keeps the band
+    // order up to 32 points per head (measured on MI355X at BEVFormer-base:
+    // P = 8 1.44 ms band against 1.47 head order, P = 32 4.50 against 4.36)
+    p.head_xcd = ((v->heads % kScaXcds) == 0 && (!backward || LP > 32)) ? kScaHeadChunks : 0;
     {
         int lg = 0;
         while ((kMrgRows * waves) >> (lg + 1)) ++lg;

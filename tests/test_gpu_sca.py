@@ -106,6 +106,7 @@ def test_sca_reduce_modes(fb, device, reduce):
     (12, 4, "f32"),      # D=3: padded lanes
     (10, 2, "bf16"),     # D=5: 2-byte lanes
     (48, 3, "f16"),      # D=16, three heads
+    (512, 16, "f32"),    # D=32, two head groups in the head-to-XCD order
 ])
 def test_sca_channel_and_head_shapes(fb, device, C, heads, dtype):
     inst = small(2, C=C, heads=heads, dtype=dtype, X=9, Y=7)

@@ -132,6 +132,14 @@ def test_sca_backward_channel_and_head_shapes(fb, device, C, heads, dtype):
           what=f"C={C} heads={heads} {dtype}")
 
 
+@pytest.mark.parametrize("C,heads,dtype", [(256, 8, "f32"), (512, 16, "f32"), (256, 8, "bf16")])
+def test_sca_backward_head_to_xcd_order(fb, device, C, heads, dtype):
+    # heads a multiple of 8 and more than 32 points per head: tiles follow the
+    # head-to-XCD order (two head groups at 16 heads, both batch elements)
+    check(fb, small(5, C=C, heads=heads, dtype=dtype, P=16, Z=4, X=23, Y=19), device,
+          what=f"head order C={C} heads={heads} {dtype} P=16")
+
+
 @pytest.mark.parametrize("P,Z,L", [(1, 1, 1), (3, 1, 2), (8, 4, 4), (32, 4, 4), (64, 8, 8)])
 def test_sca_backward_points_anchors_levels(fb, device, P, Z, L):
     levels = ((24, 64), (12, 32), (6, 16), (3, 8), (2, 4), (1, 2), (1, 1), (5, 3))[:L]
