@@ -19,7 +19,9 @@
  * Slots of a wavefront's 16 (unsigned 64-bit): 0 start, 1 staged, 2
  * projection, 3 set-up, 4 padding, 5 gather, 6 stash (2..6 are tick sums),
  * 7 barrier, 8 end, 9 rounds (groups of cells), 10 projection passes,
- * 11..15 zero.
+ * 11 the wavefront's HW_ID register (SIMD, CU, shader array, shader engine)
+ * in bits 0..31 and its XCC_ID register (the XCD) in bits 32..63, 12 the
+ * valid samples of its groups, 13..15 zero.
  */
 #ifndef FLASHBEV_PHASES_H
 #define FLASHBEV_PHASES_H

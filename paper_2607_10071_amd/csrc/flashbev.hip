@@ -62,7 +62,9 @@ constexpr int kStripe = 16;               // consecutive tiles per XCD stripe
 // (B X Y Z C elem) take contiguous bands of tiles per XCD, larger ones
 // interleaved stripes.  Measured on MI355X (bands against stripes of 16):
 // rep 23.9 -> 23.5 us, half_batch 77.6 -> 74.6, the paper's reference
-// setting 35.1 -> 32.8, long_range 105.6 -> 103.1, z_sweep 213.7 -> 212.0;
+// setting 35.1 -> 32.8, long_range 105.6 -> 103.1, z_sweep 213.7 -> 212.0
+// (re-checked since: half_batch 70.5 -> 66.8, long_range 72.7 -> 71.7,
+// z_sweep 182.3 -> 180.4, the reference setting 33.1 -> 31.1, rep equal);
 // but with 8x the work (Z = 64, C = 1024 or a 1600 x 1600 grid at the
 // reference setting) bands lose 4% to the stripes' better balance.
 constexpr uint64_t kBandsWorkMax = 1ull << 30;
@@ -97,6 +99,8 @@ struct Params {
     float x_min, dx, y_min, dy, depth_eps;
     int32_t reduce;        // 0 valid mean, 1 sum
     int32_t bands;         // 1: one contiguous band of tiles per XCD, 0: interleaved stripes
+    int32_t tail_prio;     // 1: all workgroups resident at once; waves take issue priority
+                           // from their groups' longest sample list (per-cell passes)
     uint32_t row_bytes;    // C * element size
     uint32_t step_x;       // byte step to the right-hand tap (0 if W == 1)
     uint32_t step_y;       // byte step to the lower tap (0 if H == 1)
@@ -233,12 +237,18 @@ __device__ unsigned long long *phase_log;
 constexpr int kPhaseSlots = 16;
 enum PhaseSlot {
     kPhStart = 0, kPhStaged = 1, kPhProject = 2, kPhSetup = 3, kPhPad = 4, kPhGather = 5,
-    kPhStash = 6, kPhBarrier = 7, kPhEnd = 8, kPhRounds = 9, kPhPasses = 10
+    kPhStash = 6, kPhBarrier = 7, kPhEnd = 8, kPhRounds = 9, kPhPasses = 10, kPhHwId = 11,
+    kPhSamples = 12
 };
+// slot 11: the wavefront's HW_ID register (SIMD, CU, shader array and engine)
+// in the low 32 bits and XCC_ID (its XCD) in the high 32; slot 12: the valid
+// samples of its groups
 #define PH_DECL                                                              \
     unsigned long long ph_t = __builtin_amdgcn_s_memrealtime();              \
     unsigned long long ph_s[kPhaseSlots] = {};                               \
-    ph_s[kPhStart] = ph_t
+    ph_s[kPhStart] = ph_t;                                                   \
+    ph_s[kPhHwId] = (unsigned)__builtin_amdgcn_s_getreg((31 << 11) | 4) |    \
+                    ((unsigned long long)(unsigned)__builtin_amdgcn_s_getreg((31 << 11) | 20) << 32)
 #define PH_AT(slot)                                                          \
     do {                                                                     \
         ph_t = __builtin_amdgcn_s_memrealtime();                             \
@@ -251,6 +261,7 @@ enum PhaseSlot {
         ph_t = ph_n;                                                         \
     } while (0)
 #define PH_COUNT(slot) (ph_s[slot] += 1)
+#define PH_ADDV(slot, v) (ph_s[slot] += (unsigned long long)(v))
 #define PH_WRITE(lane)                                                       \
     do {                                                                     \
         if (phase_log && (lane) == 0) {                                      \
@@ -264,6 +275,7 @@ enum PhaseSlot {
 #define PH_AT(slot) ((void)0)
 #define PH_ADD(slot) ((void)0)
 #define PH_COUNT(slot) ((void)0)
+#define PH_ADDV(slot, v) ((void)0)
 #define PH_WRITE(lane) ((void)0)
 #endif
 
@@ -317,7 +329,7 @@ sample_vt_fwd(const Params p)
     //    S consecutive tiles interleaved over the grid, so that each XCD sees
     //    a like mix of heavy and light regions and the tail stays short.
     // Either way neighbouring tiles merge their partial output lines in one
-    // L2.  The choice is made on the host (make_plan).
+    // L2.  The choice is made on the host (make_plan, forward_order).
     const int g = blockIdx.x;
     int tile = g;
     if (p.bands) {
@@ -595,6 +607,7 @@ sample_vt_fwd(const Params p)
                         // the pass's valid samples per cell
                         for (int mm = 0; mm < cpp && m0 + mm < ncell; ++mm) {
                             const int c = __popcll(mask & (lowmask64(P) << (mm * P)));
+                            PH_ADDV(kPhSamples, c);
                             cnt_lane = lane == m0 + mm ? c : cnt_lane;
                             maxcnt = c > maxcnt ? c : maxcnt;
                         }
@@ -656,6 +669,28 @@ sample_vt_fwd(const Params p)
                 }
                 const int maxpad = (maxcnt + kUnroll - 1) / kUnroll * kUnroll;
                 wave_lds_sync();
+                if (p.tail_prio) {
+                    // When every workgroup is resident from the start, the
+                    // call ends with its heaviest wavefronts: the longest
+                    // sample list sets a group's gather iterations, and the
+                    // lists of cells that several cameras see at most heights
+                    // (overlap zones, far range) are up to twice the median.
+                    // Such wavefronts take a higher issue priority, so they
+                    // are not left to finish alone at the end (measured on
+                    // MI355X: rep 22.25 -> 21.6 us, Z = 4 15.8 -> 15.3, Z = 6
+                    // 19.0 -> 18.5; thresholds between 1.05 and 2 samples per
+                    // height give the same).  With several generations of
+                    // workgroups the hardware balances the finish by itself
+                    // and the priorities cost 1-2% (the paper's reference
+                    // setting), so they stay off there.
+                    const int zh = (p.Z - z0) < p.zc ? (p.Z - z0) : p.zc;
+                    const int t20 = maxcnt * 20;
+                    if (t20 >= 38 * zh) __builtin_amdgcn_s_setprio(3);
+                    else if (t20 >= 32 * zh) __builtin_amdgcn_s_setprio(2);
+                    else if (t20 >= 26 * zh) __builtin_amdgcn_s_setprio(1);
+                    else __builtin_amdgcn_s_setprio(0);
+                }
+                PH_ADDV(kPhSamples, total);
                 PH_ADD(kPhProject);
                 PH_COUNT(kPhPasses);
 
@@ -2027,6 +2062,7 @@ struct Plan {
     int lw, vpl;
     bool cull_path;     // the culled, packed projection phase
     bool empty;
+    bool band_work;     // little enough work for contiguous bands
 };
 
 bool finite(float v) { return v == v && v - v == 0.0f; }
@@ -2172,7 +2208,9 @@ int make_plan(const flashbev_features *f, const float *l2i, const flashbev_bev_g
     p.x_min = s->x_min; p.dx = s->dx; p.y_min = s->y_min; p.dy = s->dy;
     p.depth_eps = s->depth_eps;
     p.reduce = s->reduce;
-    p.bands = (size_prod({(uint64_t)f->B, XY, (uint64_t)zb->Z, row}) <= kBandsWorkMax) ? 1 : 0;
+    p.bands = 0;       // forward_order, at launch
+    p.tail_prio = 0;
+    pl->band_work = size_prod({(uint64_t)f->B, XY, (uint64_t)zb->Z, row}) <= kBandsWorkMax;
     p.row_bytes = (uint32_t)row;
     p.step_x = f->W >= 2 ? (uint32_t)row : 0u;
     p.step_y = f->H >= 2 ? (uint32_t)(row * f->W) : 0u;
@@ -2639,6 +2677,49 @@ int launch_bwd_gather(const BwdGatherPlan &pl, hipStream_t st)
 
 }  // namespace
 
+// Workgroups of one forward kernel resident at once on the current device
+// (occupancy of its registers and LDS times the compute units), 0 if HIP
+// cannot say.  Kept per (kernel, threads, LDS, device).
+int64_t resident_workgroups(const void *fn, int threads, size_t lds)
+{
+    struct Entry {
+        const void *fn;
+        int threads;
+        size_t lds;
+        int dev;
+        int64_t resident;
+    };
+    static std::mutex mu;
+    static Entry cache[64];
+    static int used = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < used; ++i)
+        if (cache[i].fn == fn && cache[i].threads == threads && cache[i].lds == lds &&
+            cache[i].dev == dev)
+            return cache[i].resident;
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    const int64_t r = (int64_t)per_cu * cus;
+    if (used < 64) cache[used++] = Entry{fn, threads, lds, dev, r};
+    return r;
+}
+
+// Launch-time choices of a forward call: contiguous bands of tiles per XCD
+// for calls up to kBandsWorkMax (else stripes), and whether every workgroup
+// is resident from the start, which turns on the waves' tail priorities
+// (tail_prio).  Resident workgroups come from HIP's occupancy query for the
+// kernel; if HIP cannot say, there are no priorities.
+void forward_order(const void *fn, Plan &pl)
+{
+    const int64_t resident = resident_workgroups(fn, pl.threads, pl.lds);
+    pl.prm.tail_prio = (resident > 0 && pl.workgroups <= resident) ? 1 : 0;
+    pl.prm.bands = pl.band_work ? 1 : 0;
+}
+
 extern "C" {
 
 int flashbev_abi_version(void) { return FLASHBEV_ABI_VERSION; }
@@ -2686,6 +2767,7 @@ int flashbev_sample_vt(const flashbev_features *features, const float *lidar2img
     if (pl.empty) return FLASHBEV_OK;
     const KernelFn fn = pick_kernel(features->dtype, pl.lw, pl.vpl, pl.cull_path);
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
+    forward_order(reinterpret_cast<const void *>(fn), pl);
     void *args[] = {&pl.prm};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(fn),
                                          dim3((unsigned)pl.workgroups), dim3(pl.threads), args,
