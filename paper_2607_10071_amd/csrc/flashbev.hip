@@ -675,16 +675,18 @@ sample_vt_fwd(const Params p)
                     // sample list sets a group's gather iterations, and the
                     // lists of cells that several cameras see at most heights
                     // (overlap zones, far range) are up to twice the median.
-                    // Such wavefronts take a higher issue priority, so they
-                    // are not left to finish alone at the end (measured on
-                    // MI355X: rep 22.25 -> 21.6 us, Z = 4 15.8 -> 15.3, Z = 6
-                    // 19.0 -> 18.5; thresholds between 1.05 and 2 samples per
-                    // height give the same).  With several generations of
-                    // workgroups the hardware balances the finish by itself
-                    // and the priorities cost 1-2% (the paper's reference
-                    // setting), so they stay off there.
+                    // Such wavefronts take a higher issue priority, the work
+                    // left to them estimated as this group's longest list
+                    // times the rounds left, so they are not left to finish
+                    // alone at the end (measured on MI355X: rep 22.25 ->
+                    // 21.4 us, Z = 4 15.8 -> 15.2, Z = 6 19.0 -> 17.7;
+                    // thresholds between 1.05 and 2 samples per height give
+                    // the same).  With several generations of workgroups the
+                    // hardware balances the finish by itself and the
+                    // priorities cost 1-2% (the paper's reference setting),
+                    // so they stay off there.
                     const int zh = (p.Z - z0) < p.zc ? (p.Z - z0) : p.zc;
-                    const int t20 = maxcnt * 20;
+                    const int t20 = maxcnt * 20 * (p.rounds - r);
                     if (t20 >= 38 * zh) __builtin_amdgcn_s_setprio(3);
                     else if (t20 >= 32 * zh) __builtin_amdgcn_s_setprio(2);
                     else if (t20 >= 26 * zh) __builtin_amdgcn_s_setprio(1);
