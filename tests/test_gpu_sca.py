@@ -113,6 +113,17 @@ def test_sca_channel_and_head_shapes(fb, device, C, heads, dtype):
     check(fb, inst, device, what=f"C={C} heads={heads} {dtype}")
 
 
+@pytest.mark.parametrize("C,heads,dtype", [(256, 8, "f32"), (256, 8, "bf16"), (32, 4, "f32")])
+def test_sca_azimuth_block_order(fb, device, C, heads, dtype):
+    # a 32 x 48 grid of six whole 16 x 16 blocks and 144 points per head: the
+    # query groups are visited in the azimuth order of the blocks (with the
+    # head order at 8 heads, the band order at 4); every output element is
+    # overwritten
+    inst = small(6, C=C, heads=heads, dtype=dtype, X=32, Y=48, P=48, Z=4, x_min=-30.0, dx=2.0,
+                 y_min=-45.0, dy=2.0)
+    check(fb, inst, device, what=f"azimuth order C={C} heads={heads} {dtype}", prefill=np.nan)
+
+
 @pytest.mark.parametrize("P,Z,L", [(1, 1, 1), (3, 1, 2), (8, 4, 4), (16, 4, 4), (32, 4, 4),
                                    (6, 3, 3), (64, 8, 8)])
 def test_sca_points_anchors_levels(fb, device, P, Z, L):

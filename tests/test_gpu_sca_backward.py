@@ -140,6 +140,15 @@ def test_sca_backward_head_to_xcd_order(fb, device, C, heads, dtype):
           what=f"head order C={C} heads={heads} {dtype} P=16")
 
 
+@pytest.mark.parametrize("C,heads,P", [(256, 8, 8), (256, 8, 16), (32, 4, 16)])
+def test_sca_backward_azimuth_block_order(fb, device, C, heads, P):
+    # a 32 x 48 grid of six whole 16 x 16 blocks: rank order at P = 8 (24
+    # points per head), the azimuth order of the blocks at P = 16 (with the
+    # head order at 8 heads, the band order at 4)
+    check(fb, small(6, C=C, heads=heads, P=P, Z=4, X=32, Y=48, x_min=-30.0, dx=2.0, y_min=-45.0,
+                    dy=2.0), device, what=f"azimuth order C={C} heads={heads} P={P}", prefill=np.nan)
+
+
 @pytest.mark.parametrize("P,Z,L", [(1, 1, 1), (3, 1, 2), (8, 4, 4), (32, 4, 4), (64, 8, 8)])
 def test_sca_backward_points_anchors_levels(fb, device, P, Z, L):
     levels = ((24, 64), (12, 32), (6, 16), (3, 8), (2, 4), (1, 2), (1, 1), (5, 3))[:L]
