@@ -25,9 +25,13 @@
  *     counts in the per-height denominator;
  *   - accumulation in float32 for every input type; the output is float32.
  *
- * Thread safety: the library keeps no state; calls are asynchronous on the
- * given stream and may be issued from several threads.  It never allocates
- * device or host memory, never prints and never aborts.
+ * Thread safety: calls are asynchronous on the given stream and may be
+ * issued from several threads.  The library keeps no per-call state; it
+ * remembers, per device and under a lock, how many workgroups of each
+ * forward kernel shape fit the GPU at once (HIP's occupancy query, which
+ * picks the forward's tile order and tail priorities), and the no-allocation
+ * backward holds its static scratch array (below).  It never allocates device
+ * or host memory, never prints and never aborts.
  *
  * Device: kernels run on the calling thread's current HIP device, which must
  * hold every buffer of the call and the stream.
