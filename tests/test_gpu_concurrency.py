@@ -1,7 +1,7 @@
 """Statelessness of the C ABI under concurrent callers (GPU).
 
-The headers state that the library keeps no state and that calls may come
-from several threads on their own streams.  Here two host threads, each with
+The headers state that the library keeps no per-call state and that calls
+may come from several threads on their own streams.  Here two host threads, each with
 its own stream and its own inputs, issue forward, FlashSCA forward and
 backward calls in a loop; every result must equal what the same call gives
 alone (bitwise for the forwards, which have no atomics; within the parity

@@ -237,6 +237,28 @@ def test_run_to_run_bitwise_determinism(fb, device):
     assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("name,copies", [("rep", 3), ("paper_ref", 8)])
+def test_launch_order_leaves_outputs_bitwise(fb, device, name, copies):
+    # rep at B = 1 has every workgroup resident at once (contiguous bands,
+    # tail priorities); repeated three times it needs several generations of
+    # workgroups (no priorities).  paper_ref at B = 1 takes bands, repeated
+    # eight times (over 2^30 gathered bytes) interleaved stripes.  The tile
+    # order and the issue priorities decide only when a cell is computed, not
+    # how, so every copy equals the B = 1 result bit for bit.
+    import torch
+    inst = synth.make_workload(synth.config(name))
+    wl = inst.wl
+    ft, l2i = to_dev(inst, device)
+    grid, img = fb.grid_of(wl), (wl.img_h, wl.img_w)
+    one = fb.sample_vt(ft[:1].contiguous(), l2i[:1].contiguous(), inst.z, grid, img)
+    ftk = ft[:1].repeat(copies, 1, 1, 1, 1).contiguous()
+    l2ik = l2i[:1].repeat(copies, 1, 1, 1).contiguous()
+    many = fb.sample_vt(ftk, l2ik, inst.z, grid, img)
+    torch.cuda.synchronize()
+    for b in range(copies):
+        assert torch.equal(many[b], one[0]), f"{name}: copy {b} differs from the single call"
+
+
 def test_non_default_stream(fb, device):
     import torch
     inst = small(C=24)

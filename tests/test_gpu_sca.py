@@ -124,6 +124,34 @@ def test_sca_azimuth_block_order(fb, device, C, heads, dtype):
     check(fb, inst, device, what=f"azimuth order C={C} heads={heads} {dtype}", prefill=np.nan)
 
 
+@pytest.mark.parametrize("P", [8, 32])
+def test_sca_launch_order_leaves_outputs_bitwise(fb, device, P):
+    # BEVFormer-base (heads to XCDs; at P = 32 also the azimuth order of the
+    # blocks) at B = 1 and the same batch element twice: the tile orders
+    # decide only when a query is computed, so both copies equal the single
+    # call bit for bit, and so do the backward's offset and logit gradients
+    # (no atomics there)
+    import torch
+    inst = synth.make_sca_workload(synth.sca_config("sca_base", P=P))
+    wl = inst.wl
+    v, l2i, off, lg = _dev(inst, device)
+    grid, img = fb.grid_of(wl), (wl.img_h, wl.img_w)
+    two = [t[:1].repeat(2, *([1] * (t.dim() - 1))).contiguous() for t in (v, l2i, off, lg)]
+    one = fb.sca_forward(v, l2i, inst.z, grid, img, wl.levels, wl.heads, off, lg)
+    dup = fb.sca_forward(*two[:2], inst.z, grid, img, wl.levels, wl.heads, *two[2:])
+    g = torch.from_numpy(np.random.default_rng(P).standard_normal(
+        (1, wl.Q, wl.C)).astype(np.float32)).to(device)
+    want = ("offsets", "logits")
+    b1 = fb.sca_backward(v, l2i, inst.z, grid, img, wl.levels, wl.heads, off, lg, g, want=want)
+    b2 = fb.sca_backward(*two[:2], inst.z, grid, img, wl.levels, wl.heads, *two[2:],
+                         g.repeat(2, 1, 1).contiguous(), want=want)
+    torch.cuda.synchronize()
+    for b in range(2):
+        assert torch.equal(dup[b], one[0]), f"P={P}: forward copy {b} differs"
+        for k in want:
+            assert torch.equal(b2[k][b], b1[k][0]), f"P={P}: {k} gradient copy {b} differs"
+
+
 @pytest.mark.parametrize("P,Z,L", [(1, 1, 1), (3, 1, 2), (8, 4, 4), (16, 4, 4), (32, 4, 4),
                                    (6, 3, 3), (64, 8, 8)])
 def test_sca_points_anchors_levels(fb, device, P, Z, L):
