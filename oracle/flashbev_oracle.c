@@ -23,7 +23,7 @@
  * of the forward's linear map, written as a scatter of each valid sample's
  * weighted output gradient onto its bilinear taps.
  *
- * Readings where the paper is silent (each one is also listed in the design doc):
+ * Readings where the paper is silent:
  *   - coordinates follow one fixed float32 recipe: every product and sum is
  *     rounded on its own (no fused multiply-add), left to right, and the
  *     perspective divide is an IEEE float32 division.  Mask and floor

@@ -23,7 +23,7 @@
  *                softmax_{l,k}(s[b,q,m,:,:])[l,k] *
  *                bilinear(V[b,n,l][:, :, c], ref_n(anchor(k)) * (W_l, H_l) + dp[b,q,m,l,k] - 1/2)
  *
- * Readings (each one is also listed in the design doc):
+ * Readings (the paper gives the idea; the semantics are BEVFormer's published SCA):
  *   - queries are the BEV cells of the Eq. 1 grid, q = i Y + j, with cell
  *     centre (x_min + (i + 1/2) dx, y_min + (j + 1/2) dy);
  *   - point k of a (head, level) belongs to anchor k mod Z (BEVFormer splits
