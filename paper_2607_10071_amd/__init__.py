@@ -19,6 +19,7 @@ __all__ = [
     "sca_backward", "sca_backward_launch_info", "prepare_sca_backward",
     "launch_info", "backward_launch_info", "status_string", "abi_version", "library_path",
     "FlashBevError", "DTYPE_CODES", "REDUCE_CODES", "STATUS",
+    "sample_vt_autograd", "sca_autograd",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -827,3 +828,84 @@ def prepare_sca_backward(value, lidar2img, anchors, grid: BevGrid, img_hw, level
     return _Prepared(_lib().flashsca_backward, args,
                      (value, lidar2img, offsets, logits, grad_out, outs, z, v, g, zb),
                      "flashsca_backward", dev)
+
+
+# ---------------------------------------------------------------------------
+# autograd: the two operators as differentiable torch functions
+# ---------------------------------------------------------------------------
+_AUTOGRAD = {}
+
+
+def _autograd_functions():
+    """The torch.autograd.Function classes, made on first use (torch is
+    imported lazily).  Their forward and backward are the calls above."""
+    if _AUTOGRAD:
+        return _AUTOGRAD
+    import torch
+
+    class _SampleVT(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, features, lidar2img, z_bins, grid, img_hw, reduce, method):
+            ctx.save_for_backward(lidar2img)
+            ctx.meta = (tuple(features.shape), features.dtype, z_bins, grid, tuple(img_hw),
+                        reduce, method)
+            return sample_vt(features, lidar2img, z_bins, grid, img_hw, reduce=reduce)
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            (l2i,) = ctx.saved_tensors
+            shape, dtype, z_bins, grid, img_hw, reduce, method = ctx.meta
+            g = None
+            if ctx.needs_input_grad[0]:
+                g = sample_vt_backward(grad_out.float().contiguous(), l2i, z_bins, grid, img_hw,
+                                       shape, _dtype_name(dtype), reduce=reduce, method=method)
+                if g.dtype != dtype:
+                    g = g.to(dtype)
+            return g, None, None, None, None, None, None
+
+    class _SCA(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, value, lidar2img, offsets, logits, anchors, grid, img_hw, levels, heads,
+                    reduce):
+            ctx.save_for_backward(value, lidar2img, offsets, logits)
+            ctx.meta = (anchors, grid, tuple(img_hw), tuple(levels), heads, reduce)
+            return sca_forward(value, lidar2img, anchors, grid, img_hw, levels, heads, offsets,
+                               logits, reduce=reduce)
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            value, l2i, off, lg = ctx.saved_tensors
+            anchors, grid, img_hw, levels, heads, reduce = ctx.meta
+            want = tuple(k for k, i in (("value", 0), ("offsets", 2), ("logits", 3))
+                         if ctx.needs_input_grad[i])
+            if not want:
+                return (None,) * 10
+            r = sca_backward(value, l2i, anchors, grid, img_hw, levels, heads, off, lg,
+                             grad_out.float().contiguous(), want=want, reduce=reduce)
+            gv = r["value"]
+            if gv is not None and gv.dtype != value.dtype:
+                gv = gv.to(value.dtype)
+            return gv, None, r["offsets"], r["logits"], None, None, None, None, None, None
+
+    _AUTOGRAD["sample_vt"] = _SampleVT
+    _AUTOGRAD["sca"] = _SCA
+    return _AUTOGRAD
+
+
+def sample_vt_autograd(features, lidar2img, z_bins, grid: BevGrid, img_hw: Tuple[int, int],
+                       reduce: str = "mean", method: str = "gather"):
+    """``sample_vt`` as a differentiable function: the gradient with respect to
+    ``features`` is ``sample_vt_backward`` (``method``), cast to the features'
+    dtype; the camera matrices get none (they are fixed inputs of Eq. 1)."""
+    return _autograd_functions()["sample_vt"].apply(features, lidar2img, z_bins, grid, img_hw,
+                                                    reduce, method)
+
+
+def sca_autograd(value, lidar2img, anchors, grid: BevGrid, img_hw: Tuple[int, int], levels,
+                 heads: int, offsets, logits, reduce: str = "mean"):
+    """``sca_forward`` as a differentiable function: the gradients with respect
+    to ``value`` (cast to its dtype), ``offsets`` and ``logits`` are
+    ``sca_backward``'s, computed only for the inputs that need them; the
+    camera matrices and anchors get none."""
+    return _autograd_functions()["sca"].apply(value, lidar2img, offsets, logits, anchors, grid,
+                                              img_hw, levels, heads, reduce)

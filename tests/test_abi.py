@@ -443,3 +443,19 @@ def test_noalloc_backward_checks_before_any_hip_call():
     # nothing to do: no HIP call either
     assert raw((0, 6, 32, 88, 80), "f32", L2I, z, grid, (256, 704), OUT, FEAT) == S["OK"]
     assert fb.status_string(S["ERR_SCRATCH"]) != "unknown status"
+
+
+def test_autograd_wrappers_are_exported_and_refuse_host_tensors():
+    # the differentiable wrappers marshal to the same C calls; on host
+    # tensors they raise rather than compute anything
+    import torch
+    import paper_2607_10071_amd as fb
+    assert "sample_vt_autograd" in fb.__all__ and "sca_autograd" in fb.__all__
+    fns = fb._autograd_functions()
+    assert issubclass(fns["sample_vt"], torch.autograd.Function)
+    assert issubclass(fns["sca"], torch.autograd.Function)
+    feats = torch.zeros((1, 1, 2, 2, 4), requires_grad=True)
+    l2i = torch.eye(4).reshape(1, 1, 4, 4)
+    grid = fb.BevGrid(x_min=-1.0, dx=1.0, X=2, y_min=-1.0, dy=1.0, Y=2)
+    with pytest.raises(ValueError):
+        fb.sample_vt_autograd(feats, l2i, [0.0], grid, (8, 8))
