@@ -1,10 +1,11 @@
 /*
- * flashbev_phases.h -- phase clock of the fused Sampling-VT forward
- * (measurement tool, MI355X / gfx950).
+ * flashbev_phases.h -- phase clocks of the fused Sampling-VT forward and the
+ * FlashSCA backward (measurement tool, MI355X / gfx950).
  *
  * libflashbev_phases.so is the operator library of include/flashbev.h and
- * include/flashsca.h built once more with the forward's phase clock compiled
- * in; it is not the operator's library (libflashbev.so has no clock).  In
+ * include/flashsca.h built once more with the phase clocks of the forward and
+ * of the FlashSCA backward compiled in; it is not the operator's library
+ * (libflashbev.so has no clock).  In
  * it, lane 0 of every wavefront of the forward kernel records the 100 MHz
  * real-time counter (s_memrealtime) at its start, after it has staged the
  * camera matrices and heights (and the workgroup barrier), after the
@@ -41,6 +42,25 @@ extern "C" {
  * fails.
  */
 int flashbev_phase_log(void *log);
+
+/*
+ * The same for the FlashSCA backward (include/flashsca.h, flashsca_backward;
+ * the BEVFormer spatial cross-attention of Sec. 4.5): lane 0 of every
+ * wavefront of its kernel sums the real-time counter over the kernel's steps.
+ * Memory of at least workgroups * (threads_per_workgroup / 64) * 16 unsigned
+ * 64-bit words (flashsca_backward_launch_info), written at
+ * [(workgroup * waves + wave) * 16 + slot]; NULL stops the recording.
+ * Slots (tick sums unless stated): 0 start (counter), 1 projection of the
+ * tile's anchors and hit masks, 2 softmax statistics, output-gradient rows and
+ * merge-table set-up, 3 chunk set-up and records, 4 point gradients (tap
+ * loads, dot products, sums across the slot), 5 inserts into the merge table,
+ * 6 the barrier after the inserts, 7 the walk of the distinct rows with their
+ * float atomics, 8 the barrier after the walk, 9 emptying the table, 10
+ * chunk-camera steps (count), 11 distinct rows over all steps (count), 12 the
+ * tail (offset and logit gradients), 13 end (counter), 14..15 zero.  Returns
+ * 0, or -1 if the copy to the device variable fails.
+ */
+int flashsca_phase_log(void *log);
 
 #ifdef __cplusplus
 }

@@ -606,6 +606,47 @@ sca_fwd(const ScaParams p)
     }
 }
 
+// Phase clock of the backward, compiled in only with FLASHBEV_PHASE_CLOCK
+// (the instrumented library libflashbev_phases.so; the operator's library
+// has none of it).  Lane 0 of each wavefront sums the real-time counter
+// (100 MHz) over the kernel's steps and writes the sums at its end to
+// sca_phase_log[(workgroup * waves + wave) * kScaPhaseSlots + slot].
+#ifdef FLASHBEV_PHASE_CLOCK
+__device__ unsigned long long *sca_phase_log;
+constexpr int kScaPhaseSlots = 16;
+enum ScaPhaseSlot {
+    kSpStart = 0, kSpProject = 1, kSpSetup = 2, kSpRecords = 3, kSpPoint = 4, kSpInsert = 5,
+    kSpInsertBarrier = 6, kSpWalk = 7, kSpWalkBarrier = 8, kSpClear = 9, kSpSteps = 10,
+    kSpKeys = 11, kSpTail = 12, kSpEnd = 13
+};
+#define SPH_DECL                                                             \
+    unsigned long long sph_t = __builtin_amdgcn_s_memrealtime();             \
+    unsigned long long sph[kScaPhaseSlots] = {};                             \
+    sph[kSpStart] = sph_t
+#define SPH_ADD(slot)                                                        \
+    do {                                                                     \
+        const unsigned long long sph_n = __builtin_amdgcn_s_memrealtime();   \
+        sph[slot] += sph_n - sph_t;                                          \
+        sph_t = sph_n;                                                       \
+    } while (0)
+#define SPH_COUNT(slot, v) (sph[slot] += (unsigned long long)(v))
+#define SPH_WRITE(lane)                                                      \
+    do {                                                                     \
+        if (sca_phase_log && (lane) == 0) {                                  \
+            sph[kSpEnd] = __builtin_amdgcn_s_memrealtime();                  \
+            unsigned long long *sph_o = sca_phase_log +                      \
+                ((size_t)blockIdx.x * (blockDim.x / kScaWave) + threadIdx.x / kScaWave) * \
+                    kScaPhaseSlots;                                          \
+            for (int k = 0; k < kScaPhaseSlots; ++k) sph_o[k] = sph[k];      \
+        }                                                                    \
+    } while (0)
+#else
+#define SPH_DECL
+#define SPH_ADD(slot) ((void)0)
+#define SPH_COUNT(slot, v) ((void)0)
+#define SPH_WRITE(lane) ((void)0)
+#endif
+
 // Backward: gradients of value (scatter), offsets and logits.
 template <int DT, int LW>
 __global__ void __launch_bounds__(kScaBwdThreads)
@@ -620,10 +661,12 @@ sca_bwd(const ScaParams p)
     const int tid = threadIdx.x;
     const int nthreads = blockDim.x;
 
+    SPH_DECL;
     const ScaTile tl = sca_tile(p);
     const int b = tl.b;
     const int r_first = tl.qg * p.tile_pairs;   // first query rank of the tile
     sca_project_tile(p, m, b, r_first);
+    SPH_ADD(kSpProject);
 
     const ScaSlot s = sca_slot(p, m, b, r_first, tl.head, wave, lane);
     const int lph = p.lph, LP = p.LP;
@@ -668,6 +711,7 @@ sca_bwd(const ScaParams p)
     const int u0 = div_small(tid, D, p.rcp_d), ch0 = tid - u0 * D;
     const int du = div_small(nthreads, D, p.rcp_d), dch = nthreads - du * D;
     __syncthreads();
+    SPH_ADD(kSpSetup);
 
     // Chunks of lph points (lane sub owns point c0 + sub), each over the
     // cameras the tile's queries hit.  The owner keeps its point's gradients
@@ -696,6 +740,8 @@ sca_bwd(const ScaParams p)
             *reinterpret_cast<uint4 *>(mine_rec) = o;
             *reinterpret_cast<float4 *>(mine_rec + 4) = make_float4(ax, ay, aa, 0.0f);
             wave_lds_sync();
+            SPH_COUNT(kSpSteps, 1);
+            SPH_ADD(kSpRecords);
             // gradients of the point this lane owns (point c0 + sub)
             float my_da = 0.0f, my_dx = 0.0f, my_dy = 0.0f;
             for (int t = 0; t < npts; ++t) {
@@ -736,6 +782,7 @@ sca_bwd(const ScaParams p)
             g_da += my_da;
             g_dx += my_dx;
             g_dy += my_dy;
+            SPH_ADD(kSpPoint);
             // value gradient: mean * a * w * G[c] onto each in-range tap.  Each
             // wavefront puts its (point, slot, tap) rows into the table by tap
             // offset; rows on the same pixel (all slots share the head) land
@@ -791,8 +838,11 @@ sca_bwd(const ScaParams p)
                             unsafeAtomicAdd(gv + key / ES + ch, coef * m.gst[sl * D + ch]);
                     }
                 }
+                SPH_ADD(kSpInsert);
                 __syncthreads();
+                SPH_ADD(kSpInsertBarrier);
                 const int nel = (int)*tcount * D;
+                SPH_COUNT(kSpKeys, *tcount);
                 // element E = u D + ch, stepped by nthreads = du D + dch
                 int u = u0, ch = ch0;
                 for (int E = tid; E < nel; E += nthreads) {
@@ -825,13 +875,16 @@ sca_bwd(const ScaParams p)
                         ++u;
                     }
                 }
+                SPH_ADD(kSpWalk);
                 __syncthreads();
+                SPH_ADD(kSpWalkBarrier);
                 for (int h = tid; h < trows; h += nthreads) {
                     tkey[h] = kMrgEmpty;
                     thead[h] = kMrgEnd;
                 }
                 if (tid == 0) *tcount = 0u;
                 __syncthreads();
+                SPH_ADD(kSpClear);
             } else {
                 wave_lds_sync();
             }
@@ -865,6 +918,8 @@ sca_bwd(const ScaParams p)
             }
         }
     }
+    SPH_ADD(kSpTail);
+    SPH_WRITE(lane);
 }
 
 __global__ void __launch_bounds__(256) sca_zero_fill(float *dst, uint64_t n)
@@ -1317,3 +1372,10 @@ extern "C" int flashsca_backward(const flashsca_value *value, const float *lidar
     if (!fn) return FLASHBEV_ERR_UNSUPPORTED;
     return launch(fn, pl, st);
 }
+
+#ifdef FLASHBEV_PHASE_CLOCK
+extern "C" int flashsca_phase_log(void *log)
+{
+    return hipMemcpyToSymbol(HIP_SYMBOL(sca_phase_log), &log, sizeof(log)) == hipSuccess ? 0 : -1;
+}
+#endif
